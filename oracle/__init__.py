@@ -1,0 +1,21 @@
+"""CPU oracle of the MoE-layer forward pass (test infrastructure only).
+
+Only the tests, the smoke check and the benchmark's CPU-baseline leg import
+this package. The GPU path never does.
+"""
+
+from .oracle import (  # noqa: F401
+    build_oracle,
+    combine,
+    expert_rows,
+    gelu,
+    layer,
+    logits,
+    num_threads,
+    permute,
+    round_bf16,
+    route,
+    scores,
+    sigmoid,
+    topk_from_scores,
+)
