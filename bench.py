@@ -1,0 +1,228 @@
+#!/usr/bin/env python3
+"""Benchmark of the MoE-layer forward pass on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--config NAME] [--gpus 1]
+
+One step is one moe_layer_forward (route, permute, grouped routed experts,
+shared expert, combine) over a seeded synthetic batch already resident in
+HBM. Prints ONE JSON line: whole-layer tokens/s over the K timed steps, the
+roofline of the dominant kernel pair (the routed grouped GEMM, fc1 + fc2),
+per-stage times, the single-image (weight-read bound) layer, and the CPU
+oracle timed on a bounded sample of the same workload.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "MoE-layer tokens/s + % bf16 MFMA peak (large batch) / % HBM BW (1 image)"
+PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 4096 flop/clk x 2.4 GHz, dense
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--config", default="vitg_skew_bf16")
+    p.add_argument("--single-image-config", default="single_image_bf16")
+    p.add_argument("--no-single-image", action="store_true")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=15.0,
+                   help="target CPU time of the oracle sample")
+    p.add_argument("--stage-reps", type=int, default=10)
+    return p.parse_args()
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this MoE-layer build runs on one GPU only; the layer shards by tokens "
+                                   "(data parallel) or by experts, neither of which is built here",
+                          "n_gpus": args.gpus}), flush=True)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2608_17402_amd import binding
+    from workloads import get_config, make_inputs
+
+    torch.cuda.set_device(0)
+    binding.load()
+
+    def dev(a):
+        if a is None:
+            return None
+        a = np.ascontiguousarray(a)
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).cuda().view(torch.bfloat16)
+        return torch.from_numpy(a).cuda()
+
+    class Layer:
+        def __init__(self, cfg):
+            self.cfg = cfg
+            t0 = time.perf_counter()
+            inp = make_inputs(cfg)
+            self.inp = inp
+            self.desc = binding.make_desc(cfg.T, cfg.d, cfg.E, cfg.K, cfg.h, cfg.h_shared, cfg.lam, cfg.dtype)
+            self.dt = binding.torch_dtype(self.desc)
+            self.x, self.wr, self.b = dev(inp.x), dev(inp.w_router), dev(inp.bias)
+            self.w1, self.w2, self.w1s, self.w2s = dev(inp.w1), dev(inp.w2), dev(inp.w1s), dev(inp.w2s)
+            self.ws = binding.alloc_workspace(self.desc)
+            T, K, E, d = cfg.T, cfg.K, cfg.E, cfg.d
+            self.y = torch.empty(T, d, dtype=self.dt, device="cuda")
+            self.idx = torch.empty(T, K, dtype=torch.int32, device="cuda")
+            self.gate = torch.empty(T, K, dtype=torch.float32, device="cuda")
+            self.counts = torch.empty(E, dtype=torch.int32, device="cuda")
+            self.offsets = torch.empty(E + 1, dtype=torch.int32, device="cuda")
+            self.slots = torch.empty(T * K, dtype=torch.int32, device="cuda")
+            self.eout = torch.empty(T * K, d, dtype=self.dt, device="cuda")
+            self.shared = torch.empty(T, d, dtype=self.dt, device="cuda") if cfg.h_shared else None
+            torch.cuda.synchronize()
+            self.setup_s = time.perf_counter() - t0
+
+        def forward(self):
+            binding.moe_layer_forward(self.desc, self.x, self.wr, self.b, self.w1, self.w2, self.w1s, self.w2s,
+                                      self.y, self.idx, self.gate, self.ws)
+
+        def stages(self):
+            """Stage entry points, in layer order (for per-stage timing)."""
+            return {
+                "route": lambda: binding.moe_route(self.desc, self.x, self.wr, self.b, self.idx, self.gate,
+                                                   self.ws),
+                "permute": lambda: binding.moe_permute(self.desc, self.idx, self.counts, self.offsets, self.slots,
+                                                       self.ws),
+                "grouped_mlp": lambda: binding.moe_grouped_mlp(self.desc, self.x, self.slots, self.offsets,
+                                                               self.w1, self.w2, self.eout, self.ws),
+                "combine": lambda: binding.moe_combine(self.desc, self.eout, self.gate, self.shared, self.y),
+            }
+
+    def time_calls(fn, reps):
+        """Average ms per call, HIP events on the stream the kernels run on."""
+        s = torch.cuda.current_stream()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        fn()
+        torch.cuda.synchronize()
+        e0.record(s)
+        for _ in range(reps):
+            fn()
+        e1.record(s)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    cfg = get_config(args.config)
+    lay = Layer(cfg)
+    for _ in range(args.warmup):
+        lay.forward()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    wall0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        lay.forward()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms = ev0.elapsed_time(ev1) / args.steps
+    value = cfg.T / (ms * 1e-3)
+
+    # Per-stage times (the stage entry points run the same kernels).
+    stages_ms = {k: time_calls(f, args.stage_reps) for k, f in lay.stages().items()}
+    gemm_ms = stages_ms["grouped_mlp"]
+    routed_flops = 4.0 * cfg.T * cfg.K * cfg.d * cfg.h
+    achieved = routed_flops / (gemm_ms * 1e-3) / 1e12
+    roofline = {
+        "kernel": "routed grouped GEMM: fc1+GELU and fc2 kernels of one moe_grouped_mlp call",
+        "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+        "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+        "algorithmic_flops_per_launch": routed_flops, "avg_launch_us": round(gemm_ms * 1e3, 2),
+    }
+    layer_flops = cfg.gemm_flops()
+
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": cfg.dtype, "data": "synthetic",
+        "config": {"workload": cfg.name, "tokens": cfg.T, "images": cfg.images,
+                   "tokens_per_image": cfg.tokens_per_image, "d_model": cfg.d, "experts": cfg.E, "top_k": cfg.K,
+                   "expert_hidden": cfg.h, "shared_hidden": cfg.h_shared, "bias": cfg.bias},
+        "us_per_layer": round(ms * 1e3, 1),
+        "layer_gemm_tflops": round(layer_flops / (ms * 1e-3) / 1e12, 2),
+        "layer_gemm_frac_of_bf16_peak": round(layer_flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "roofline": roofline,
+        "stages_us": {k: round(v * 1e3, 1) for k, v in stages_ms.items()},
+        "timed_wall_s": round(wall, 3),
+    }
+
+    if not args.no_single_image:
+        c5 = get_config(args.single_image_config)
+        si = Layer(c5)
+        for _ in range(3):
+            si.forward()
+        si_ms = time_calls(si.forward, max(args.steps, 20))
+        si_stages = {k: time_calls(f, max(args.stage_reps, 20)) for k, f in si.stages().items()}
+        w_bytes = c5.routed_weight_bytes()
+        gbs = w_bytes / (si_stages["grouped_mlp"] * 1e-3) / 1e9
+        out["single_image"] = {
+            "workload": c5.name, "tokens": c5.T, "us_per_layer": round(si_ms * 1e3, 1),
+            "tokens_per_s": round(c5.T / (si_ms * 1e-3), 1),
+            "roofline": {"kernel": "routed grouped GEMM (fc1+fc2), expert weights read once", "bound": "hbm",
+                         "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                         "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": None,
+                         "algorithmic_bytes_per_launch": w_bytes,
+                         "avg_launch_us": round(si_stages["grouped_mlp"] * 1e3, 2)},
+            "layer_weight_gbs": round((w_bytes + c5.shared_weight_bytes()) / (si_ms * 1e-3) / 1e9, 1),
+            "stages_us": {k: round(v * 1e3, 1) for k, v in si_stages.items()},
+        }
+        del si
+
+    if not args.no_cpu_baseline:
+        import oracle
+
+        inp = lay.inp
+        f = {k: inp.f32(k) for k in ("x", "w_router", "w1", "w2", "w1s", "w2s")}
+        bf16 = cfg.dtype == "bf16"
+
+        def run(n):
+            t0 = time.perf_counter()
+            oracle.layer(f["x"][:n], f["w_router"], inp.bias, f["w1"], f["w2"], f["w1s"], f["w2s"], cfg.K,
+                         cfg.lam, bf16)
+            return time.perf_counter() - t0
+
+        n0 = 64
+        t_probe = run(n0)
+        n = int(min(cfg.T, max(n0, n0 * args.cpu_seconds / max(t_probe, 1e-6))))
+        t = run(n)
+        cpu_model = platform.processor()
+        try:
+            with open("/proc/cpuinfo") as fh:
+                for line in fh:
+                    if line.startswith("model name"):
+                        cpu_model = line.split(":", 1)[1].strip()
+                        break
+        except OSError:
+            pass
+        out["cpu_baseline"] = {
+            "value": round(n / t, 2), "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"first {n} of {cfg.T} tokens of {cfg.name}: full layer per token (route, {cfg.K} experts, "
+                      f"shared expert, combine), fp64 plain loops, {t:.1f} s",
+            "cpu_model": cpu_model, "os_cpu_count": os.cpu_count(),
+        }
+
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,152 @@
+/*
+ * moe_vie.h - C ABI of the MI355X (gfx950) forward pass of one fine-grained
+ * Mixture-of-Experts MLP layer of a ViT encoder (MoE-ViE).
+ *
+ * The layer, per token x in R^d (paper Sec. 3.1 Eq. (1)-(3), Sec. 3.2
+ * Eq. (4)-(7)):
+ *   s      = W_r x                                   router logits, E routed experts
+ *   sel    = top-K of Sigmoid(s) + b                 b only selects experts
+ *   g'_e   = Sigmoid(s_e) / sum_{i in sel} Sigmoid(s_i)     for e in sel
+ *   y      = sum_{e in sel} g'_e E_e(x) + lambda * E_shared(x)
+ *   E(x)   = W2 GELU(W1 x)                           fc1 -> exact-erf GELU -> fc2
+ * The five stages (route, permute, grouped expert MLP, combine) are exposed
+ * separately and fused in moe_layer_forward.
+ *
+ * Conventions shared by every entry point
+ *  - All tensors are row-major and live in device memory of the current HIP
+ *    device; the caller allocates and owns every buffer, the library
+ *    allocates nothing and keeps no state between calls.
+ *  - "Layer dtype" (desc->dtype) is the element type of x, all weights,
+ *    expert outputs and y: MOE_F32 (fp32) or MOE_BF16 (bf16 bit patterns,
+ *    round-to-nearest-even). Biases and gates are fp32, indices int32.
+ *  - Weights use the nn.Linear layout [out, in]: W_r [E, d], W1 [E, h, d],
+ *    W2 [E, d, h], shared W1s [h_s, d], W2s [d, h_s].
+ *  - A "slot" is one (token, choice) pair, slot id n = t*K + j, j < K.
+ *  - Every call is asynchronous on `stream` (a hipStream_t; NULL is the
+ *    default stream) and never synchronises with the host.
+ *  - Arguments are validated on the host before anything is enqueued; a call
+ *    that returns an error has enqueued nothing. Inputs must be finite.
+ *  - Pointers must be 16-byte aligned; d, h and h_s must be multiples of 64.
+ *  - Calls on one stream are ordered; calls that share output or workspace
+ *    buffers must not overlap on different streams.
+ */
+#ifndef MOE_VIE_H
+#define MOE_VIE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    MOE_OK = 0,
+    MOE_ERR_INVALID_ARG = 1, /* null pointer, bad size, misaligned pointer   */
+    MOE_ERR_UNSUPPORTED = 2, /* dtype or shape outside what is implemented  */
+    MOE_ERR_WORKSPACE = 3,   /* workspace smaller than moe_workspace_size   */
+    MOE_ERR_HIP = 4          /* a HIP runtime call or kernel launch failed  */
+} moe_status_t;
+
+typedef enum { MOE_F32 = 0, MOE_BF16 = 1 } moe_dtype_t;
+
+/* Layer descriptor. Limits: 1 <= T, T*K < 2^31; 1 <= K <= 16; K <= E <= 1024;
+ * 64 <= d <= 8192, 64 <= h <= 8192, 0 <= h_shared <= 8192 (0 = no shared
+ * expert), all multiples of 64; flags must be 0. */
+typedef struct {
+    int32_t T;        /* tokens                                   */
+    int32_t d;        /* model width                              */
+    int32_t E;        /* routed experts                           */
+    int32_t K;        /* experts chosen per token                 */
+    int32_t h;        /* hidden width of one routed expert        */
+    int32_t h_shared; /* hidden width of the shared expert, or 0  */
+    float lambda;     /* weight of the shared expert (paper: 1)   */
+    int32_t dtype;    /* moe_dtype_t                              */
+    int32_t flags;    /* reserved, must be 0                      */
+} moe_desc_t;
+
+/* Human-readable name of a status code (static string). */
+const char *moe_status_string(moe_status_t status);
+
+/* Details of the last error returned on the calling host thread (static,
+ * thread-local buffer; "" if none). */
+const char *moe_last_error(void);
+
+/* Bytes of device workspace that every entry point below needs for `desc`
+ * (one size serves all of them). Writes *bytes; validates desc. */
+moe_status_t moe_workspace_size(const moe_desc_t *desc, size_t *bytes);
+
+/* Stages 1+2: router and gating (Eq. (1), Eqs. (4)-(5), Eq. (7)).
+ *   x         [T, d] layer dtype          w_router [E, d] layer dtype
+ *   bias      [E] fp32 or NULL (= 0): added to the sigmoid score for
+ *             selection only
+ *   topk_idx  [T, K] int32 out: chosen experts, in descending selection key
+ *             (Sigmoid(s_e) + b_e); equal keys go to the lower expert index
+ *   topk_gate [T, K] fp32 out: Sigmoid(s_e) / sum of Sigmoid over the chosen
+ * Arithmetic is fp32 and reproducible bit for bit: each logit is one fused
+ * multiply-add chain over i = 0..d-1 in ascending order starting from +0;
+ * the sigmoid is 1/(1 + exp(-s)) with -s clamped to [-87, 87]
+ * and evaluated by Cody-Waite reduction with ln2 = 22713*2^-15 + fl32(ln2 -
+ * 22713*2^-15) and a degree-7 Taylor polynomial in Horner form; the gate
+ * denominator is summed in slot order. Uses the workspace (sigmoid scores). */
+moe_status_t moe_route(const moe_desc_t *desc, const void *x, const void *w_router,
+                       const float *bias, int32_t *topk_idx, float *topk_gate, void *workspace,
+                       size_t workspace_bytes, void *stream);
+
+/* Stage 3: group slots by expert (Algorithm 1, Phase 1: sort by expert id,
+ * bincount, cumulative sum).
+ *   topk_idx     [T, K] int32 in, every entry in [0, E)
+ *   counts       [E] int32 out: slots routed to each expert
+ *   offsets      [E+1] int32 out: exclusive prefix sum of counts
+ *   sorted_slots [T*K] int32 out: slot ids grouped by expert; within an
+ *                expert in ascending slot id (a stable sort)
+ * Deterministic; uses the workspace. */
+moe_status_t moe_permute(const moe_desc_t *desc, const int32_t *topk_idx, int32_t *counts,
+                         int32_t *offsets, int32_t *sorted_slots, void *workspace,
+                         size_t workspace_bytes, void *stream);
+
+/* Stage 4: grouped expert MLPs (Algorithm 1, Phases 2-3, with fc1 -> GELU ->
+ * fc2 experts and no routing weight applied).
+ *   x            [T, d] layer dtype: token rows, gathered via slot / K
+ *   sorted_slots [T*K], offsets [E+1]: as produced by moe_permute
+ *   w1 [E, h, d], w2 [E, d, h] layer dtype
+ *   expert_out   [T*K, d] layer dtype out, row n = W2[e] GELU(W1[e] x_t) for
+ *                slot n = t*K + j routed to expert e
+ * For bf16 the activation GELU(W1 x) is rounded to bf16 before fc2;
+ * accumulation is fp32. The shared expert can be run through this call with
+ * a descriptor {E = 1, K = 1, h = h_s}, sorted_slots = 0..T-1, offsets =
+ * {0, T}. Uses the workspace. */
+moe_status_t moe_grouped_mlp(const moe_desc_t *desc, const void *x, const int32_t *sorted_slots,
+                             const int32_t *offsets, const void *w1, const void *w2,
+                             void *expert_out, void *workspace, size_t workspace_bytes,
+                             void *stream);
+
+/* Stage 5: gate-weighted combine back to token order (Eq. (6)).
+ *   expert_out [T*K, d] layer dtype, topk_gate [T, K] fp32
+ *   shared_out [T, d] layer dtype or NULL: added with weight desc->lambda
+ *   y          [T, d] layer dtype out
+ * y[t] = sum_j topk_gate[t, j] * expert_out[t*K + j] + lambda * shared_out[t],
+ * accumulated in fp32 in that order (deterministic, no atomics). */
+moe_status_t moe_combine(const moe_desc_t *desc, const void *expert_out, const float *topk_gate,
+                         const void *shared_out, void *y, void *stream);
+
+/* The whole layer (Eq. (6) with routing by Eq. (7)): route, permute, grouped
+ * routed experts, shared expert (if desc->h_shared > 0) and combine, enqueued
+ * back to back on `stream` with no host synchronisation.
+ *   x [T, d], w_router [E, d], bias [E] fp32 or NULL, w1 [E, h, d],
+ *   w2 [E, d, h], w1s [h_s, d] and w2s [d, h_s] (ignored when h_s == 0)
+ *   y [T, d] layer dtype out
+ *   topk_idx_out [T, K] int32 and topk_gate_out [T, K] fp32: optional
+ *   copies of the routing (NULL = not returned)
+ * The shared expert's output stays fp32 until the combine. */
+moe_status_t moe_layer_forward(const moe_desc_t *desc, const void *x, const void *w_router,
+                               const float *bias, const void *w1, const void *w2,
+                               const void *w1s, const void *w2s, void *y, int32_t *topk_idx_out,
+                               float *topk_gate_out, void *workspace, size_t workspace_bytes,
+                               void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOE_VIE_H */

@@ -1,0 +1,329 @@
+// Host side of the C ABI declared in include/moe_vie.h: argument validation
+// (before anything is enqueued), the workspace layout, and the stream-ordered
+// kernel sequence of each entry point. No host synchronisation anywhere.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <cmath>
+
+#include "moe_internal.h"
+
+#define MOE_API extern "C" __attribute__((visibility("default")))
+
+namespace moe {
+
+int32_t permute_blocks(int64_t n_slots, int32_t E);
+int gemm_tile_bm(int32_t dtype);
+
+namespace {
+
+thread_local char g_err[512];
+
+moe_status_t fail(moe_status_t st, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+moe_status_t ok() {
+    g_err[0] = 0;
+    return MOE_OK;
+}
+
+moe_status_t hip_fail(hipError_t e, const char* where) {
+    return fail(MOE_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+bool dim_ok(int32_t v, int32_t lo) { return v >= lo && v <= 8192; }
+
+moe_status_t check_desc(const moe_desc_t* d) {
+    if (!d) return fail(MOE_ERR_INVALID_ARG, "desc is NULL");
+    if (d->dtype != MOE_F32 && d->dtype != MOE_BF16)
+        return fail(MOE_ERR_UNSUPPORTED, "dtype %d is not MOE_F32 or MOE_BF16", d->dtype);
+    if (d->flags != 0) return fail(MOE_ERR_INVALID_ARG, "flags must be 0 (got %d)", d->flags);
+    if (d->T < 1) return fail(MOE_ERR_INVALID_ARG, "T = %d must be >= 1", d->T);
+    if (d->K < 1 || d->K > kMaxK) return fail(MOE_ERR_INVALID_ARG, "K = %d must be in [1, %d]", d->K, kMaxK);
+    if (d->E < d->K || d->E > kMaxE)
+        return fail(MOE_ERR_INVALID_ARG, "E = %d must be in [K = %d, %d]", d->E, d->K, kMaxE);
+    if ((int64_t)d->T * d->K >= ((int64_t)1 << 31))
+        return fail(MOE_ERR_INVALID_ARG, "T*K = %lld must be < 2^31", (long long)d->T * d->K);
+    if (!dim_ok(d->d, 64) || !dim_ok(d->h, 64) || (d->h_shared != 0 && !dim_ok(d->h_shared, 64)))
+        return fail(MOE_ERR_INVALID_ARG, "d = %d, h = %d, h_shared = %d out of range [64, 8192]", d->d,
+                    d->h, d->h_shared);
+    if (d->d % 64 || d->h % 64 || d->h_shared % 64)
+        return fail(MOE_ERR_UNSUPPORTED, "d = %d, h = %d, h_shared = %d must be multiples of 64", d->d,
+                    d->h, d->h_shared);
+    if (!std::isfinite(d->lambda)) return fail(MOE_ERR_INVALID_ARG, "lambda is not finite");
+    return MOE_OK;
+}
+
+moe_status_t check_ptr(const void* p, const char* name, bool nullable = false) {
+    if (!p) {
+        if (nullable) return MOE_OK;
+        return fail(MOE_ERR_INVALID_ARG, "%s is NULL", name);
+    }
+    if (reinterpret_cast<uintptr_t>(p) & 15u) return fail(MOE_ERR_INVALID_ARG, "%s is not 16-byte aligned", name);
+    return MOE_OK;
+}
+
+#define CHECK(expr)                         \
+    do {                                    \
+        const moe_status_t _st = (expr);    \
+        if (_st != MOE_OK) return _st;      \
+    } while (0)
+
+#define HIP_CHECK(expr, where)                      \
+    do {                                            \
+        const hipError_t _e = (expr);               \
+        if (_e != hipSuccess) return hip_fail(_e, where); \
+    } while (0)
+
+size_t align_up(size_t v) { return (v + 255) & ~(size_t)255; }
+
+moe_status_t check_ws(const moe_desc_t& d, const void* ws, size_t bytes, WorkspacePlan* plan) {
+    *plan = plan_workspace(d);
+    if (!ws) return fail(MOE_ERR_WORKSPACE, "workspace is NULL (need %zu bytes)", plan->total);
+    if (reinterpret_cast<uintptr_t>(ws) & 255u)
+        return fail(MOE_ERR_INVALID_ARG, "workspace is not 256-byte aligned");
+    if (bytes < plan->total)
+        return fail(MOE_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", bytes, plan->total);
+    return MOE_OK;
+}
+
+template <typename T>
+T* region(void* ws, size_t off) {
+    return reinterpret_cast<T*>(static_cast<uint8_t*>(ws) + off);
+}
+
+}  // namespace
+
+size_t elem_size(int32_t dtype) { return dtype == MOE_BF16 ? 2 : 4; }
+
+int choose_tile_bm(const moe_desc_t& d) { return gemm_tile_bm(d.dtype); }
+
+WorkspacePlan plan_workspace(const moe_desc_t& d) {
+    WorkspacePlan p;
+    const size_t es = elem_size(d.dtype);
+    const size_t TK = (size_t)d.T * d.K;
+    p.n_hist_blocks = permute_blocks((int64_t)TK, d.E);
+    p.tile_bm = choose_tile_bm(d);
+    const size_t busy = TK < (size_t)d.E ? TK : (size_t)d.E;  // experts that can hold a slot
+    p.max_tiles = (int32_t)((TK + busy * (p.tile_bm - 1)) / p.tile_bm);
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t o = off;
+        off = align_up(off + bytes);
+        return o;
+    };
+    p.idx = take(TK * 4);
+    p.gate = take(TK * 4);
+    p.scores = take((size_t)d.T * d.E * 4);
+    p.counts = take((size_t)d.E * 4);
+    p.offsets = take((size_t)(d.E + 1) * 4);
+    p.slots = take(TK * 4);
+    p.blockhist = take((size_t)p.n_hist_blocks * d.E * 4);
+    p.tiles = take((size_t)p.max_tiles * sizeof(TileDesc));
+    p.ntiles = take(16);
+    p.act = take(TK * d.h * es);
+    p.eout = take(TK * d.d * es);
+    p.sact = take((size_t)d.T * d.h_shared * es);
+    p.sout = take(d.h_shared ? (size_t)d.T * d.d * 4 : 0);
+    p.total = off;
+    return p;
+}
+
+// Routed experts: fc1 + GELU into the activation buffer (sorted order), then
+// fc2 scattered to slot order.
+static moe_status_t enqueue_routed_mlp(const moe_desc_t& d, const WorkspacePlan& p, void* ws, const void* x,
+                                       const int32_t* sorted_slots, const int32_t* offsets, const void* w1,
+                                       const void* w2, void* expert_out, hipStream_t s) {
+    TileDesc* tiles = region<TileDesc>(ws, p.tiles);
+    int32_t* ntiles = region<int32_t>(ws, p.ntiles);
+    HIP_CHECK(launch_build_tiles(d.E, p.tile_bm, p.max_tiles, offsets, tiles, ntiles, s), "build_tiles");
+    GemmArgs g{};
+    g.A = x;
+    g.B = w1;
+    g.C = region<void>(ws, p.act);
+    g.row_map = sorted_slots;
+    g.tiles = tiles;
+    g.n_tiles = ntiles;
+    g.N = d.h;
+    g.Kdim = d.d;
+    g.route_k = d.K;
+    g.row_mode = ROWS_GATHER_TOKENS;
+    g.max_tiles = p.max_tiles;
+    g.b_group_stride = (int64_t)d.h * d.d;
+    HIP_CHECK(launch_gemm(d, EPI_GELU_STORE, p.tile_bm, g, s), "fc1 grouped gemm");
+    GemmArgs g2 = g;
+    g2.A = region<void>(ws, p.act);
+    g2.B = w2;
+    g2.C = expert_out;
+    g2.N = d.d;
+    g2.Kdim = d.h;
+    g2.row_mode = ROWS_IDENTITY;
+    g2.b_group_stride = (int64_t)d.d * d.h;
+    HIP_CHECK(launch_gemm(d, EPI_SCATTER_SLOT, p.tile_bm, g2, s), "fc2 grouped gemm");
+    return MOE_OK;
+}
+
+// Shared expert over all T tokens in token order; fp32 output.
+static moe_status_t enqueue_shared_mlp(const moe_desc_t& d, const WorkspacePlan& p, void* ws, const void* x,
+                                       const void* w1s, const void* w2s, float* out, hipStream_t s) {
+    GemmArgs g{};
+    g.A = x;
+    g.B = w1s;
+    g.C = region<void>(ws, p.sact);
+    g.dense_rows = d.T;
+    g.N = d.h_shared;
+    g.Kdim = d.d;
+    g.route_k = 1;
+    g.row_mode = ROWS_IDENTITY;
+    g.max_tiles = (d.T + p.tile_bm - 1) / p.tile_bm;
+    HIP_CHECK(launch_gemm(d, EPI_GELU_STORE, p.tile_bm, g, s), "shared fc1 gemm");
+    GemmArgs g2 = g;
+    g2.A = region<void>(ws, p.sact);
+    g2.B = w2s;
+    g2.C = out;
+    g2.N = d.d;
+    g2.Kdim = d.h_shared;
+    HIP_CHECK(launch_gemm(d, EPI_STORE_F32, p.tile_bm, g2, s), "shared fc2 gemm");
+    return MOE_OK;
+}
+
+}  // namespace moe
+
+using namespace moe;
+
+MOE_API const char* moe_status_string(moe_status_t st) {
+    switch (st) {
+        case MOE_OK: return "MOE_OK";
+        case MOE_ERR_INVALID_ARG: return "MOE_ERR_INVALID_ARG";
+        case MOE_ERR_UNSUPPORTED: return "MOE_ERR_UNSUPPORTED";
+        case MOE_ERR_WORKSPACE: return "MOE_ERR_WORKSPACE";
+        case MOE_ERR_HIP: return "MOE_ERR_HIP";
+    }
+    return "MOE_ERR_UNKNOWN";
+}
+
+MOE_API const char* moe_last_error(void) { return g_err; }
+
+MOE_API moe_status_t moe_workspace_size(const moe_desc_t* desc, size_t* bytes) {
+    CHECK(check_desc(desc));
+    if (!bytes) return fail(MOE_ERR_INVALID_ARG, "bytes is NULL");
+    *bytes = plan_workspace(*desc).total;
+    return ok();
+}
+
+MOE_API moe_status_t moe_route(const moe_desc_t* desc, const void* x, const void* w_router, const float* bias,
+                               int32_t* topk_idx, float* topk_gate, void* workspace, size_t workspace_bytes,
+                               void* stream) {
+    CHECK(check_desc(desc));
+    CHECK(check_ptr(x, "x"));
+    CHECK(check_ptr(w_router, "w_router"));
+    CHECK(check_ptr(bias, "bias", true));
+    CHECK(check_ptr(topk_idx, "topk_idx"));
+    CHECK(check_ptr(topk_gate, "topk_gate"));
+    WorkspacePlan p;
+    CHECK(check_ws(*desc, workspace, workspace_bytes, &p));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    (void)hipGetLastError();
+    float* scores = region<float>(workspace, p.scores);
+    HIP_CHECK(launch_router_scores(*desc, x, w_router, scores, s), "router scores");
+    HIP_CHECK(launch_topk(*desc, scores, bias, topk_idx, topk_gate, s), "top-k");
+    return ok();
+}
+
+MOE_API moe_status_t moe_permute(const moe_desc_t* desc, const int32_t* topk_idx, int32_t* counts,
+                                 int32_t* offsets, int32_t* sorted_slots, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+    CHECK(check_desc(desc));
+    CHECK(check_ptr(topk_idx, "topk_idx"));
+    CHECK(check_ptr(counts, "counts"));
+    CHECK(check_ptr(offsets, "offsets"));
+    CHECK(check_ptr(sorted_slots, "sorted_slots"));
+    WorkspacePlan p;
+    CHECK(check_ws(*desc, workspace, workspace_bytes, &p));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    (void)hipGetLastError();
+    HIP_CHECK(launch_permute(*desc, topk_idx, counts, offsets, sorted_slots, region<int32_t>(workspace, p.blockhist),
+                             p.n_hist_blocks, s),
+              "permute");
+    return ok();
+}
+
+MOE_API moe_status_t moe_grouped_mlp(const moe_desc_t* desc, const void* x, const int32_t* sorted_slots,
+                                     const int32_t* offsets, const void* w1, const void* w2, void* expert_out,
+                                     void* workspace, size_t workspace_bytes, void* stream) {
+    CHECK(check_desc(desc));
+    CHECK(check_ptr(x, "x"));
+    CHECK(check_ptr(sorted_slots, "sorted_slots"));
+    CHECK(check_ptr(offsets, "offsets"));
+    CHECK(check_ptr(w1, "w1"));
+    CHECK(check_ptr(w2, "w2"));
+    CHECK(check_ptr(expert_out, "expert_out"));
+    WorkspacePlan p;
+    CHECK(check_ws(*desc, workspace, workspace_bytes, &p));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    (void)hipGetLastError();
+    CHECK(enqueue_routed_mlp(*desc, p, workspace, x, sorted_slots, offsets, w1, w2, expert_out, s));
+    return ok();
+}
+
+MOE_API moe_status_t moe_combine(const moe_desc_t* desc, const void* expert_out, const float* topk_gate,
+                                 const void* shared_out, void* y, void* stream) {
+    CHECK(check_desc(desc));
+    CHECK(check_ptr(expert_out, "expert_out"));
+    CHECK(check_ptr(topk_gate, "topk_gate"));
+    CHECK(check_ptr(shared_out, "shared_out", true));
+    CHECK(check_ptr(y, "y"));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    (void)hipGetLastError();
+    HIP_CHECK(launch_combine(*desc, expert_out, topk_gate, shared_out, desc->dtype == MOE_F32, y, s), "combine");
+    return ok();
+}
+
+MOE_API moe_status_t moe_layer_forward(const moe_desc_t* desc, const void* x, const void* w_router,
+                                       const float* bias, const void* w1, const void* w2, const void* w1s,
+                                       const void* w2s, void* y, int32_t* topk_idx_out, float* topk_gate_out,
+                                       void* workspace, size_t workspace_bytes, void* stream) {
+    CHECK(check_desc(desc));
+    const moe_desc_t& d = *desc;
+    CHECK(check_ptr(x, "x"));
+    CHECK(check_ptr(w_router, "w_router"));
+    CHECK(check_ptr(bias, "bias", true));
+    CHECK(check_ptr(w1, "w1"));
+    CHECK(check_ptr(w2, "w2"));
+    if (d.h_shared > 0) {
+        CHECK(check_ptr(w1s, "w1s"));
+        CHECK(check_ptr(w2s, "w2s"));
+    }
+    CHECK(check_ptr(y, "y"));
+    CHECK(check_ptr(topk_idx_out, "topk_idx_out", true));
+    CHECK(check_ptr(topk_gate_out, "topk_gate_out", true));
+    WorkspacePlan p;
+    CHECK(check_ws(d, workspace, workspace_bytes, &p));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    (void)hipGetLastError();
+
+    int32_t* idx = topk_idx_out ? topk_idx_out : region<int32_t>(workspace, p.idx);
+    float* gate = topk_gate_out ? topk_gate_out : region<float>(workspace, p.gate);
+    float* scores = region<float>(workspace, p.scores);
+    int32_t* counts = region<int32_t>(workspace, p.counts);
+    int32_t* offsets = region<int32_t>(workspace, p.offsets);
+    int32_t* slots = region<int32_t>(workspace, p.slots);
+    void* eout = region<void>(workspace, p.eout);
+    float* sout = d.h_shared ? region<float>(workspace, p.sout) : nullptr;
+
+    HIP_CHECK(launch_router_scores(d, x, w_router, scores, s), "router scores");
+    HIP_CHECK(launch_topk(d, scores, bias, idx, gate, s), "top-k");
+    HIP_CHECK(launch_permute(d, idx, counts, offsets, slots, region<int32_t>(workspace, p.blockhist),
+                             p.n_hist_blocks, s),
+              "permute");
+    CHECK(enqueue_routed_mlp(d, p, workspace, x, slots, offsets, w1, w2, eout, s));
+    if (d.h_shared) CHECK(enqueue_shared_mlp(d, p, workspace, x, w1s, w2s, sout, s));
+    HIP_CHECK(launch_combine(d, eout, gate, sout, 1, y, s), "combine");
+    return ok();
+}

@@ -1,0 +1,87 @@
+// Internal declarations shared by the HIP translation units of the MoE-layer
+// library: element types, the workspace plan, tile tables and the kernel
+// launchers. Nothing here is part of the public C ABI (include/moe_vie.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "moe_vie.h"
+
+namespace moe {
+
+// bf16 is carried as raw 16-bit patterns in memory.
+typedef uint16_t bf16_t;
+
+constexpr int kWave = 64;          // CDNA wavefront width
+constexpr int kNumXcd = 8;         // MI355X: 8 accelerator complex dies, 32 CUs each
+constexpr int kMaxE = 1024;
+constexpr int kMaxK = 16;
+
+// One M-tile of a grouped GEMM: `rows` rows (<= BM) of expert `e`, starting
+// at sorted position `row0` (rows of one expert are contiguous).
+struct TileDesc {
+    int32_t e;
+    int32_t row0;
+    int32_t rows;
+    int32_t pad;
+};
+
+// How the GEMM kernels find the A rows and where the output rows go.
+enum GemmRowMode : int {
+    ROWS_GATHER_TOKENS = 0,  // A row of sorted position p is x[sorted_slots[p] / K]
+    ROWS_IDENTITY = 1,       // A row of position p is row p
+};
+
+enum GemmEpilogue : int {
+    EPI_GELU_STORE = 0,     // C[p, :] = act(GELU(acc)) at the sorted position p
+    EPI_SCATTER_SLOT = 1,   // C[sorted_slots[p], :] = acc  (expert_out in slot order)
+    EPI_STORE_F32 = 2,      // C[p, :] = acc as fp32 (shared expert output)
+};
+
+struct GemmArgs {
+    const void* A;             // rows of length Kdim (layer dtype)
+    const void* B;             // weights [groups][N][Kdim] (layer dtype)
+    void* C;                   // output rows of length N
+    const int32_t* row_map;    // sorted_slots (gather / scatter), may be null for identity
+    const TileDesc* tiles;     // grouped mode: tile table
+    const int32_t* n_tiles;    // grouped mode: device-side tile count
+    int32_t dense_rows;        // dense mode (tiles == null): M rows in one group
+    int32_t N;
+    int32_t Kdim;
+    int32_t route_k;           // K of the routing (slot -> token = slot / route_k)
+    int32_t row_mode;          // GemmRowMode
+    int32_t max_tiles;         // upper bound on the number of M-tiles (grid sizing)
+    int64_t b_group_stride;    // elements between consecutive experts' weights
+};
+
+// Offsets (bytes) of every workspace region for one descriptor.
+struct WorkspacePlan {
+    size_t idx, gate, scores, counts, offsets, slots, blockhist, tiles, ntiles;
+    size_t act, eout, sact, sout;
+    size_t total;
+    int32_t n_hist_blocks;   // blocks of the permute histogram / scatter
+    int32_t tile_bm;         // M-tile height of the routed grouped GEMM
+    int32_t max_tiles;       // upper bound on routed M-tiles
+};
+
+size_t elem_size(int32_t dtype);
+WorkspacePlan plan_workspace(const moe_desc_t& d);
+int choose_tile_bm(const moe_desc_t& d);
+
+// ---- launchers (each returns the first HIP error, hipSuccess otherwise)
+hipError_t launch_router_scores(const moe_desc_t& d, const void* x, const void* w_router,
+                                float* scores, hipStream_t s);
+hipError_t launch_topk(const moe_desc_t& d, const float* scores, const float* bias,
+                       int32_t* topk_idx, float* topk_gate, hipStream_t s);
+hipError_t launch_permute(const moe_desc_t& d, const int32_t* topk_idx, int32_t* counts,
+                          int32_t* offsets, int32_t* sorted_slots, int32_t* blockhist,
+                          int32_t n_blocks, hipStream_t s);
+hipError_t launch_build_tiles(int32_t E, int32_t bm, int32_t max_tiles, const int32_t* offsets,
+                              TileDesc* tiles, int32_t* n_tiles, hipStream_t s);
+hipError_t launch_gemm(const moe_desc_t& d, int epilogue, int bm, const GemmArgs& a, hipStream_t s);
+hipError_t launch_combine(const moe_desc_t& d, const void* expert_out, const float* gate,
+                          const void* shared, int shared_is_f32, void* y, hipStream_t s);
+
+}  // namespace moe

@@ -1,0 +1,102 @@
+"""The C ABI library on the CPU: it loads, exports every entry point that
+include/moe_vie.h declares, and rejects bad arguments on the host (before any
+HIP call, so these run without a GPU)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_17402_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "moe_vie.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+char\s*\*|moe_status_t|size_t)\s*(moe_\w+)\s*\(", text, re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(binding.LIB_PATH):
+        pytest.fail("libmoevie.so is not built (run __graft_entry__.build())")
+    return binding.load()
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ("moe_route", "moe_permute", "moe_grouped_mlp", "moe_combine", "moe_layer_forward",
+              "moe_workspace_size", "moe_status_string", "moe_last_error"):
+        assert n in names
+    assert set(names) == set(binding.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), f"{name} is declared but not exported"
+
+
+def test_status_strings(lib):
+    assert lib.moe_status_string(0) == b"MOE_OK"
+    assert lib.moe_status_string(3) == b"MOE_ERR_WORKSPACE"
+    assert lib.moe_status_string(99) == b"MOE_ERR_UNKNOWN"
+
+
+def _ws(desc):
+    n = ctypes.c_size_t(0)
+    st = binding.load().moe_workspace_size(ctypes.byref(desc), ctypes.byref(n))
+    return st, n.value
+
+
+def test_workspace_size_and_desc_validation(lib):
+    st, n = _ws(binding.make_desc(196, 256, 8, 2, 256, 0, 1.0, "f32"))
+    assert st == 0 and n > 196 * 2 * 256 * 4 * 2
+    st4, n4 = _ws(binding.make_desc(65536, 1536, 256, 8, 768, 1536, 1.0, "bf16"))
+    assert st4 == 0
+    # activation + expert outputs (bf16) + shared output (fp32) at least
+    assert n4 >= 65536 * 8 * (768 + 1536) * 2 + 65536 * 1536 * 4
+    bad = {
+        "K=0": (binding.make_desc(10, 64, 8, 0, 64), 1),
+        "K>16": (binding.make_desc(10, 64, 32, 17, 64), 1),
+        "E<K": (binding.make_desc(10, 64, 2, 4, 64), 1),
+        "E>1024": (binding.make_desc(10, 64, 1025, 4, 64), 1),
+        "T=0": (binding.make_desc(0, 64, 8, 2, 64), 1),
+        "d%64": (binding.make_desc(10, 96, 8, 2, 64), 2),
+        "h%64": (binding.make_desc(10, 64, 8, 2, 100), 2),
+        "hs%64": (binding.make_desc(10, 64, 8, 2, 64, 65), 2),
+        "d>8192": (binding.make_desc(10, 8256, 8, 2, 64), 1),
+        "dtype": (binding.make_desc(10, 64, 8, 2, 64, 0, 1.0, 7), 2),
+        "flags": (binding.make_desc(10, 64, 8, 2, 64, 0, 1.0, "bf16", flags=1), 1),
+        "lambda": (binding.make_desc(10, 64, 8, 2, 64, 0, float("nan")), 1),
+        "T*K": (binding.make_desc(2 ** 28, 64, 16, 8, 64), 1),
+    }
+    for name, (desc, want) in bad.items():
+        st, _ = _ws(desc)
+        assert st == want, name
+        assert lib.moe_last_error() != b""
+
+
+def test_entry_points_reject_bad_pointers_before_any_launch(lib):
+    desc = binding.make_desc(100, 64, 8, 2, 64, 64, 1.0, "bf16")
+    _, need = _ws(desc)
+    P = ctypes.c_void_p
+    fake = P(1 << 20)  # 16-byte aligned, never dereferenced: validation fails first
+    mis = P((1 << 20) + 4)
+    S = ctypes.c_size_t
+    d = ctypes.byref(desc)
+    assert lib.moe_route(d, None, fake, None, fake, fake, fake, S(need), None) == 1
+    assert b"x is NULL" in lib.moe_last_error()
+    assert lib.moe_route(d, mis, fake, None, fake, fake, fake, S(need), None) == 1
+    assert b"aligned" in lib.moe_last_error()
+    assert lib.moe_route(d, fake, fake, None, fake, fake, fake, S(need - 1), None) == 3
+    assert lib.moe_permute(d, fake, fake, fake, fake, None, S(0), None) == 3
+    assert lib.moe_grouped_mlp(d, fake, fake, fake, fake, None, fake, fake, S(need), None) == 1
+    assert lib.moe_combine(d, fake, None, None, fake, None) == 1
+    assert lib.moe_layer_forward(d, fake, fake, None, fake, fake, None, fake, fake, None, None, fake,
+                                 S(need), None) == 1  # shared weights required when h_shared > 0
+    bad = binding.make_desc(100, 64, 8, 0, 64)
+    assert lib.moe_layer_forward(ctypes.byref(bad), fake, fake, None, fake, fake, None, None, fake, None,
+                                 None, fake, S(need), None) == 1

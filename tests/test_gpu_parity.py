@@ -1,0 +1,263 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Routing (indices, gates) and permutation are compared bit for bit; expert
+outputs and the layer output within max-abs 2e-2 / rel-L2 5e-3 (bf16) or
+1e-5 / 1e-5 (fp32). Reduced-token variants of every layer shape run the
+oracle over every token (several tiles per expert plus ragged tails); the
+full-size shapes compare the whole routing and sampled tokens of the layer.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import DeviceLayer, check_close, dev, desc_for, host
+from paper_2608_17402_amd import binding
+from workloads import get_config, make_inputs
+
+pytestmark = pytest.mark.gpu
+
+# (config, tokens) small enough for the oracle over every token.
+SMALL = [("c1", None), ("c2", 1000), ("c3", 700), ("c4", 600), ("c5", None)]
+
+
+def small_id(c):
+    return f"{c[0]}-T{c[1] or 'full'}"
+
+
+def _layer(name, T):
+    cfg = get_config(name)
+    if T is not None:
+        cfg = cfg.with_tokens(T)
+    return cfg, make_inputs(cfg)
+
+
+@pytest.fixture(scope="module", params=SMALL, ids=small_id)
+def small(request):
+    name, T = request.param
+    cfg, inp = _layer(name, T)
+    lay = DeviceLayer(inp)
+    bf16 = cfg.dtype == "bf16"
+    ref_idx, ref_gate = oracle.route(inp.f32("x"), inp.f32("w_router"), inp.bias, cfg.K)
+    return cfg, inp, lay, bf16, ref_idx, ref_gate
+
+
+def test_route_bit_exact(small):
+    cfg, inp, lay, _, ref_idx, ref_gate = small
+    idx, gate = lay.route()
+    torch.cuda.synchronize()
+    assert np.array_equal(host(idx), ref_idx)
+    assert np.array_equal(host(gate), ref_gate)
+    g = host(gate).astype(np.float64)
+    assert np.max(np.abs(g.sum(1) - 1.0)) <= cfg.K * 2.0 ** -23
+
+
+def test_permute_exact(small):
+    cfg, inp, lay, _, ref_idx, _ = small
+    counts, offsets, slots = lay.permute(dev(ref_idx))
+    torch.cuda.synchronize()
+    rc, ro, rs = oracle.permute(ref_idx, cfg.E)
+    assert np.array_equal(host(counts), rc)
+    assert np.array_equal(host(offsets), ro)
+    assert np.array_equal(host(slots), rs)
+
+
+def test_grouped_mlp(small):
+    cfg, inp, lay, bf16, ref_idx, _ = small
+    _, ro, rs = oracle.permute(ref_idx, cfg.E)
+    eo = host(lay.grouped_mlp(dev(rs), dev(ro)))
+    x = inp.f32("x")
+    w1, w2 = inp.f32("w1"), inp.f32("w2")
+    ref = np.zeros((cfg.T * cfg.K, cfg.d))
+    for e in range(cfg.E):
+        seg = rs[ro[e]:ro[e + 1]]
+        if seg.size:
+            ref[seg] = oracle.expert_rows(x[seg // cfg.K], w1[e], w2[e], bf16)
+    check_close(eo, ref, bf16, "expert_out")
+
+
+def test_combine(small):
+    cfg, inp, lay, bf16, ref_idx, ref_gate = small
+    rng = np.random.default_rng(7)
+    eo = (rng.standard_normal((cfg.T * cfg.K, cfg.d)) * 0.3).astype(np.float32)
+    sh = (rng.standard_normal((cfg.T, cfg.d)) * 0.3).astype(np.float32)
+    if bf16:
+        from workloads import bf16_bits_to_f32, f32_to_bf16_bits
+
+        eo_b, sh_b = f32_to_bf16_bits(eo), f32_to_bf16_bits(sh)
+        eo, sh = bf16_bits_to_f32(eo_b), bf16_bits_to_f32(sh_b)
+        eo_d, sh_d = dev(eo_b), dev(sh_b)
+    else:
+        eo_d, sh_d = dev(eo), dev(sh)
+    y = lay.empty(cfg.T, cfg.d)
+    binding.moe_combine(lay.desc, eo_d, dev(ref_gate), sh_d, y)
+    check_close(host(y), oracle.combine(eo, ref_gate, sh, cfg.lam), bf16, "combine")
+    y2 = lay.empty(cfg.T, cfg.d)
+    binding.moe_combine(lay.desc, eo_d, dev(ref_gate), None, y2)
+    check_close(host(y2), oracle.combine(eo, ref_gate, None, cfg.lam), bf16, "combine without shared")
+
+
+def test_layer_forward(small):
+    cfg, inp, lay, bf16, ref_idx, ref_gate = small
+    y, idx, gate = lay.forward()
+    torch.cuda.synchronize()
+    assert np.array_equal(host(idx), ref_idx) and np.array_equal(host(gate), ref_gate)
+    o_idx, o_gate, y_ref = oracle.layer(inp.f32("x"), inp.f32("w_router"), inp.bias, inp.f32("w1"),
+                                        inp.f32("w2"), inp.f32("w1s"), inp.f32("w2s"), cfg.K, cfg.lam, bf16)
+    assert np.array_equal(o_idx, ref_idx)
+    check_close(host(y), y_ref, bf16, "layer y")
+
+
+def test_layer_deterministic(small):
+    _, _, lay, _, _, _ = small
+    y1, i1, g1 = lay.forward()
+    y2, i2, g2 = lay.forward(with_routing=False)
+    torch.cuda.synchronize()
+    assert torch.equal(y1.view(torch.int16) if y1.dtype == torch.bfloat16 else y1,
+                       y2.view(torch.int16) if y2.dtype == torch.bfloat16 else y2)
+
+
+def test_layer_token_permutation_equivariance(small):
+    cfg, inp, lay, _, _, _ = small
+    y, _, _ = lay.forward()
+    perm = np.random.default_rng(3).permutation(cfg.T)
+    inp_p = make_inputs(cfg)
+    inp_p.x = inp.x[perm]
+    lay_p = DeviceLayer(inp_p)
+    y_p, _, _ = lay_p.forward()
+    torch.cuda.synchronize()
+    a = host(y)[perm]
+    b = host(y_p)
+    assert np.array_equal(a, b)
+
+
+# ------------------------------------------------------------------ edge cases
+
+
+def _synthetic(T, d, E, K, h, hs, dtype, seed, bias=None):
+    from workloads.configs import LayerConfig
+
+    cfg = LayerConfig(name=f"edge{seed}", T=T, d=d, E=E, K=K, h=h, h_shared=hs, dtype=dtype, bias="uniform",
+                      seed=seed)
+    inp = make_inputs(cfg)
+    if bias is not None:
+        inp.bias = np.asarray(bias, np.float32)
+    return cfg, inp
+
+
+EDGE = {
+    "one_token": dict(T=1, d=64, E=8, K=2, h=64, hs=64, dtype="bf16"),
+    "k_equals_e": dict(T=77, d=128, E=8, K=8, h=64, hs=0, dtype="bf16"),
+    "single_expert": dict(T=130, d=64, E=1, K=1, h=128, hs=64, dtype="bf16"),
+    "k16_e1024": dict(T=50, d=64, E=1024, K=16, h=64, hs=0, dtype="bf16"),
+    "f32_ragged": dict(T=131, d=192, E=5, K=3, h=320, hs=128, dtype="f32"),
+    "wide_h_odd_tiles": dict(T=257, d=320, E=6, K=2, h=448, hs=192, dtype="bf16"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(EDGE))
+def test_edge_layer(name):
+    p = EDGE[name]
+    cfg, inp = _synthetic(p["T"], p["d"], p["E"], p["K"], p["h"], p["hs"], p["dtype"], seed=len(name))
+    lay = DeviceLayer(inp)
+    y, idx, gate = lay.forward()
+    bf16 = cfg.dtype == "bf16"
+    o_idx, o_gate, y_ref = oracle.layer(inp.f32("x"), inp.f32("w_router"), inp.bias, inp.f32("w1"),
+                                        inp.f32("w2"), inp.f32("w1s"), inp.f32("w2s"), cfg.K, cfg.lam, bf16)
+    assert np.array_equal(host(idx), o_idx) and np.array_equal(host(gate), o_gate)
+    check_close(host(y), y_ref, bf16, name)
+
+
+def test_skew_all_tokens_to_few_experts():
+    # Bias +2 forces every token onto experts {1, 5}; every other expert is empty.
+    E = 16
+    bias = np.zeros(E, np.float32)
+    bias[[1, 5]] = 2.0
+    cfg, inp = _synthetic(300, 128, E, 2, 128, 0, "bf16", seed=11, bias=bias)
+    lay = DeviceLayer(inp)
+    y, idx, gate = lay.forward()
+    counts, offsets, _ = lay.permute(idx)
+    torch.cuda.synchronize()
+    assert sorted(set(host(idx).reshape(-1).tolist())) == [1, 5]
+    c = host(counts)
+    assert c[1] == c[5] == 300 and c.sum() == 600
+    o_idx, _, y_ref = oracle.layer(inp.f32("x"), inp.f32("w_router"), inp.bias, inp.f32("w1"), inp.f32("w2"),
+                                   None, None, cfg.K, cfg.lam, True)
+    assert np.array_equal(host(idx), o_idx)
+    check_close(host(y), y_ref, True, "forced skew")
+
+
+def test_shared_expert_through_grouped_mlp():
+    # The shared expert as a grouped MLP with one group of every token.
+    cfg, inp = _synthetic(200, 128, 4, 2, 128, 192, "bf16", seed=12)
+    d1 = desc_for(cfg, E=1, K=1, h=cfg.h_shared, h_shared=0)
+    ws = binding.alloc_workspace(d1)
+    slots = torch.arange(cfg.T, dtype=torch.int32, device="cuda")
+    offs = torch.tensor([0, cfg.T], dtype=torch.int32, device="cuda")
+    out = torch.empty(cfg.T, cfg.d, dtype=torch.bfloat16, device="cuda")
+    binding.moe_grouped_mlp(d1, dev(inp.x), slots, offs, dev(inp.w1s)[None], dev(inp.w2s)[None], out, ws)
+    ref = oracle.expert_rows(inp.f32("x"), inp.f32("w1s"), inp.f32("w2s"), True)
+    check_close(host(out), ref, True, "shared via grouped")
+
+
+def test_permute_with_empty_and_full_experts():
+    T, E, K = 5000, 64, 4
+    rng = np.random.default_rng(5)
+    # experts 0..3 take most slots, 40..63 none; distinct experts per token
+    idx = np.stack([rng.choice(40, K, replace=False, p=np.r_[np.full(4, 0.2), np.full(36, 0.2 / 36)])
+                    for _ in range(T)]).astype(np.int32)
+    d = binding.make_desc(T, 64, E, K, 64)
+    ws = binding.alloc_workspace(d)
+    counts = torch.empty(E, dtype=torch.int32, device="cuda")
+    offsets = torch.empty(E + 1, dtype=torch.int32, device="cuda")
+    slots = torch.empty(T * K, dtype=torch.int32, device="cuda")
+    binding.moe_permute(d, dev(idx), counts, offsets, slots, ws)
+    rc, ro, rs = oracle.permute(idx, E)
+    assert np.array_equal(host(counts), rc) and np.array_equal(host(offsets), ro)
+    assert np.array_equal(host(slots), rs)
+
+
+def test_errors_raise_and_enqueue_nothing():
+    cfg, inp = _synthetic(10, 64, 4, 2, 64, 0, "bf16", seed=13)
+    lay = DeviceLayer(inp)
+    y = lay.empty(cfg.T, cfg.d)
+    small_ws = torch.empty(256, dtype=torch.uint8, device="cuda")
+    with pytest.raises(binding.MoeError) as e:
+        binding.moe_layer_forward(lay.desc, lay.x, lay.w_router, lay.bias, lay.w1, lay.w2, None, None, y,
+                                  workspace=small_ws)
+    assert e.value.status == 3
+
+
+# ------------------------------------------------------------- full-size runs
+
+FULL = ["c2", "c3", "c4", "c5"]
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name", FULL)
+def test_full_size_route_and_sampled_layer(name):
+    cfg = get_config(name)
+    inp = make_inputs(cfg)
+    lay = DeviceLayer(inp)
+    y, idx, gate = lay.forward()
+    torch.cuda.synchronize()
+    x, wr = inp.f32("x"), inp.f32("w_router")
+    ref_idx, ref_gate = oracle.route(x, wr, inp.bias, cfg.K)
+    gi, gg = host(idx), host(gate)
+    n_bad = int((gi != ref_idx).any(1).sum())
+    assert n_bad == 0, f"{n_bad} tokens routed differently"
+    assert np.array_equal(gg, ref_gate)
+    counts, offsets, slots = lay.permute(idx)
+    rc, ro, rs = oracle.permute(ref_idx, cfg.E)
+    assert np.array_equal(host(counts), rc) and np.array_equal(host(slots), rs)
+    rng = np.random.default_rng(0)
+    tok = np.unique(np.r_[0, cfg.T - 1, rng.choice(cfg.T, 46, replace=False)]).astype(np.int32)
+    if name == "c4":  # include tokens routed to the rarest experts
+        rare = np.argsort(rc)[:4]
+        hits = [int(rs[ro[e]]) // cfg.K for e in rare if rc[e] > 0]
+        tok = np.unique(np.r_[tok, hits]).astype(np.int32)
+    o_idx, _, y_ref = oracle.layer(x, wr, inp.bias, inp.f32("w1"), inp.f32("w2"), inp.f32("w1s"),
+                                   inp.f32("w2s"), cfg.K, cfg.lam, True, tokens=tok)
+    assert np.array_equal(o_idx, ref_idx[tok])
+    check_close(host(y)[tok], y_ref, True, f"{name} sampled y")
