@@ -28,7 +28,6 @@ namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ bf16_t f32_to_bf16_rne(float f) {
     uint32_t u = __float_as_uint(f);
@@ -77,20 +76,120 @@ __device__ __forceinline__ TileCoord locate_tile(const GemmArgs& a, int bm, int 
     return tc;
 }
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, int EPI, bool GROUPED>
-__global__ __launch_bounds__(WAVES_M* WAVES_N* kWave) void k_gemm_bf16(const GemmArgs a) {
-    constexpr int NT = WAVES_M * WAVES_N * kWave;
-    constexpr int BK = 64;             // K slab: 64 bf16 = 128 bytes = 8 chunks per row
+// GELU for the bf16 path: 0.5 x (1 + erf(x / sqrt 2)) with erf from
+// Abramowitz & Stegun 7.1.26 (|error| <= 1.5e-7, far below the bf16 rounding
+// of the activation), built from the hardware reciprocal and exp2.
+__device__ __forceinline__ float gelu_as(float x) {
+    const float z = x * 0.70710678118654752f;
+    const float az = fabsf(z);
+    const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, az, 1.0f));
+    float p = fmaf(1.061405429f, t, -1.453152027f);
+    p = fmaf(p, t, 1.421413741f);
+    p = fmaf(p, t, -0.284496736f);
+    p = fmaf(p, t, 0.254829592f);
+    p *= t;
+    const float e = __builtin_amdgcn_exp2f((az * az) * -1.44269504088896341f);
+    const float erf_v = copysignf(fmaf(-p, e, 1.0f), z);
+    const float hx = 0.5f * x;
+    return fmaf(hx, erf_v, hx);
+}
+
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// Four fp32 values -> four bf16 (round to nearest even) packed in 8 bytes.
+__device__ __forceinline__ uint2 pack4_bf16(float a, float b, float c, float d) {
+    const bf16x2_t lo = __builtin_convertvector((f32x2_t){a, b}, bf16x2_t);
+    const bf16x2_t hi = __builtin_convertvector((f32x2_t){c, d}, bf16x2_t);
+    uint2 r;
+    r.x = __builtin_bit_cast(uint32_t, lo);
+    r.y = __builtin_bit_cast(uint32_t, hi);
+    return r;
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+__device__ __forceinline__ void wait_lgkmcnt0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+// Workgroup barrier without the memory fence of __syncthreads (which would
+// wait for every copy still in flight, including slabs prefetched ahead).
+// Each wave waits for its own copies of the current slab with vmcnt before
+// arriving, and every LDS read of the slab before has been consumed by MFMAs,
+// so the bare barrier is enough.
+__device__ __forceinline__ void barrier_no_fence() { asm volatile("s_barrier" ::: "memory"); }
+
+// Buffer resource over `bytes` bytes at `base` (raw buffer, gfx9 format word).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+// 16 bytes per lane from (rsrc, voffset + soffset) straight into LDS at
+// lds + 16 * lane; lds is the same for the whole wave.
+__device__ __forceinline__ void copy16_to_lds(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff,
+                                              uint8_t* lds) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, (int)voff,
+                                             (int)soff, 0, 0);
+}
+
+__device__ __forceinline__ uint32_t lds_address(const uint8_t* p) {
+    return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) uint8_t*)p);
+}
+
+// One 16-byte fragment from LDS. Issued as inline assembly so the compiler
+// does not pair it with the in-flight copies into other stages (it cannot
+// tell them apart and would wait for all of them); completion is awaited
+// explicitly with wait_lgkmcnt0 and pinned with tie().
+template <int OFF>
+__device__ __forceinline__ bf16x8_t lds_read16(uint32_t addr) {
+    bf16x8_t r;
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+    return r;
+}
+__device__ __forceinline__ void tie(bf16x8_t& v) { asm volatile("" : "+v"(v)); }
+
+// bf16 grouped / dense GEMM, C[m, n] = sum_k X[m, k] W[n, k], fp32 accumulation.
+//
+// Tiles of BM token rows x BN output columns; WAVES_M x WAVES_N waves, each
+// owning a (BM / WAVES_M) x (BN / WAVES_N) sub-tile of 32x32 MFMA blocks.
+// The weight fragment is the MFMA's first operand and the token fragment the
+// second, so each lane's accumulators hold ONE token row and, per block,
+// four runs of four consecutive output columns: the epilogue writes 8- or
+// 16-byte row-contiguous pieces with one row address per lane.
+//
+// K slabs of BK (32 or 64) stream global -> LDS through a ring of STAGES
+// buffers with buffer_load ... lds (the K offset is a scalar, so issuing a
+// copy costs no vector instructions), STAGES - 1 slabs ahead of the MFMAs. A
+// wave fills whole 1 KB pieces: lane l of piece q lands in slot q*64 + l =
+// (row, physical chunk) and loads logical chunk physical ^ swizzle(row); the
+// swizzle puts the 16 rows read together by a quarter-wave of a fragment read
+// on 16 distinct 16-byte bank groups of the 64-bank LDS. Fragments for the
+// next 16-wide K step are read while the MFMAs of the current one run.
+template <int BM, int BN, int WAVES_M, int WAVES_N, int BK, int STAGES, int EPI, bool GROUPED, int WPE>
+__global__ __launch_bounds__(WAVES_M* WAVES_N* kWave) __attribute__((amdgpu_waves_per_eu(WPE, 8)))
+void k_gemm_bf16(const GemmArgs a) {
+    constexpr int NW = WAVES_M * WAVES_N;
+    constexpr int NT = NW * kWave;
+    constexpr int CPR = BK / 8;  // 16-byte chunks per LDS row
     constexpr int ROWB = BK * 2;
-    constexpr int WTM = BM / WAVES_M;  // wave tile
+    constexpr int KS = BK / 16;  // MFMA K steps per slab
+    constexpr int WTM = BM / WAVES_M;
     constexpr int WTN = BN / WAVES_N;
     constexpr int FM = WTM / 32;
     constexpr int FN = WTN / 32;
-    constexpr int ACH = BM * 8 / NT;  // 16-byte chunks per thread per slab
-    constexpr int BCH = BN * 8 / NT;
-    static_assert(ACH * NT == BM * 8 && BCH * NT == BN * 8, "tile / thread mismatch");
+    static_assert(FM >= 1 && FN >= 1, "wave tile must hold at least one 32x32 block");
+    constexpr int A_PIECES = BM * CPR / kWave;
+    constexpr int B_PIECES = BN * CPR / kWave;
+    static_assert(A_PIECES % NW == 0 && B_PIECES % NW == 0, "pieces must split evenly over waves");
+    constexpr int AP = A_PIECES / NW;
+    constexpr int BP = B_PIECES / NW;
     constexpr int STAGE = (BM + BN) * ROWB;
-    __shared__ __attribute__((aligned(16))) uint8_t smem[2 * STAGE];
+    static_assert(CPR == 4 || CPR == 8, "BK must be 32 or 64");
+    static_assert(STAGES >= 2 && STAGES <= 5, "2 to 5 stages");
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES * STAGE];
     __shared__ int32_t srow[BM];
 
     const TileCoord tc = locate_tile<GROUPED>(a, BM, BN);
@@ -100,7 +199,7 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N* kWave) void k_gemm_bf16(const Gem
     const int wave = tid / kWave;
     const int wm = wave / WAVES_N, wn = wave % WAVES_N;
 
-    // Row ids of this tile: A source rows (gather) or output rows (scatter).
+    // Row ids: gathered token rows (fc1 of routed experts) or output slots (fc2).
     for (int r = tid; r < BM; r += NT) {
         const int rr = r < tc.rows ? r : tc.rows - 1;  // pad rows repeat the last valid row
         const int p = tc.row0 + rr;
@@ -111,116 +210,154 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N* kWave) void k_gemm_bf16(const Gem
     }
     __syncthreads();
 
-    const bf16_t* __restrict__ A = static_cast<const bf16_t*>(a.A);
-    const bf16_t* __restrict__ B = static_cast<const bf16_t*>(a.B) + (size_t)tc.e * a.b_group_stride;
     const int Kd = a.Kdim;
+    const __amdgpu_buffer_rsrc_t xres = make_rsrc(a.A, a.a_bytes);
+    const __amdgpu_buffer_rsrc_t wres =
+        make_rsrc(static_cast<const bf16_t*>(a.B) + (size_t)tc.e * a.b_group_stride, (uint32_t)a.N * Kd * 2);
 
-    const bf16_t* ap[ACH];
-    int a_lds[ACH];
+    constexpr int SWZ_SHIFT = CPR == 8 ? 1 : 2;
+    constexpr int SWZ_MASK = CPR - 1;
+
+    uint32_t xv[AP];
 #pragma unroll
-    for (int i = 0; i < ACH; ++i) {
-        const int q = tid + NT * i;
-        const int r = q >> 3, c = q & 7;
-        int arow;
-        if (EPI == EPI_GELU_STORE) arow = srow[r];  // gathered token row or identity row
-        else arow = tc.row0 + (r < tc.rows ? r : tc.rows - 1);
-        ap[i] = A + (size_t)arow * Kd + c * 8;
-        a_lds[i] = r * ROWB + ((c ^ (r & 7)) << 4);
+    for (int i = 0; i < AP; ++i) {
+        const int sl = (wave + NW * i) * kWave + lane;
+        const int r = sl / CPR, pch = sl % CPR;
+        const int c = pch ^ ((r >> SWZ_SHIFT) & SWZ_MASK);
+        int xrow;
+        if (EPI == EPI_GELU_STORE) xrow = srow[r];
+        else xrow = tc.row0 + (r < tc.rows ? r : tc.rows - 1);
+        xv[i] = (uint32_t)xrow * (uint32_t)(Kd * 2) + c * 16;
     }
-    const bf16_t* bp[BCH];
-    int b_lds[BCH];
+    uint32_t wv[BP];
 #pragma unroll
-    for (int i = 0; i < BCH; ++i) {
-        const int q = tid + NT * i;
-        const int r = q >> 3, c = q & 7;
-        bp[i] = B + (size_t)(tc.n0 + r) * Kd + c * 8;
-        b_lds[i] = BM * ROWB + r * ROWB + ((c ^ (r & 7)) << 4);
+    for (int i = 0; i < BP; ++i) {
+        const int sl = (wave + NW * i) * kWave + lane;
+        const int r = sl / CPR, pch = sl % CPR;
+        const int c = pch ^ ((r >> SWZ_SHIFT) & SWZ_MASK);
+        wv[i] = (uint32_t)(tc.n0 + r) * (uint32_t)(Kd * 2) + c * 16;
     }
 
-    f32x16_t acc[FM][FN];
+    f32x16_t acc[FN][FM];
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+    for (int j = 0; j < FN; ++j)
 #pragma unroll
-        for (int j = 0; j < FN; ++j)
+        for (int i = 0; i < FM; ++i)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+            for (int v = 0; v < 16; ++v) acc[j][i][v] = 0.0f;
 
-    u32x4_t ra[ACH], rb[BCH];
-#define MOE_GLOAD(k0)                                                                        \
-    do {                                                                                     \
-        _Pragma("unroll") for (int i = 0; i < ACH; ++i) ra[i] =                              \
-            *reinterpret_cast<const u32x4_t*>(ap[i] + (k0));                                   \
-        _Pragma("unroll") for (int i = 0; i < BCH; ++i) rb[i] =                              \
-            *reinterpret_cast<const u32x4_t*>(bp[i] + (k0));                                   \
-    } while (0)
-#define MOE_LSTORE(stage)                                                                    \
-    do {                                                                                     \
-        uint8_t* base_ = smem + (stage) * STAGE;                                             \
-        _Pragma("unroll") for (int i = 0; i < ACH; ++i)                                      \
-            *reinterpret_cast<u32x4_t*>(base_ + a_lds[i]) = ra[i];                             \
-        _Pragma("unroll") for (int i = 0; i < BCH; ++i)                                      \
-            *reinterpret_cast<u32x4_t*>(base_ + b_lds[i]) = rb[i];                             \
-    } while (0)
-
-    // Fragment rows of this lane (the same for every slab).
-    const int fr = lane & 31;   // row within a 32-row block
-    const int fk = lane >> 5;   // which 8-wide half of each 16-wide K step
-
+    // Per-lane fragment offsets: row fr of a 32-row block, chunk (ks*2 + fk)
+    // swizzled; the swizzle depends only on fr because blocks start at
+    // multiples of 32 rows.
+    const int fr = lane & 31;
+    const int fk = lane >> 5;
+    const int lane_sw = (fr >> SWZ_SHIFT) & SWZ_MASK;
+    uint32_t xoff[KS], woff[KS];
+    const uint32_t base = lds_address(smem);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+        const uint32_t k = fr * ROWB + (((ks * 2 + fk) ^ lane_sw) << 4);
+        xoff[ks] = base + (wm * WTM) * ROWB + k;
+        woff[ks] = base + BM * ROWB + (wn * WTN) * ROWB + k;
+    }
     const int nk = Kd / BK;
-    MOE_GLOAD(0);
-    MOE_LSTORE(0);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        if (kt + 1 < nk) MOE_GLOAD((kt + 1) * BK);
-        const uint8_t* base = smem + (kt & 1) * STAGE;
-#pragma unroll
-        for (int ks = 0; ks < BK / 16; ++ks) {
-            const int ch = ks * 2 + fk;
-            bf16x8_t af[FM], bfr[FN];
-#pragma unroll
-            for (int i = 0; i < FM; ++i) {
-                const int r = wm * WTM + i * 32 + fr;
-                af[i] = *reinterpret_cast<const bf16x8_t*>(base + r * ROWB + ((ch ^ (r & 7)) << 4));
-            }
-#pragma unroll
-            for (int j = 0; j < FN; ++j) {
-                const int r = wn * WTN + j * 32 + fr;
-                bfr[j] = *reinterpret_cast<const bf16x8_t*>(base + BM * ROWB + r * ROWB + ((ch ^ (r & 7)) << 4));
-            }
-#pragma unroll
-            for (int i = 0; i < FM; ++i)
-#pragma unroll
-                for (int j = 0; j < FN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-        }
-        if (kt + 1 < nk) MOE_LSTORE((kt + 1) & 1);
-        __syncthreads();
-    }
-#undef MOE_GLOAD
-#undef MOE_LSTORE
 
-    // Epilogue. Accumulator v of a 32x32 block sits at row 8*(v/4) + 4*(lane/32)
-    // + v%4 and column lane%32.
-    const int col_in = lane & 31;
-    const int row_in = (lane >> 5) * 4;
+    auto issue = [&](int stage, int kslab) {
+        uint8_t* buf = smem + stage * STAGE;
+        const uint32_t soff = (uint32_t)kslab * BK * 2;
+#pragma unroll
+        for (int i = 0; i < AP; ++i) copy16_to_lds(xres, xv[i], soff, buf + (wave + NW * i) * 1024);
+#pragma unroll
+        for (int i = 0; i < BP; ++i) copy16_to_lds(wres, wv[i], soff, buf + BM * ROWB + (wave + NW * i) * 1024);
+    };
+    auto read_frags = [&](uint32_t sbase, int ks, bf16x8_t* xf, bf16x8_t* wf) {
+        const uint32_t xa = xoff[ks] + sbase, wa = woff[ks] + sbase;
+        if constexpr (FM >= 1) xf[0] = lds_read16<0 * 32 * ROWB>(xa);
+        if constexpr (FM >= 2) xf[1] = lds_read16<1 * 32 * ROWB>(xa);
+        if constexpr (FM >= 3) xf[2] = lds_read16<2 * 32 * ROWB>(xa);
+        if constexpr (FM >= 4) xf[3] = lds_read16<3 * 32 * ROWB>(xa);
+        if constexpr (FN >= 1) wf[0] = lds_read16<0 * 32 * ROWB>(wa);
+        if constexpr (FN >= 2) wf[1] = lds_read16<1 * 32 * ROWB>(wa);
+        if constexpr (FN >= 3) wf[2] = lds_read16<2 * 32 * ROWB>(wa);
+        if constexpr (FN >= 4) wf[3] = lds_read16<3 * 32 * ROWB>(wa);
+        static_assert(FM <= 4 && FN <= 4, "at most 4x4 blocks per wave");
+    };
+    auto settle = [&](bf16x8_t* xf, bf16x8_t* wf) {
+        wait_lgkmcnt0();
+#pragma unroll
+        for (int i = 0; i < FM; ++i) tie(xf[i]);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) tie(wf[j]);
+    };
+
+#pragma unroll
+    for (int sl = 0; sl < STAGES - 1; ++sl)
+        if (sl < nk) issue(sl, sl);
+
+    int cur_stage = 0;
+    for (int kt = 0; kt < nk; ++kt) {
+        // Slab kt must have landed; the later prefetched slabs stay in flight.
+        const int ahead = min(nk - 1 - kt, STAGES - 2);
+        if constexpr (STAGES >= 5) { if (ahead >= 3) { wait_vmcnt<3 * (AP + BP)>(); goto waited; } }
+        if constexpr (STAGES >= 4) { if (ahead >= 2) { wait_vmcnt<2 * (AP + BP)>(); goto waited; } }
+        if constexpr (STAGES >= 3) { if (ahead >= 1) { wait_vmcnt<AP + BP>(); goto waited; } }
+        wait_vmcnt<0>();
+    waited:
+        barrier_no_fence();
+        if (kt + STAGES - 1 < nk) {
+            int st = cur_stage + STAGES - 1;
+            if (st >= STAGES) st -= STAGES;
+            issue(st, kt + STAGES - 1);
+        }
+        const uint32_t sbase = cur_stage * STAGE;
+        bf16x8_t xf[2][FM], wf[2][FN];
+        read_frags(sbase, 0, xf[0], wf[0]);
+        settle(xf[0], wf[0]);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            const int c = ks & 1;
+            if (ks + 1 < KS) read_frags(sbase, ks + 1, xf[c ^ 1], wf[c ^ 1]);
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int i = 0; i < FM; ++i)
+                    acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[c][j], xf[c][i], acc[j][i], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            if (ks + 1 < KS) settle(xf[c ^ 1], wf[c ^ 1]);
+        }
+        if (++cur_stage == STAGES) cur_stage = 0;
+    }
+
+    // Epilogue. Block (j, i): this lane's token row is i*32 + (lane & 31) of
+    // the wave tile; accumulator 4g + q is column j*32 + 8g + 4*(lane >> 5) + q.
+    const int col0 = tc.n0 + wn * WTN + 4 * fk;
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
+        const int r = wm * WTM + i * 32 + fr;
+        if (r >= tc.rows) continue;
+        if (EPI == EPI_GELU_STORE || EPI == EPI_SCATTER_SLOT) {
+            const size_t orow = EPI == EPI_SCATTER_SLOT ? (size_t)srow[r] : (size_t)(tc.row0 + r);
+            bf16_t* out = static_cast<bf16_t*>(a.C) + orow * a.N + col0;
 #pragma unroll
-        for (int j = 0; j < FN; ++j) {
-            const int c = tc.n0 + wn * WTN + j * 32 + col_in;
+            for (int j = 0; j < FN; ++j)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int r = wm * WTM + i * 32 + (v >> 2) * 8 + row_in + (v & 3);
-                if (r >= tc.rows) continue;
-                const float val = acc[i][j][v];
-                if (EPI == EPI_GELU_STORE) {
-                    static_cast<bf16_t*>(a.C)[(size_t)(tc.row0 + r) * a.N + c] = f32_to_bf16_rne(gelu_erf(val));
-                } else if (EPI == EPI_SCATTER_SLOT) {
-                    static_cast<bf16_t*>(a.C)[(size_t)srow[r] * a.N + c] = f32_to_bf16_rne(val);
-                } else {
-                    static_cast<float*>(a.C)[(size_t)(tc.row0 + r) * a.N + c] = val;
+                for (int g = 0; g < 4; ++g) {
+                    float v0 = acc[j][i][4 * g + 0], v1 = acc[j][i][4 * g + 1];
+                    float v2 = acc[j][i][4 * g + 2], v3 = acc[j][i][4 * g + 3];
+                    if (EPI == EPI_GELU_STORE) {
+                        v0 = gelu_as(v0); v1 = gelu_as(v1); v2 = gelu_as(v2); v3 = gelu_as(v3);
+                    }
+                    *reinterpret_cast<uint2*>(out + j * 32 + 8 * g) = pack4_bf16(v0, v1, v2, v3);
                 }
-            }
+        } else {
+            float* out = static_cast<float*>(a.C) + (size_t)(tc.row0 + r) * a.N + col0;
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int g = 0; g < 4; ++g)
+                    *reinterpret_cast<float4*>(out + j * 32 + 8 * g) =
+                        make_float4(acc[j][i][4 * g], acc[j][i][4 * g + 1], acc[j][i][4 * g + 2],
+                                    acc[j][i][4 * g + 3]);
         }
     }
 }
@@ -294,13 +431,13 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const GemmArgs a) {
     }
 }
 
-template <int BM, int BN, int WM, int WN, int EPI, bool GROUPED>
+template <int BM, int BN, int WM, int WN, int BK, int ST, int WPE, int EPI, bool GROUPED>
 hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
     const int n_n = a.N / BN;
     const long long total = (long long)a.max_tiles * n_n;
     const long long grid = (total + kNumXcd - 1) / kNumXcd * kNumXcd;
-    hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, EPI, GROUPED>), dim3((unsigned)grid), dim3(WM * WN * kWave),
-                       0, s, a);
+    hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, BK, ST, EPI, GROUPED, WPE>), dim3((unsigned)grid),
+                       dim3(WM * WN * kWave), 0, s, a);
     return hipGetLastError();
 }
 
@@ -313,11 +450,28 @@ hipError_t launch_f32(const GemmArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
+// Tile shapes. Large groups (M-tiles of 256 token rows): 256 x 256 when N
+// allows, else 256 x 128 or 256 x 64. Small groups (M-tiles of 64 rows, the
+// weight-read-bound regime where an expert sees a few dozen tokens): 64 x 128
+// or 64 x 64, several workgroups per CU to keep many weight loads in flight.
+// Tile shapes. Large groups (M-tiles of 256 token rows): 256 x 256 with 8
+// waves of 128 x 64 (64-wide K slabs, double-buffered) when N allows, else
+// 256 x 128 or 256 x 64 with 4 waves. Small groups (M-tiles of 64 rows, the
+// weight-read-bound regime where an expert sees a few dozen tokens): 64 x 128
+// or 64 x 64 with three slabs in the ring and several workgroups per CU, to
+// keep many weight loads in flight.
 template <int EPI, bool GROUPED>
 hipError_t dispatch_bf16(int bm, const GemmArgs& a, hipStream_t s) {
-    if (bm != 128) return hipErrorInvalidValue;
-    if (a.N % 128 == 0) return launch_bf16<128, 128, 2, 2, EPI, GROUPED>(a, s);
-    return launch_bf16<128, 64, 2, 2, EPI, GROUPED>(a, s);
+    if (bm == 256) {
+        if (a.N % 256 == 0) return launch_bf16<256, 256, 2, 4, 64, 2, 1, EPI, GROUPED>(a, s);
+        if (a.N % 128 == 0) return launch_bf16<256, 128, 2, 2, 64, 2, 1, EPI, GROUPED>(a, s);
+        return launch_bf16<256, 64, 4, 1, 64, 2, 1, EPI, GROUPED>(a, s);
+    }
+    if (bm == 64) {
+        if (a.N % 128 == 0) return launch_bf16<64, 128, 1, 4, 64, 3, 2, EPI, GROUPED>(a, s);
+        return launch_bf16<64, 64, 2, 2, 64, 3, 2, EPI, GROUPED>(a, s);
+    }
+    return hipErrorInvalidValue;
 }
 
 template <bool GROUPED>
@@ -325,15 +479,23 @@ hipError_t dispatch(const moe_desc_t& d, int epilogue, int bm, const GemmArgs& a
     if (d.dtype == MOE_BF16) {
         switch (epilogue) {
             case EPI_GELU_STORE: return dispatch_bf16<EPI_GELU_STORE, GROUPED>(bm, a, s);
-            case EPI_SCATTER_SLOT: return dispatch_bf16<EPI_SCATTER_SLOT, GROUPED>(bm, a, s);
-            case EPI_STORE_F32: return dispatch_bf16<EPI_STORE_F32, GROUPED>(bm, a, s);
+            case EPI_SCATTER_SLOT:
+                if (GROUPED) return dispatch_bf16<EPI_SCATTER_SLOT, true>(bm, a, s);
+                break;
+            case EPI_STORE_F32:
+                if (!GROUPED) return dispatch_bf16<EPI_STORE_F32, false>(bm, a, s);
+                break;
         }
     } else {
         if (bm != 64) return hipErrorInvalidValue;
         switch (epilogue) {
             case EPI_GELU_STORE: return launch_f32<EPI_GELU_STORE, GROUPED>(a, s);
-            case EPI_SCATTER_SLOT: return launch_f32<EPI_SCATTER_SLOT, GROUPED>(a, s);
-            case EPI_STORE_F32: return launch_f32<EPI_STORE_F32, GROUPED>(a, s);
+            case EPI_SCATTER_SLOT:
+                if (GROUPED) return launch_f32<EPI_SCATTER_SLOT, true>(a, s);
+                break;
+            case EPI_STORE_F32:
+                if (!GROUPED) return launch_f32<EPI_STORE_F32, false>(a, s);
+                break;
         }
     }
     return hipErrorInvalidValue;
@@ -341,17 +503,22 @@ hipError_t dispatch(const moe_desc_t& d, int epilogue, int bm, const GemmArgs& a
 
 }  // namespace
 
-int gemm_tile_bm(int32_t dtype) { return dtype == MOE_BF16 ? 128 : 64; }
+int gemm_tile_bm(int32_t dtype, int64_t avg_rows) {
+    if (dtype != MOE_BF16) return 64;
+    return avg_rows >= 512 ? 256 : 64;
+}
+
+int gemm_dense_bm(int32_t dtype, int64_t rows, int32_t n) {
+    if (dtype != MOE_BF16) return 64;
+    // 256-row tiles only when they still give a few workgroups per CU.
+    const int64_t tiles = (rows + 255) / 256 * (n / 256 > 0 ? n / 256 : 1);
+    return tiles >= 512 ? 256 : 64;
+}
 
 hipError_t launch_gemm(const moe_desc_t& d, int epilogue, int bm, const GemmArgs& a, hipStream_t s) {
     // Grouped (routed experts, tile table) and dense (shared expert) launches
     // are separate kernel instances.
-    if (a.tiles) {
-        // Only the two routed stages run grouped.
-        if (epilogue == EPI_STORE_F32) return hipErrorInvalidValue;
-        return dispatch<true>(d, epilogue, bm, a, s);
-    }
-    if (epilogue == EPI_SCATTER_SLOT) return hipErrorInvalidValue;
+    if (a.tiles) return dispatch<true>(d, epilogue, bm, a, s);
     return dispatch<false>(d, epilogue, bm, a, s);
 }
 

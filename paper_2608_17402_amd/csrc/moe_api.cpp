@@ -14,7 +14,6 @@
 namespace moe {
 
 int32_t permute_blocks(int64_t n_slots, int32_t E);
-int gemm_tile_bm(int32_t dtype);
 
 namespace {
 
@@ -57,6 +56,11 @@ moe_status_t check_desc(const moe_desc_t* d) {
         return fail(MOE_ERR_UNSUPPORTED, "d = %d, h = %d, h_shared = %d must be multiples of 64", d->d,
                     d->h, d->h_shared);
     if (!std::isfinite(d->lambda)) return fail(MOE_ERR_INVALID_ARG, "lambda is not finite");
+    // GEMM operands are addressed through 32-bit buffer offsets.
+    const uint64_t es = d->dtype == MOE_BF16 ? 2 : 4, lim = (uint64_t)1 << 32;
+    if ((uint64_t)d->T * d->d * es >= lim || (uint64_t)d->T * d->K * d->h * es >= lim ||
+        (uint64_t)d->T * d->h_shared * es >= lim)
+        return fail(MOE_ERR_UNSUPPORTED, "x, the expert activations or the shared activations exceed 4 GiB");
     return MOE_OK;
 }
 
@@ -102,14 +106,12 @@ T* region(void* ws, size_t off) {
 
 size_t elem_size(int32_t dtype) { return dtype == MOE_BF16 ? 2 : 4; }
 
-int choose_tile_bm(const moe_desc_t& d) { return gemm_tile_bm(d.dtype); }
-
 WorkspacePlan plan_workspace(const moe_desc_t& d) {
     WorkspacePlan p;
     const size_t es = elem_size(d.dtype);
     const size_t TK = (size_t)d.T * d.K;
     p.n_hist_blocks = permute_blocks((int64_t)TK, d.E);
-    p.tile_bm = choose_tile_bm(d);
+    p.tile_bm = gemm_tile_bm(d.dtype, (int64_t)TK / d.E);
     const size_t busy = TK < (size_t)d.E ? TK : (size_t)d.E;  // experts that can hold a slot
     p.max_tiles = (int32_t)((TK + busy * (p.tile_bm - 1)) / p.tile_bm);
     size_t off = 0;
@@ -156,6 +158,7 @@ static moe_status_t enqueue_routed_mlp(const moe_desc_t& d, const WorkspacePlan&
     g.row_mode = ROWS_GATHER_TOKENS;
     g.max_tiles = p.max_tiles;
     g.b_group_stride = (int64_t)d.h * d.d;
+    g.a_bytes = (uint32_t)((size_t)d.T * d.d * elem_size(d.dtype));
     HIP_CHECK(launch_gemm(d, EPI_GELU_STORE, p.tile_bm, g, s), "fc1 grouped gemm");
     GemmArgs g2 = g;
     g2.A = region<void>(ws, p.act);
@@ -165,13 +168,15 @@ static moe_status_t enqueue_routed_mlp(const moe_desc_t& d, const WorkspacePlan&
     g2.Kdim = d.h;
     g2.row_mode = ROWS_IDENTITY;
     g2.b_group_stride = (int64_t)d.d * d.h;
+    g2.a_bytes = (uint32_t)((size_t)d.T * d.K * d.h * elem_size(d.dtype));
     HIP_CHECK(launch_gemm(d, EPI_SCATTER_SLOT, p.tile_bm, g2, s), "fc2 grouped gemm");
     return MOE_OK;
 }
 
-// Shared expert over all T tokens in token order; fp32 output.
+// Shared expert over all T tokens in token order, fp32 output for the combine.
 static moe_status_t enqueue_shared_mlp(const moe_desc_t& d, const WorkspacePlan& p, void* ws, const void* x,
-                                       const void* w1s, const void* w2s, float* out, hipStream_t s) {
+                                       const void* w1s, const void* w2s, float* sout, hipStream_t s) {
+    const int bm = gemm_dense_bm(d.dtype, d.T, d.h_shared < d.d ? d.h_shared : d.d);
     GemmArgs g{};
     g.A = x;
     g.B = w1s;
@@ -181,15 +186,17 @@ static moe_status_t enqueue_shared_mlp(const moe_desc_t& d, const WorkspacePlan&
     g.Kdim = d.d;
     g.route_k = 1;
     g.row_mode = ROWS_IDENTITY;
-    g.max_tiles = (d.T + p.tile_bm - 1) / p.tile_bm;
-    HIP_CHECK(launch_gemm(d, EPI_GELU_STORE, p.tile_bm, g, s), "shared fc1 gemm");
+    g.max_tiles = (d.T + bm - 1) / bm;
+    g.a_bytes = (uint32_t)((size_t)d.T * d.d * elem_size(d.dtype));
+    HIP_CHECK(launch_gemm(d, EPI_GELU_STORE, bm, g, s), "shared fc1 gemm");
     GemmArgs g2 = g;
     g2.A = region<void>(ws, p.sact);
     g2.B = w2s;
-    g2.C = out;
+    g2.C = sout;
     g2.N = d.d;
     g2.Kdim = d.h_shared;
-    HIP_CHECK(launch_gemm(d, EPI_STORE_F32, p.tile_bm, g2, s), "shared fc2 gemm");
+    g2.a_bytes = (uint32_t)((size_t)d.T * d.h_shared * elem_size(d.dtype));
+    HIP_CHECK(launch_gemm(d, EPI_STORE_F32, bm, g2, s), "shared fc2 gemm");
     return MOE_OK;
 }
 

@@ -54,6 +54,7 @@ struct GemmArgs {
     int32_t row_mode;          // GemmRowMode
     int32_t max_tiles;         // upper bound on the number of M-tiles (grid sizing)
     int64_t b_group_stride;    // elements between consecutive experts' weights
+    uint32_t a_bytes;          // bytes of the A operand buffer (bounds of its buffer resource)
 };
 
 // Offsets (bytes) of every workspace region for one descriptor.
@@ -68,7 +69,10 @@ struct WorkspacePlan {
 
 size_t elem_size(int32_t dtype);
 WorkspacePlan plan_workspace(const moe_desc_t& d);
-int choose_tile_bm(const moe_desc_t& d);
+// M-tile height of the grouped GEMM for groups of `avg_rows` rows on average.
+int gemm_tile_bm(int32_t dtype, int64_t avg_rows);
+// M-tile height of a dense GEMM of `rows` rows and `n` output columns.
+int gemm_dense_bm(int32_t dtype, int64_t rows, int32_t n);
 
 // ---- launchers (each returns the first HIP error, hipSuccess otherwise)
 hipError_t launch_router_scores(const moe_desc_t& d, const void* x, const void* w_router,

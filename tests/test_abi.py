@@ -56,8 +56,11 @@ def test_workspace_size_and_desc_validation(lib):
     assert st == 0 and n > 196 * 2 * 256 * 4 * 2
     st4, n4 = _ws(binding.make_desc(65536, 1536, 256, 8, 768, 1536, 1.0, "bf16"))
     assert st4 == 0
-    # activation + expert outputs (bf16) + shared output (fp32) at least
-    assert n4 >= 65536 * 8 * (768 + 1536) * 2 + 65536 * 1536 * 4
+    # routed activation + expert outputs + shared activation (bf16) at least
+    assert n4 >= 65536 * 8 * (768 + 1536) * 2 + 65536 * 1536 * 2
+    st1, n1 = _ws(binding.make_desc(196, 256, 8, 2, 256, 128, 1.0, "f32"))
+    # the fp32 layer also keeps the shared expert's fp32 output for the combine
+    assert st1 == 0 and n1 >= 196 * 2 * (256 + 256) * 4 + 196 * 128 * 4 + 196 * 256 * 4
     bad = {
         "K=0": (binding.make_desc(10, 64, 8, 0, 64), 1),
         "K>16": (binding.make_desc(10, 64, 32, 17, 64), 1),
