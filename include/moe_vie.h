@@ -50,9 +50,15 @@ typedef enum {
 
 typedef enum { MOE_F32 = 0, MOE_BF16 = 1 } moe_dtype_t;
 
+/* Flags of moe_desc_t.flags. */
+#define MOE_FLAG_EXACT_ROUTER 1 /* compute every router logit by the exact chain
+                                   (no MFMA pre-pass); the routing result is the
+                                   same bit for bit, only the work differs */
+
 /* Layer descriptor. Limits: 1 <= T, T*K < 2^31; 1 <= K <= 16; K <= E <= 1024;
  * 64 <= d <= 8192, 64 <= h <= 8192, 0 <= h_shared <= 8192 (0 = no shared
- * expert), all multiples of 64; flags must be 0. */
+ * expert), all multiples of 64; T*d, T*K*h and T*h_shared elements below
+ * 4 GiB; flags a combination of MOE_FLAG_* bits. */
 typedef struct {
     int32_t T;        /* tokens                                   */
     int32_t d;        /* model width                              */
@@ -62,7 +68,7 @@ typedef struct {
     int32_t h_shared; /* hidden width of the shared expert, or 0  */
     float lambda;     /* weight of the shared expert (paper: 1)   */
     int32_t dtype;    /* moe_dtype_t                              */
-    int32_t flags;    /* reserved, must be 0                      */
+    int32_t flags;    /* MOE_FLAG_* bits, 0 by default            */
 } moe_desc_t;
 
 /* Human-readable name of a status code (static string). */
@@ -88,7 +94,11 @@ moe_status_t moe_workspace_size(const moe_desc_t *desc, size_t *bytes);
  * the sigmoid is 1/(1 + exp(-s)) with -s clamped to [-87, 87]
  * and evaluated by Cody-Waite reduction with ln2 = 22713*2^-15 + fl32(ln2 -
  * 22713*2^-15) and a degree-7 Taylor polynomial in Horner form; the gate
- * denominator is summed in slot order. Uses the workspace (sigmoid scores). */
+ * denominator is summed in slot order. For bf16 layers with E a multiple of
+ * 64 the logits are first computed with bf16 MFMA; every expert whose key
+ * could still reach the top K under a proven bound on the difference is then
+ * recomputed with the exact chain, so the result is the exact one.
+ * Uses the workspace. */
 moe_status_t moe_route(const moe_desc_t *desc, const void *x, const void *w_router,
                        const float *bias, int32_t *topk_idx, float *topk_gate, void *workspace,
                        size_t workspace_bytes, void *stream);

@@ -42,7 +42,7 @@ moe_status_t check_desc(const moe_desc_t* d) {
     if (!d) return fail(MOE_ERR_INVALID_ARG, "desc is NULL");
     if (d->dtype != MOE_F32 && d->dtype != MOE_BF16)
         return fail(MOE_ERR_UNSUPPORTED, "dtype %d is not MOE_F32 or MOE_BF16", d->dtype);
-    if (d->flags != 0) return fail(MOE_ERR_INVALID_ARG, "flags must be 0 (got %d)", d->flags);
+    if (d->flags & ~MOE_FLAG_EXACT_ROUTER) return fail(MOE_ERR_INVALID_ARG, "unknown flags 0x%x", d->flags);
     if (d->T < 1) return fail(MOE_ERR_INVALID_ARG, "T = %d must be >= 1", d->T);
     if (d->K < 1 || d->K > kMaxK) return fail(MOE_ERR_INVALID_ARG, "K = %d must be in [1, %d]", d->K, kMaxK);
     if (d->E < d->K || d->E > kMaxE)
@@ -123,6 +123,9 @@ WorkspacePlan plan_workspace(const moe_desc_t& d) {
     p.idx = take(TK * 4);
     p.gate = take(TK * 4);
     p.scores = take((size_t)d.T * d.E * 4);
+    p.xnorm = take((size_t)d.T * 4);
+    p.wnorm = take((size_t)d.E * 4);
+    p.ovf = take((size_t)(d.T + 1) * 4);
     p.counts = take((size_t)d.E * 4);
     p.offsets = take((size_t)(d.E + 1) * 4);
     p.slots = take(TK * 4);
@@ -135,6 +138,41 @@ WorkspacePlan plan_workspace(const moe_desc_t& d) {
     p.sout = take(d.h_shared ? (size_t)d.T * d.d * 4 : 0);
     p.total = off;
     return p;
+}
+
+static bool fast_router(const moe_desc_t& d) {
+    return d.dtype == MOE_BF16 && d.E % 64 == 0 && !(d.flags & MOE_FLAG_EXACT_ROUTER);
+}
+
+// Router and gating: exact chain for every logit, or MFMA logits plus exact
+// repair of the candidates (same result).
+static moe_status_t enqueue_route(const moe_desc_t& d, const WorkspacePlan& p, void* ws, const void* x,
+                                  const void* w_router, const float* bias, int32_t* idx, float* gate,
+                                  hipStream_t s) {
+    float* scores = region<float>(ws, p.scores);
+    if (!fast_router(d)) {
+        HIP_CHECK(launch_router_scores(d, x, w_router, scores, s), "router scores");
+        HIP_CHECK(launch_topk(d, scores, bias, idx, gate, s), "top-k");
+        return MOE_OK;
+    }
+    GemmArgs g{};
+    g.A = x;
+    g.B = w_router;
+    g.C = scores;
+    g.dense_rows = d.T;
+    g.N = d.E;
+    g.Kdim = d.d;
+    g.route_k = 1;
+    g.row_mode = ROWS_IDENTITY;
+    const int bm = (int64_t)d.T * d.E >= (int64_t)200 * 65536 ? 256 : 64;
+    g.max_tiles = (d.T + bm - 1) / bm;
+    g.a_bytes = (uint32_t)((size_t)d.T * d.d * 2);
+    HIP_CHECK(launch_gemm(d, EPI_STORE_F32, bm, g, s), "router logits gemm");
+    int32_t* ovf = region<int32_t>(ws, p.ovf);
+    HIP_CHECK(launch_router_fast_finish(d, scores, x, w_router, bias, region<float>(ws, p.xnorm),
+                                        region<float>(ws, p.wnorm), ovf, ovf + 1, idx, gate, s),
+              "router repair");
+    return MOE_OK;
 }
 
 // Routed experts: fc1 + GELU into the activation buffer (sorted order), then
@@ -237,9 +275,7 @@ MOE_API moe_status_t moe_route(const moe_desc_t* desc, const void* x, const void
     CHECK(check_ws(*desc, workspace, workspace_bytes, &p));
     hipStream_t s = static_cast<hipStream_t>(stream);
     (void)hipGetLastError();
-    float* scores = region<float>(workspace, p.scores);
-    HIP_CHECK(launch_router_scores(*desc, x, w_router, scores, s), "router scores");
-    HIP_CHECK(launch_topk(*desc, scores, bias, topk_idx, topk_gate, s), "top-k");
+    CHECK(enqueue_route(*desc, p, workspace, x, w_router, bias, topk_idx, topk_gate, s));
     return ok();
 }
 
@@ -317,15 +353,13 @@ MOE_API moe_status_t moe_layer_forward(const moe_desc_t* desc, const void* x, co
 
     int32_t* idx = topk_idx_out ? topk_idx_out : region<int32_t>(workspace, p.idx);
     float* gate = topk_gate_out ? topk_gate_out : region<float>(workspace, p.gate);
-    float* scores = region<float>(workspace, p.scores);
     int32_t* counts = region<int32_t>(workspace, p.counts);
     int32_t* offsets = region<int32_t>(workspace, p.offsets);
     int32_t* slots = region<int32_t>(workspace, p.slots);
     void* eout = region<void>(workspace, p.eout);
     float* sout = d.h_shared ? region<float>(workspace, p.sout) : nullptr;
 
-    HIP_CHECK(launch_router_scores(d, x, w_router, scores, s), "router scores");
-    HIP_CHECK(launch_topk(d, scores, bias, idx, gate, s), "top-k");
+    CHECK(enqueue_route(d, p, workspace, x, w_router, bias, idx, gate, s));
     HIP_CHECK(launch_permute(d, idx, counts, offsets, slots, region<int32_t>(workspace, p.blockhist),
                              p.n_hist_blocks, s),
               "permute");

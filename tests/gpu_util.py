@@ -34,7 +34,7 @@ def host(t: torch.Tensor) -> np.ndarray:
 
 def desc_for(cfg, T=None, **over):
     kw = dict(T=cfg.T if T is None else T, d=cfg.d, E=cfg.E, K=cfg.K, h=cfg.h, h_shared=cfg.h_shared,
-              lam=cfg.lam, dtype=cfg.dtype)
+              lam=cfg.lam, dtype=cfg.dtype, flags=0)
     kw.update(over)
     return binding.make_desc(**kw)
 

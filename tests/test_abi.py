@@ -72,7 +72,8 @@ def test_workspace_size_and_desc_validation(lib):
         "hs%64": (binding.make_desc(10, 64, 8, 2, 64, 65), 2),
         "d>8192": (binding.make_desc(10, 8256, 8, 2, 64), 1),
         "dtype": (binding.make_desc(10, 64, 8, 2, 64, 0, 1.0, 7), 2),
-        "flags": (binding.make_desc(10, 64, 8, 2, 64, 0, 1.0, "bf16", flags=1), 1),
+        "flags": (binding.make_desc(10, 64, 8, 2, 64, 0, 1.0, "bf16", flags=2), 1),
+        "4GiB": (binding.make_desc(2 ** 21, 1024, 8, 2, 64, 0, 1.0, "bf16"), 2),
         "lambda": (binding.make_desc(10, 64, 8, 2, 64, 0, float("nan")), 1),
         "T*K": (binding.make_desc(2 ** 28, 64, 16, 8, 64), 1),
     }

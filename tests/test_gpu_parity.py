@@ -53,6 +53,43 @@ def test_route_bit_exact(small):
     assert np.max(np.abs(g.sum(1) - 1.0)) <= cfg.K * 2.0 ** -23
 
 
+def test_route_exact_flag_agrees(small):
+    # The all-exact router and the MFMA pre-pass with exact repair must give
+    # the same routing, bit for bit.
+    cfg, inp, lay, _, ref_idx, ref_gate = small
+    d2 = desc_for(cfg, flags=binding.MOE_FLAG_EXACT_ROUTER)
+    idx = torch.empty(cfg.T, cfg.K, dtype=torch.int32, device="cuda")
+    gate = torch.empty(cfg.T, cfg.K, dtype=torch.float32, device="cuda")
+    binding.moe_route(d2, lay.x, lay.w_router, lay.bias, idx, gate, lay.ws)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(idx), ref_idx) and np.array_equal(host(gate), ref_gate)
+
+
+@pytest.mark.parametrize("dup", [1, 16, 128])
+def test_route_near_ties_take_exact_fallback(dup):
+    # Groups of `dup` identical router rows tie exactly for every token; with
+    # dup = 128 every expert is a candidate, more than the repair keeps, so
+    # every token goes through the exact all-experts kernel.
+    T, d, E, K = 300, 256, 128, 8
+    rng = np.random.default_rng(dup)
+    from workloads import bf16_bits_to_f32, f32_to_bf16_bits
+
+    x = f32_to_bf16_bits(rng.standard_normal((T, d)).astype(np.float32))
+    base = f32_to_bf16_bits((rng.standard_normal((E // dup, d)) * 0.05).astype(np.float32))
+    wr = np.repeat(base, dup, axis=0)
+    bias = np.zeros(E, np.float32)
+    desc = binding.make_desc(T, d, E, K, 64)
+    ws = binding.alloc_workspace(desc)
+    idx = torch.empty(T, K, dtype=torch.int32, device="cuda")
+    gate = torch.empty(T, K, dtype=torch.float32, device="cuda")
+    binding.moe_route(desc, dev(x), dev(wr), dev(bias), idx, gate, ws)
+    torch.cuda.synchronize()
+    ref_idx, ref_gate = oracle.route(bf16_bits_to_f32(x), bf16_bits_to_f32(wr), bias, K)
+    assert np.array_equal(host(idx), ref_idx) and np.array_equal(host(gate), ref_gate)
+    if dup == 128:
+        assert np.all(ref_idx == np.arange(K)[None, :])
+
+
 def test_permute_exact(small):
     cfg, inp, lay, _, ref_idx, _ = small
     counts, offsets, slots = lay.permute(dev(ref_idx))
