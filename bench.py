@@ -28,6 +28,35 @@ PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 4096 flop/clk x 2.4 GHz, dense
 PEAK_HBM_GBS = 8000.0
 
 
+# HBM bytes per launch pair (fc1 + fc2) of the routed grouped GEMM, from the
+# FETCH_SIZE and WRITE_SIZE hardware counters, each scaled by the factor that
+# makes the same counter read the known byte count of a plain 1 GiB device
+# copy (fetch x2.0, write x1.0). Taken with `bench.py --mode gemm` and
+# `--mode copy` under rocprofv3 --pmc; the summary under profiles/ gives the
+# commands and raw figures. The figures hold for the GEMM sources whose hash is
+# TRAFFIC_SOURCE_HASH: once those change, traffic is reported as null until
+# the counters are taken again.
+TRAFFIC_SOURCE_HASH = "411387c33e4fdf7c"
+TRAFFIC_BYTES = {"vitg_skew_bf16": 7555991150, "single_image_bf16": 1285260757}
+
+
+def gemm_source_hash():
+    import hashlib
+
+    csrc = os.path.join(ROOT, "paper_2608_17402_amd", "csrc")
+    m = hashlib.sha256()
+    for f in ("gemm.hip", "moe_internal.h"):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            m.update(fh.read())
+    return m.hexdigest()[:16]
+
+
+def traffic_bytes(workload):
+    if gemm_source_hash() != TRAFFIC_SOURCE_HASH:
+        return None
+    return TRAFFIC_BYTES.get(workload)
+
+
 def parse():
     p = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     p.add_argument("--gpus", type=int, default=1)
@@ -40,6 +69,11 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=15.0,
                    help="target CPU time of the oracle sample")
     p.add_argument("--stage-reps", type=int, default=10)
+    p.add_argument("--mode", choices=("layer", "gemm", "copy"), default="layer",
+                   help="layer: the benchmark; gemm: only the routed grouped GEMMs of --config, repeated "
+                        "(hardware-counter runs); copy: a plain device copy of --copy-mib MiB "
+                        "(calibration of the byte counters)")
+    p.add_argument("--copy-mib", type=int, default=1024)
     return p.parse_args()
 
 
@@ -92,9 +126,9 @@ def main():
             torch.cuda.synchronize()
             self.setup_s = time.perf_counter() - t0
 
-        def forward(self):
+        def forward(self, events=None):
             binding.moe_layer_forward(self.desc, self.x, self.wr, self.b, self.w1, self.w2, self.w1s, self.w2s,
-                                      self.y, self.idx, self.gate, self.ws)
+                                      self.y, self.idx, self.gate, self.ws, events=events)
 
         def stages(self):
             """Stage entry points, in layer order (for per-stage timing)."""
@@ -121,33 +155,62 @@ def main():
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / reps
 
+    if args.mode == "copy":
+        n = args.copy_mib << 20
+        a = torch.ones(n // 2, dtype=torch.bfloat16, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(args.warmup):
+            b.copy_(a)
+        ms = time_calls(lambda: b.copy_(a), args.steps)
+        print(json.dumps({"mode": "copy", "bytes_read_per_launch": n, "bytes_written_per_launch": n,
+                          "avg_us": round(ms * 1e3, 2), "gbs": round(2 * n / (ms * 1e-3) / 1e9, 1)}), flush=True)
+        return
+
     cfg = get_config(args.config)
     lay = Layer(cfg)
+
+    if args.mode == "gemm":
+        st = lay.stages()
+        st["route"]()
+        st["permute"]()
+        for _ in range(args.warmup):
+            st["grouped_mlp"]()
+        ms = time_calls(st["grouped_mlp"], args.steps)
+        print(json.dumps({"mode": "gemm", "workload": cfg.name, "launch_pairs": args.steps + 1 + args.warmup,
+                          "avg_pair_us": round(ms * 1e3, 2)}), flush=True)
+        return
+
     for _ in range(args.warmup):
         lay.forward()
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
+    hev = binding.HipEvents(3 * args.steps)
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     wall0 = time.perf_counter()
     ev0.record(stream)
-    for _ in range(args.steps):
-        lay.forward()
+    for i in range(args.steps):
+        lay.forward(hev.handles[3 * i:3 * i + 3])
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     ms = ev0.elapsed_time(ev1) / args.steps
     value = cfg.T / (ms * 1e-3)
+    fc1_ms = sum(hev.elapsed_ms(3 * i, 3 * i + 1) for i in range(args.steps)) / args.steps
+    fc2_ms = sum(hev.elapsed_ms(3 * i + 1, 3 * i + 2) for i in range(args.steps)) / args.steps
+    hev.close()
 
     # Per-stage times (the stage entry points run the same kernels).
     stages_ms = {k: time_calls(f, args.stage_reps) for k, f in lay.stages().items()}
-    gemm_ms = stages_ms["grouped_mlp"]
+    gemm_ms = fc1_ms + fc2_ms
     routed_flops = 4.0 * cfg.T * cfg.K * cfg.d * cfg.h
     achieved = routed_flops / (gemm_ms * 1e-3) / 1e12
     roofline = {
-        "kernel": "routed grouped GEMM: fc1+GELU and fc2 kernels of one moe_grouped_mlp call",
+        "kernel": "routed grouped GEMM: the fc1+GELU and fc2 kernels of one layer step",
         "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-        "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+        "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic_bytes(cfg.name),
         "algorithmic_flops_per_launch": routed_flops, "avg_launch_us": round(gemm_ms * 1e3, 2),
+        "fc1_us": round(fc1_ms * 1e3, 2), "fc2_us": round(fc2_ms * 1e3, 2),
+        "timing": "HIP events recorded by moe_layer_forward on its stream around fc1 and fc2, every timed step",
     }
     layer_flops = cfg.gemm_flops()
 
@@ -171,18 +234,29 @@ def main():
         si = Layer(c5)
         for _ in range(3):
             si.forward()
-        si_ms = time_calls(si.forward, max(args.steps, 20))
+        reps = max(args.steps, 20)
+        hev = binding.HipEvents(3 * reps)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for i in range(reps):
+            si.forward(hev.handles[3 * i:3 * i + 3])
+        e1.record(stream)
+        torch.cuda.synchronize()
+        si_ms = e0.elapsed_time(e1) / reps
+        si_gemm_ms = sum(hev.elapsed_ms(3 * i, 3 * i + 2) for i in range(reps)) / reps
+        hev.close()
         si_stages = {k: time_calls(f, max(args.stage_reps, 20)) for k, f in si.stages().items()}
         w_bytes = c5.routed_weight_bytes()
-        gbs = w_bytes / (si_stages["grouped_mlp"] * 1e-3) / 1e9
+        gbs = w_bytes / (si_gemm_ms * 1e-3) / 1e9
         out["single_image"] = {
             "workload": c5.name, "tokens": c5.T, "us_per_layer": round(si_ms * 1e3, 1),
             "tokens_per_s": round(c5.T / (si_ms * 1e-3), 1),
             "roofline": {"kernel": "routed grouped GEMM (fc1+fc2), expert weights read once", "bound": "hbm",
                          "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                         "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": None,
+                         "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": traffic_bytes(c5.name),
                          "algorithmic_bytes_per_launch": w_bytes,
-                         "avg_launch_us": round(si_stages["grouped_mlp"] * 1e3, 2)},
+                         "avg_launch_us": round(si_gemm_ms * 1e3, 2)},
             "layer_weight_gbs": round((w_bytes + c5.shared_weight_bytes()) / (si_ms * 1e-3) / 1e9, 1),
             "stages_us": {k: round(v * 1e3, 1) for k, v in si_stages.items()},
         }

@@ -148,12 +148,15 @@ moe_status_t moe_combine(const moe_desc_t *desc, const void *expert_out, const f
  *   y [T, d] layer dtype out
  *   topk_idx_out [T, K] int32 and topk_gate_out [T, K] fp32: optional
  *   copies of the routing (NULL = not returned)
+ *   events: NULL, or three hipEvent_t (created by the caller) recorded on
+ *   `stream` right before the routed fc1 launch, between fc1 and fc2, and
+ *   right after fc2, to time the grouped expert GEMMs inside the layer
  * The shared expert's output stays fp32 until the combine. */
 moe_status_t moe_layer_forward(const moe_desc_t *desc, const void *x, const void *w_router,
                                const float *bias, const void *w1, const void *w2,
                                const void *w1s, const void *w2s, void *y, int32_t *topk_idx_out,
                                float *topk_gate_out, void *workspace, size_t workspace_bytes,
-                               void *stream);
+                               void *const *events, void *stream);
 
 #ifdef __cplusplus
 }

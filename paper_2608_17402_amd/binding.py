@@ -80,7 +80,7 @@ def load(path: Optional[str] = None):
     lib.moe_grouped_mlp.restype = st
     lib.moe_combine.argtypes = [D, P, P, P, P, P]
     lib.moe_combine.restype = st
-    lib.moe_layer_forward.argtypes = [D, P, P, P, P, P, P, P, P, P, P, P, S, P]
+    lib.moe_layer_forward.argtypes = [D, P, P, P, P, P, P, P, P, P, P, P, S, P, P]
     lib.moe_layer_forward.restype = st
     if path is None:
         _lib = lib
@@ -163,12 +163,46 @@ def moe_combine(desc, expert_out, topk_gate, shared_out, y, stream=None):
 
 
 def moe_layer_forward(desc, x, w_router, bias, w1, w2, w1s, w2s, y, topk_idx_out=None, topk_gate_out=None,
-                      workspace=None, stream=None):
+                      workspace=None, stream=None, events=None):
+    """events: None or three raw hipEvent_t handles (ints) recorded before the
+    routed fc1, between fc1 and fc2, and after fc2."""
     dt = torch_dtype(desc)
+    ev = None
+    if events is not None:
+        if len(events) != 3:
+            raise ValueError("events must hold three hipEvent_t handles")
+        ev = (ctypes.c_void_p * 3)(*events)
     _check(load().moe_layer_forward(ctypes.byref(desc), _ptr(x, "x", dt), _ptr(w_router, "w_router", dt),
                                     _ptr(bias, "bias", torch.float32), _ptr(w1, "w1", dt), _ptr(w2, "w2", dt),
                                     _ptr(w1s, "w1s", dt), _ptr(w2s, "w2s", dt), _ptr(y, "y", dt),
                                     _ptr(topk_idx_out, "topk_idx_out", torch.int32),
                                     _ptr(topk_gate_out, "topk_gate_out", torch.float32),
-                                    _ptr(workspace, "workspace"), workspace.numel(), _stream(stream)),
+                                    _ptr(workspace, "workspace"), workspace.numel(), ev, _stream(stream)),
            "moe_layer_forward")
+
+
+class HipEvents:
+    """Raw HIP events through the HIP runtime (timing only)."""
+
+    def __init__(self, n: int):
+        self._hip = ctypes.CDLL("libamdhip64.so")
+        self._hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self._hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self._hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.handles = []
+        for _ in range(n):
+            h = ctypes.c_void_p()
+            if self._hip.hipEventCreate(ctypes.byref(h)) != 0:
+                raise RuntimeError("hipEventCreate failed")
+            self.handles.append(h.value)
+
+    def elapsed_ms(self, a: int, b: int) -> float:
+        ms = ctypes.c_float()
+        if self._hip.hipEventElapsedTime(ctypes.byref(ms), self.handles[a], self.handles[b]) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return ms.value
+
+    def close(self):
+        for h in self.handles:
+            self._hip.hipEventDestroy(h)
+        self.handles = []

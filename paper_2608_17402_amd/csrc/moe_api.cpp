@@ -179,10 +179,12 @@ static moe_status_t enqueue_route(const moe_desc_t& d, const WorkspacePlan& p, v
 // fc2 scattered to slot order.
 static moe_status_t enqueue_routed_mlp(const moe_desc_t& d, const WorkspacePlan& p, void* ws, const void* x,
                                        const int32_t* sorted_slots, const int32_t* offsets, const void* w1,
-                                       const void* w2, void* expert_out, hipStream_t s) {
+                                       const void* w2, void* expert_out, hipStream_t s,
+                                       void* const* events = nullptr) {
     TileDesc* tiles = region<TileDesc>(ws, p.tiles);
     int32_t* ntiles = region<int32_t>(ws, p.ntiles);
     HIP_CHECK(launch_build_tiles(d.E, p.tile_bm, p.max_tiles, offsets, tiles, ntiles, s), "build_tiles");
+    if (events) HIP_CHECK(hipEventRecord(static_cast<hipEvent_t>(events[0]), s), "event record");
     GemmArgs g{};
     g.A = x;
     g.B = w1;
@@ -198,6 +200,7 @@ static moe_status_t enqueue_routed_mlp(const moe_desc_t& d, const WorkspacePlan&
     g.b_group_stride = (int64_t)d.h * d.d;
     g.a_bytes = (uint32_t)((size_t)d.T * d.d * elem_size(d.dtype));
     HIP_CHECK(launch_gemm(d, EPI_GELU_STORE, p.tile_bm, g, s), "fc1 grouped gemm");
+    if (events) HIP_CHECK(hipEventRecord(static_cast<hipEvent_t>(events[1]), s), "event record");
     GemmArgs g2 = g;
     g2.A = region<void>(ws, p.act);
     g2.B = w2;
@@ -208,6 +211,7 @@ static moe_status_t enqueue_routed_mlp(const moe_desc_t& d, const WorkspacePlan&
     g2.b_group_stride = (int64_t)d.d * d.h;
     g2.a_bytes = (uint32_t)((size_t)d.T * d.K * d.h * elem_size(d.dtype));
     HIP_CHECK(launch_gemm(d, EPI_SCATTER_SLOT, p.tile_bm, g2, s), "fc2 grouped gemm");
+    if (events) HIP_CHECK(hipEventRecord(static_cast<hipEvent_t>(events[2]), s), "event record");
     return MOE_OK;
 }
 
@@ -331,7 +335,8 @@ MOE_API moe_status_t moe_combine(const moe_desc_t* desc, const void* expert_out,
 MOE_API moe_status_t moe_layer_forward(const moe_desc_t* desc, const void* x, const void* w_router,
                                        const float* bias, const void* w1, const void* w2, const void* w1s,
                                        const void* w2s, void* y, int32_t* topk_idx_out, float* topk_gate_out,
-                                       void* workspace, size_t workspace_bytes, void* stream) {
+                                       void* workspace, size_t workspace_bytes, void* const* events,
+                                       void* stream) {
     CHECK(check_desc(desc));
     const moe_desc_t& d = *desc;
     CHECK(check_ptr(x, "x"));
@@ -346,6 +351,8 @@ MOE_API moe_status_t moe_layer_forward(const moe_desc_t* desc, const void* x, co
     CHECK(check_ptr(y, "y"));
     CHECK(check_ptr(topk_idx_out, "topk_idx_out", true));
     CHECK(check_ptr(topk_gate_out, "topk_gate_out", true));
+    if (events && (!events[0] || !events[1] || !events[2]))
+        return fail(MOE_ERR_INVALID_ARG, "events must hold three events");
     WorkspacePlan p;
     CHECK(check_ws(d, workspace, workspace_bytes, &p));
     hipStream_t s = static_cast<hipStream_t>(stream);
@@ -363,7 +370,7 @@ MOE_API moe_status_t moe_layer_forward(const moe_desc_t* desc, const void* x, co
     HIP_CHECK(launch_permute(d, idx, counts, offsets, slots, region<int32_t>(workspace, p.blockhist),
                              p.n_hist_blocks, s),
               "permute");
-    CHECK(enqueue_routed_mlp(d, p, workspace, x, slots, offsets, w1, w2, eout, s));
+    CHECK(enqueue_routed_mlp(d, p, workspace, x, slots, offsets, w1, w2, eout, s, events));
     if (d.h_shared) CHECK(enqueue_shared_mlp(d, p, workspace, x, w1s, w2s, sout, s));
     HIP_CHECK(launch_combine(d, eout, gate, sout, 1, y, s), "combine");
     return ok();

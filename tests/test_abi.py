@@ -100,7 +100,12 @@ def test_entry_points_reject_bad_pointers_before_any_launch(lib):
     assert lib.moe_grouped_mlp(d, fake, fake, fake, fake, None, fake, fake, S(need), None) == 1
     assert lib.moe_combine(d, fake, None, None, fake, None) == 1
     assert lib.moe_layer_forward(d, fake, fake, None, fake, fake, None, fake, fake, None, None, fake,
-                                 S(need), None) == 1  # shared weights required when h_shared > 0
+                                 S(need), None, None) == 1  # shared weights required when h_shared > 0
     bad = binding.make_desc(100, 64, 8, 0, 64)
     assert lib.moe_layer_forward(ctypes.byref(bad), fake, fake, None, fake, fake, None, None, fake, None,
-                                 None, fake, S(need), None) == 1
+                                 None, fake, S(need), None, None) == 1
+    half = (ctypes.c_void_p * 3)(1 << 20, 1 << 21, None)
+    desc0 = binding.make_desc(100, 64, 8, 2, 64, 0, 1.0, "bf16")
+    assert lib.moe_layer_forward(ctypes.byref(desc0), fake, fake, None, fake, fake, None, None, fake, None,
+                                 None, fake, S(need), half, None) == 1
+    assert b"events" in lib.moe_last_error()
