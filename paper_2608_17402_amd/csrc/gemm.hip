@@ -135,13 +135,6 @@ __device__ __forceinline__ void copy16_to_lds(__amdgpu_buffer_rsrc_t r, uint32_t
                                              (int)soff, 0, 0);
 }
 
-// 4 bytes per lane into LDS scratch: used only to pull a cache line into L2
-// ahead of the real copy (the LDS bytes are never read).
-__device__ __forceinline__ void touch_line(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, uint8_t* lds) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 4, (int)voff,
-                                             (int)soff, 0, 0);
-}
-
 __device__ __forceinline__ uint32_t lds_address(const uint8_t* p) {
     return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) uint8_t*)p);
 }
@@ -157,6 +150,16 @@ __device__ __forceinline__ bf16x8_t lds_read16(uint32_t addr) {
     return r;
 }
 __device__ __forceinline__ void tie(bf16x8_t& v) { asm volatile("" : "+v"(v)); }
+
+// Lanes of one wave handing data to each other through LDS: orders the
+// writes before the reads (and the reads before the next writes) for every
+// lane. Without it the compiler may treat the exchange as a data race and
+// move a lane's reads away from the other lanes' writes.
+__device__ __forceinline__ void wave_sync_lds() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
 
 // bf16 grouped / dense GEMM, C[m, n] = sum_k X[m, k] W[n, k], fp32 accumulation.
 //
@@ -175,8 +178,7 @@ __device__ __forceinline__ void tie(bf16x8_t& v) { asm volatile("" : "+v"(v)); }
 // swizzle puts the 16 rows read together by a quarter-wave of a fragment read
 // on 16 distinct 16-byte bank groups of the 64-bank LDS. Fragments for the
 // next 16-wide K step are read while the MFMAs of the current one run.
-template <int BM, int BN, int WAVES_M, int WAVES_N, int BK, int STAGES, int EPI, bool GROUPED, int WPE,
-          int WARM>
+template <int BM, int BN, int WAVES_M, int WAVES_N, int BK, int STAGES, int EPI, bool GROUPED, int WPE>
 __global__ __launch_bounds__(WAVES_M* WAVES_N* kWave) __attribute__((amdgpu_waves_per_eu(WPE, 8)))
 void k_gemm_bf16(const GemmArgs a) {
     constexpr int NW = WAVES_M * WAVES_N;
@@ -199,13 +201,6 @@ void k_gemm_bf16(const GemmArgs a) {
     static_assert(STAGES >= 2 && STAGES <= 5, "2 to 5 stages");
     __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES * STAGE];
     __shared__ int32_t srow[BM];
-    // L2 warm-up: slab kt + STAGES - 1 + WARM is touched (one 4-byte load per
-    // 128-byte row piece) while slab kt + STAGES - 1 is copied, so its lines
-    // are already in L2 when their copy is issued. WR pieces of 64 rows per wave.
-    constexpr int WROWS = (BM + BN) * (BK * 2 / 128);  // 128-byte lines per slab
-    constexpr int WR = WARM > 0 ? (WROWS / kWave + NW - 1) / NW : 0;
-    __shared__ __attribute__((aligned(256))) uint8_t wscratch[WARM > 0 ? NW * kWave * 4 : 4];
-
     const TileCoord tc = locate_tile<GROUPED>(a, BM, BN);
     if (!tc.valid) return;
     const int tid = threadIdx.x;
@@ -252,29 +247,6 @@ void k_gemm_bf16(const GemmArgs a) {
         wv[i] = (uint32_t)(tc.n0 + r) * (uint32_t)(Kd * 2) + c * 16;
     }
 
-    // Warm-up addresses: line q of the slab is row q / LPR of the tile (token
-    // rows first, then weight rows), 128-byte piece q % LPR of its K slab.
-    constexpr int LPR = BK * 2 / 128 > 0 ? BK * 2 / 128 : 1;
-    uint32_t wmv[WR > 0 ? WR : 1];
-    bool wmx[WR > 0 ? WR : 1];
-#pragma unroll
-    for (int i = 0; i < WR; ++i) {
-        const int q = (wave + NW * i) * kWave + lane;
-        const int r = (q / LPR) < BM + BN ? q / LPR : BM + BN - 1;
-        const int piece = q % LPR;
-        if (r < BM) {
-            int xrow;
-            if (EPI == EPI_GELU_STORE) xrow = srow[r];
-            else xrow = tc.row0 + (r < tc.rows ? r : tc.rows - 1);
-            wmv[i] = (uint32_t)xrow * (uint32_t)(Kd * 2) + piece * 128;
-            wmx[i] = true;
-        } else {
-            wmv[i] = (uint32_t)(tc.n0 + r - BM) * (uint32_t)(Kd * 2) + piece * 128;
-            wmx[i] = false;
-        }
-    }
-    (void)wmx;
-
     f32x16_t acc[FN][FM];
 #pragma unroll
     for (int j = 0; j < FN; ++j)
@@ -307,16 +279,6 @@ void k_gemm_bf16(const GemmArgs a) {
 #pragma unroll
         for (int i = 0; i < BP; ++i) copy16_to_lds(wres, wv[i], soff, buf + BM * ROWB + (wave + NW * i) * 1024);
     };
-    auto warm = [&](int kslab) {
-        const uint32_t soff = (uint32_t)kslab * BK * 2;
-#pragma unroll
-        for (int i = 0; i < WR; ++i) {
-            // A wave's line group never mixes token and weight rows when BM is
-            // a multiple of 64 / LPR lines; wmx is uniform across the wave.
-            if (wmx[i]) touch_line(xres, wmv[i], soff, wscratch + wave * kWave * 4);
-            else touch_line(wres, wmv[i], soff, wscratch + wave * kWave * 4);
-        }
-    };
     auto read_frags = [&](uint32_t sbase, int ks, bf16x8_t* xf, bf16x8_t* wf) {
         const uint32_t xa = xoff[ks] + sbase, wa = woff[ks] + sbase;
         if constexpr (FM >= 1) xf[0] = lds_read16<0 * 32 * ROWB>(xa);
@@ -340,39 +302,20 @@ void k_gemm_bf16(const GemmArgs a) {
 #pragma unroll
     for (int sl = 0; sl < STAGES - 1; ++sl)
         if (sl < nk) issue(sl, sl);
-    if constexpr (WARM > 0) {
-#pragma unroll
-        for (int sl = STAGES - 1; sl < STAGES - 1 + WARM; ++sl)
-            if (sl < nk) warm(sl);
-    }
 
     int cur_stage = 0;
     for (int kt = 0; kt < nk; ++kt) {
-        // Slab kt must have landed; later prefetched slabs and the warm-up
-        // touches issued after it stay in flight.
+        // Slab kt must have landed; later prefetched slabs stay in flight.
         const int ahead = min(nk - 1 - kt, STAGES - 2);
-        // Touch groups issued after slab kt's copies: the prologue issues WARM
-        // of them after slab 0; every later step issues one after its copy.
-        const int warms = WARM == 0 ? 0 : (kt == 0 ? min(nk - 1, WARM) : (kt + WARM < nk ? 1 : 0));
-        if constexpr (WARM == 0) {
-            if constexpr (STAGES >= 4) { if (ahead >= 2) { wait_vmcnt<2 * (AP + BP)>(); goto waited; } }
-            if constexpr (STAGES >= 3) { if (ahead >= 1) { wait_vmcnt<AP + BP>(); goto waited; } }
-            wait_vmcnt<0>();
-        } else {
-            static_assert(STAGES == 2, "warm-up is used with two stages");
-            if (warms >= 2) { wait_vmcnt<2 * WR>(); goto waited; }
-            if (warms >= 1) { wait_vmcnt<WR>(); goto waited; }
-            wait_vmcnt<0>();
-        }
+        if constexpr (STAGES >= 4) { if (ahead >= 2) { wait_vmcnt<2 * (AP + BP)>(); goto waited; } }
+        if constexpr (STAGES >= 3) { if (ahead >= 1) { wait_vmcnt<AP + BP>(); goto waited; } }
+        wait_vmcnt<0>();
     waited:
         barrier_no_fence();
         if (kt + STAGES - 1 < nk) {
             int st = cur_stage + STAGES - 1;
             if (st >= STAGES) st -= STAGES;
             issue(st, kt + STAGES - 1);
-        }
-        if constexpr (WARM > 0) {
-            if (kt + STAGES - 1 + WARM < nk) warm(kt + STAGES - 1 + WARM);
         }
         const uint32_t sbase = cur_stage * STAGE;
         bf16x8_t xf[2][FM], wf[2][FN];
@@ -427,8 +370,8 @@ void k_gemm_bf16(const GemmArgs a) {
                     *reinterpret_cast<uint2*>(dst) = pack4_bf16(v0, v1, v2, v3);
                 }
             }
-        // Each wave reads back only its own area (no barrier needed; the
-        // compiler orders the wave's LDS write -> read).
+        // Each wave reads back only its own area: a wave-level sync suffices.
+        wave_sync_lds();
 #pragma unroll
         for (int k = 0; k < PIECES; ++k) {
             const int q = lane + kWave * k;
@@ -441,6 +384,7 @@ void k_gemm_bf16(const GemmArgs a) {
                 *reinterpret_cast<uint4*>(out) = v;
             }
         }
+        wave_sync_lds();
     }
 }
 
@@ -513,20 +457,13 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const GemmArgs a) {
     }
 }
 
-#ifndef MOE_GEMM_WARM
-#define MOE_GEMM_WARM 0
-#endif
-#ifndef MOE_BIG_CFG
-#define MOE_BIG_CFG 0
-#endif
 
 template <int BM, int BN, int WM, int WN, int BK, int ST, int WPE, int EPI, bool GROUPED>
 hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
-    constexpr int WARM = ST == 2 ? MOE_GEMM_WARM : 0;
     const int n_n = a.N / BN;
     const long long total = (long long)a.max_tiles * n_n;
     const long long grid = (total + kNumXcd - 1) / kNumXcd * kNumXcd;
-    hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, BK, ST, EPI, GROUPED, WPE, WARM>), dim3((unsigned)grid),
+    hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, BK, ST, EPI, GROUPED, WPE>), dim3((unsigned)grid),
                        dim3(WM * WN * kWave), 0, s, a);
     return hipGetLastError();
 }
@@ -553,11 +490,6 @@ hipError_t launch_f32(const GemmArgs& a, hipStream_t s) {
 template <int EPI, bool GROUPED>
 hipError_t dispatch_bf16(int bm, const GemmArgs& a, hipStream_t s) {
     if (bm == 256) {
-#if MOE_BIG_CFG == 1
-        if (a.N % 128 == 0) return launch_bf16<256, 128, 2, 2, 32, 2, 2, EPI, GROUPED>(a, s);
-#elif MOE_BIG_CFG == 2
-        if (a.N % 128 == 0) return launch_bf16<256, 128, 2, 2, 32, 3, 2, EPI, GROUPED>(a, s);
-#endif
         if (a.N % 256 == 0) return launch_bf16<256, 256, 2, 4, 64, 2, 1, EPI, GROUPED>(a, s);
         if (a.N % 128 == 0) return launch_bf16<256, 128, 2, 2, 64, 2, 1, EPI, GROUPED>(a, s);
         return launch_bf16<256, 64, 4, 1, 64, 2, 1, EPI, GROUPED>(a, s);

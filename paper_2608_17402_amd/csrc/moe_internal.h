@@ -60,7 +60,7 @@ struct GemmArgs {
 // Offsets (bytes) of every workspace region for one descriptor.
 struct WorkspacePlan {
     size_t idx, gate, scores, counts, offsets, slots, blockhist, tiles, ntiles;
-    size_t xnorm, wnorm, ovf;
+    size_t xnorm, wnorm, ovf, cand, ncand;
     size_t act, eout, sact, sout;
     size_t total;
     int32_t n_hist_blocks;   // blocks of the permute histogram / scatter
@@ -82,10 +82,13 @@ hipError_t launch_topk(const moe_desc_t& d, const float* scores, const float* bi
                        int32_t* topk_idx, float* topk_gate, hipStream_t s);
 // Fast-router tail: norms, candidate repair with exact recomputation, and the
 // exact fallback for tokens with too many candidates. s_fast = MFMA logits.
+// cand [T][router_cand_slots(K)] and ncand [T] are scratch of the candidate
+// pass.
 hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, const void* x,
                                      const void* w_router, const float* bias, float* xnorm, float* wnorm,
-                                     int32_t* ovf_count, int32_t* ovf_list, int32_t* topk_idx,
-                                     float* topk_gate, hipStream_t s);
+                                     uint16_t* cand, int32_t* ncand, int32_t* ovf_count, int32_t* ovf_list,
+                                     int32_t* topk_idx, float* topk_gate, hipStream_t s);
+int router_cand_slots(int K);
 hipError_t launch_permute(const moe_desc_t& d, const int32_t* topk_idx, int32_t* counts,
                           int32_t* offsets, int32_t* sorted_slots, int32_t* blockhist,
                           int32_t n_blocks, hipStream_t s);

@@ -12,6 +12,8 @@
 
 #include <math.h>
 
+#include <type_traits>
+
 namespace moe {
 namespace {
 
@@ -232,10 +234,17 @@ __global__ __launch_bounds__(256) void k_topk(const float* __restrict__ scores,
 // lower bound of the true K-th key, so any expert whose upper end is below L
 // cannot be selected. The remaining candidates (a dozen or so per token) are
 // recomputed with the exact chain and selected exactly as on the exact path:
-// indices and gates are identical bit for bit. A token with more than
-// kMaxCand candidates is queued and routed by the exact all-experts kernel.
+// indices and gates are identical bit for bit. A token with more candidates
+// than its slots (16, or 32 when K > 8) is queued and routed by the exact
+// all-experts kernel.
+//
+// The interval test itself uses a cheap sigmoid (hardware exp2 and
+// reciprocal, absolute error below 1e-6 for every input, covered by extra
+// slack in the half-width); only the candidates go through recipe S.
 
-constexpr int kMaxCand = 32;
+__device__ __forceinline__ float sigmoid_fast(float s) {
+    return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-s * kLog2e));
+}
 
 // Upper bound of the 2-norm of every row of a [rows, d] bf16 matrix (fp32 sum
 // of squares, inflated to cover its rounding). One wave per row. Block 0 also
@@ -259,236 +268,282 @@ __global__ __launch_bounds__(256) void k_row_norms(const bf16_t* __restrict__ a,
     if (lane == 0) out[row] = sqrtf(acc) * 1.001f + 1e-30f;
 }
 
-// Candidate selection, exact recomputation of the candidates, exact top-K for
-// RB consecutive tokens per block of 512 threads. The router weights stream
-// through LDS in chunks of DC columns, double-buffered through registers, so
-// each block reads them once; x rows of the block come along in the same
-// chunks.
-constexpr int kRepairThreads = 512;
-constexpr int kRepairWaves = kRepairThreads / kWave;
-
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
-template <int RB, int DC, int EMAX, int PER>
-__global__ __launch_bounds__(kRepairThreads) void k_router_repair(
-    const float* __restrict__ s_fast, const float* __restrict__ xnorm, const float* __restrict__ wnorm,
-    const float* __restrict__ bias, const bf16_t* __restrict__ x, const bf16_t* __restrict__ wr, int T,
-    int d, int E, int K, float cst, int32_t* __restrict__ topk_idx, float* __restrict__ topk_gate,
-    int32_t* __restrict__ ovf_count, int32_t* __restrict__ ovf_list) {
-    __shared__ uint16_t cand[RB][kMaxCand];
-    __shared__ int ncand[RB];
-    __shared__ int poff[RB + 1];
-    __shared__ uint8_t ptok[RB * kMaxCand];
-    __shared__ float sex[RB * kMaxCand];
-    __shared__ __attribute__((aligned(16))) bf16_t xs[2][RB][DC];
-    __shared__ __attribute__((aligned(16))) bf16_t ws[2][EMAX][DC];
-
+// Candidates of each token: LPA lanes per token, lane g holding experts
+// g, g + LPA, ... (PER of them). L = the K-th largest lower end of the key
+// intervals; the candidates are the experts whose upper end reaches L, written
+// to cand[t][0 .. NS) with their count in ncand[t]. A token with more than NS
+// candidates gets ncand = -1 and is appended to the overflow queue.
+template <int LPA, int PER, int NS>
+__global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s_fast,
+                                                    const float* __restrict__ xnorm,
+                                                    const float* __restrict__ wnorm,
+                                                    const float* __restrict__ bias, int T, int E, int K,
+                                                    float cst, uint16_t* __restrict__ cand,
+                                                    int32_t* __restrict__ ncand, int32_t* __restrict__ ovf_count,
+                                                    int32_t* __restrict__ ovf_list) {
+    static_assert(LPA <= kWave && kWave % LPA == 0, "token groups inside a wave");
     const int lane = threadIdx.x & (kWave - 1);
-    const int wave = threadIdx.x / kWave;
-    const int t0 = blockIdx.x * RB;
+    const int g = lane % LPA;
+    const int t = blockIdx.x * (256 / LPA) + threadIdx.x / LPA;
+    const bool live = t < T;  // uniform within the group: dead groups compute on -inf
+    const uint64_t grp = (LPA == kWave ? ~0ull : ((1ull << LPA) - 1ull)) << (lane - g);
+    const uint64_t below = grp & ((1ull << lane) - 1ull);
 
-    // Phase A: candidates of each token (a wave per token); lane l holds
-    // experts l, l + 64, ... (PER of them).
-    for (int tl = wave; tl < RB; tl += kRepairWaves) {
-        const int t = t0 + tl;
-        if (t >= T) {
-            if (lane == 0) ncand[tl] = 0;
-            continue;
-        }
-        const float xn = xnorm[t];
-        float lo[PER], hi[PER];
+    const float xn = live ? xnorm[t] : 0.0f;
+    float lo[PER], hi[PER];
 #pragma unroll
-        for (int m = 0; m < PER; ++m) {
-            const int e = lane + kWave * m;
-            lo[m] = -INFINITY;
-            hi[m] = -INFINITY;
-            if (e < E) {
-                const float b = bias ? bias[e] : 0.0f;
-                const float key = sigmoid_fp32(s_fast[(size_t)t * E + e]) + b;
-                const float delta = 0.25f * (cst * xn * wnorm[e]) + 2e-6f + 1e-6f * fabsf(b);
-                lo[m] = key - delta;
-                hi[m] = key + delta;
-            }
+    for (int m = 0; m < PER; ++m) {
+        const int e = g + LPA * m;
+        lo[m] = -INFINITY;
+        hi[m] = -INFINITY;
+        if (live && e < E) {
+            const float b = bias ? bias[e] : 0.0f;
+            const float key = sigmoid_fast(s_fast[(size_t)t * E + e]) + b;
+            const float delta = 0.25f * (cst * xn * wnorm[e]) + 4e-6f + 1e-6f * fabsf(b);
+            lo[m] = key - delta;
+            hi[m] = key + delta;
         }
-        // L = K-th largest lower end (a lower bound of the true K-th key).
-        uint32_t taken = 0;
-        float L = -INFINITY;
-        for (int j = 0; j < K; ++j) {
-            float bv = -INFINITY;
-            int bm = -1;
-#pragma unroll
-            for (int m = 0; m < PER; ++m)
-                if (!((taken >> m) & 1u) && lo[m] > bv) {
-                    bv = lo[m];
-                    bm = m;
-                }
-            float wvmax = bv;
-#pragma unroll
-            for (int off = kWave / 2; off > 0; off >>= 1) wvmax = fmaxf(wvmax, __shfl_xor(wvmax, off));
-            const uint64_t holders = __ballot(bm >= 0 && bv == wvmax);
-            const int first = __ffsll((unsigned long long)holders) - 1;
-            if (lane == first) taken |= 1u << bm;
-            L = wvmax;
-        }
-        // Candidates: upper end >= L, gathered in expert order.
-        int nc = 0;
-#pragma unroll
-        for (int m = 0; m < PER; ++m) {
-            const bool c = hi[m] >= L;
-            const uint64_t bal = __ballot(c);
-            if (c) {
-                const int pos = nc + __popcll(bal & ((1ull << lane) - 1ull));
-                if (pos < kMaxCand) cand[tl][pos] = (uint16_t)(lane + kWave * m);
-            }
-            nc += __popcll(bal);
-        }
-        if (nc > kMaxCand) {
-            if (lane == 0) {
-                const int slot = atomicAdd(ovf_count, 1);
-                ovf_list[slot] = t;
-            }
-            nc = 0;
-        }
-        if (lane == 0) ncand[tl] = nc;
     }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        int run = 0;
-        for (int tl = 0; tl < RB; ++tl) {
-            poff[tl] = run;
-            run += ncand[tl];
-        }
-        poff[RB] = run;
+    // L: the K-th largest of the lanes' two largest lower ends. These are a
+    // subset of all lower ends, so L is at most the K-th largest lower end and
+    // still a lower bound of the true K-th key; it equals it unless one lane
+    // holds three or more of the K largest.
+    float t1 = -INFINITY, t2 = -INFINITY;
+#pragma unroll
+    for (int m = 0; m < PER; ++m) {
+        const float v = lo[m];
+        t2 = fmaxf(t2, fminf(t1, v));
+        t1 = fmaxf(t1, v);
     }
-    __syncthreads();
-    for (int tl = wave; tl < RB; tl += kRepairWaves)
-        for (int j = lane; j < ncand[tl]; j += kWave) ptok[poff[tl] + j] = (uint8_t)tl;
-    const int P = poff[RB];
+    float L = -INFINITY;
+    int used = 0;  // 0: t1 and t2 available, 1: t2 available, 2: none
+    for (int j = 0; j < K; ++j) {
+        const float mine = used == 0 ? t1 : (used == 1 ? t2 : -INFINITY);
+        float gmax = mine;
+#pragma unroll
+        for (int off = LPA / 2; off > 0; off >>= 1) gmax = fmaxf(gmax, __shfl_xor(gmax, off));
+        const uint64_t holders = __ballot(used < 2 && mine == gmax) & grp;
+        if (holders && lane == __ffsll((unsigned long long)holders) - 1) ++used;
+        L = gmax;
+    }
+    int nc = 0;
+#pragma unroll
+    for (int m = 0; m < PER; ++m) {
+        const bool c = live && hi[m] >= L;
+        const uint64_t bal = __ballot(c) & grp;
+        if (c) {
+            const int pos = nc + __popcll(bal & below);
+            if (pos < NS) cand[(size_t)t * NS + pos] = (uint16_t)(g + LPA * m);
+        }
+        nc += __popcll(bal);
+    }
+    if (live && g == 0) {
+        if (nc > NS) {
+            const int slot = atomicAdd(ovf_count, 1);
+            ovf_list[slot] = t;
+            nc = -1;
+        }
+        ncand[t] = nc;
+    }
+}
 
-    // Phase B: exact logits of every (token, candidate) pair, one FMA chain per
-    // pair over the model width in ascending order.
-    constexpr int KP = RB * kMaxCand / kRepairThreads;
-    constexpr int CPR = DC / 8;                       // 16-byte chunks per staged row
-    constexpr int XQ = (RB * CPR + kRepairThreads - 1) / kRepairThreads;
-    constexpr int WQ = (EMAX * CPR + kRepairThreads - 1) / kRepairThreads;
-    float acc[KP];
+// Exact logits of the candidates, recipe S, exact top-K and gates. LPT lanes
+// per token, each running CPL candidate chains (slots g, g + LPT, ...) side by
+// side: one fused multiply-add chain per candidate over the model width, in
+// ascending order. The block's tokens stream their x rows from global memory;
+// the router weights of every expert stream through LDS in chunks of DC
+// columns (bf16, rows padded by 16 bytes against bank conflicts, widened to
+// fp32 in registers), double-buffered with one barrier per chunk. Tokens
+// queued by the candidate kernel are skipped.
+template <int TPB, int LPT, int CPL, int EMAX, int DC>
+__global__ __launch_bounds__(TPB* LPT) void k_router_chain(const bf16_t* __restrict__ x,
+                                                         const bf16_t* __restrict__ wr,
+                                                         const float* __restrict__ bias,
+                                                         const uint16_t* __restrict__ cand,
+                                                         const int32_t* __restrict__ ncand, int T, int d, int E,
+                                                         int K, int32_t* __restrict__ topk_idx,
+                                                         float* __restrict__ topk_gate) {
+    constexpr int NT = TPB * LPT;
+    constexpr int NS = LPT * CPL;
+    constexpr int ROW = DC + 8;             // bf16 per LDS row (16 bytes of padding)
+    constexpr int XQ = DC / 8;              // 16-byte x pieces per chunk
+    constexpr int WP = EMAX * DC / 8;        // 16-byte router-weight pieces per chunk
+    constexpr int WQ = (WP + NT - 1) / NT;   // per thread
+    static_assert(NS <= 32, "at most 32 candidate slots");
+    constexpr int RING = 2 * EMAX * ROW * 2, SEL = TPB * NS * 8;
+    __shared__ __attribute__((aligned(16))) uint8_t lds[RING > SEL ? RING : SEL];
+    auto wsh = reinterpret_cast<bf16_t(*)[EMAX][ROW]>(lds);
+
+    const int tid = threadIdx.x;
+    const int g = tid % LPT;
+    const int tl = tid / LPT;
+    const int t = blockIdx.x * TPB + tl;
+    int nc = t < T ? ncand[t] : 0;
+    nc = nc < 0 ? 0 : nc;  // queued tokens are routed by the exact-list kernel
+    int ec[CPL];
+    bool on[CPL];
 #pragma unroll
-    for (int k = 0; k < KP; ++k) acc[k] = 0.0f;
+    for (int c = 0; c < CPL; ++c) {
+        const int j = g + LPT * c;
+        on[c] = j < nc;
+        ec[c] = on[c] ? (int)cand[(size_t)t * NS + j] : 0;
+    }
+    const bf16_t* xt = x + (size_t)(t < T ? t : 0) * d;
+
     u32x4_t xr[XQ], wrg[WQ];
-#define MOE_FETCH(d0)                                                                                      \
-    do {                                                                                                   \
-        _Pragma("unroll") for (int i = 0; i < XQ; ++i) {                                                   \
-            const int q = threadIdx.x + kRepairThreads * i;                                                \
-            const int r = q / CPR, c = (q % CPR) * 8;                                                      \
-            xr[i] = (u32x4_t){0u, 0u, 0u, 0u};                                                             \
-            if (q < RB * CPR && t0 + r < T)                                                                \
-                xr[i] = *reinterpret_cast<const u32x4_t*>(x + (size_t)(t0 + r) * d + (d0) + c);            \
-        }                                                                                                  \
-        _Pragma("unroll") for (int i = 0; i < WQ; ++i) {                                                   \
-            const int q = threadIdx.x + kRepairThreads * i;                                                \
-            const int r = q / CPR, c = (q % CPR) * 8;                                                      \
-            if (r < E) wrg[i] = *reinterpret_cast<const u32x4_t*>(wr + (size_t)r * d + (d0) + c);         \
-        }                                                                                                  \
-    } while (0)
-#define MOE_STASH(b)                                                                                       \
-    do {                                                                                                   \
-        _Pragma("unroll") for (int i = 0; i < XQ; ++i) {                                                   \
-            const int q = threadIdx.x + kRepairThreads * i;                                                \
-            if (q < RB * CPR) *reinterpret_cast<u32x4_t*>(&xs[b][q / CPR][(q % CPR) * 8]) = xr[i];         \
-        }                                                                                                  \
-        _Pragma("unroll") for (int i = 0; i < WQ; ++i) {                                                   \
-            const int q = threadIdx.x + kRepairThreads * i;                                                \
-            if (q / CPR < E) *reinterpret_cast<u32x4_t*>(&ws[b][q / CPR][(q % CPR) * 8]) = wrg[i];         \
-        }                                                                                                  \
-    } while (0)
-    MOE_FETCH(0);
-    MOE_STASH(0);
+    auto fetch = [&](int k0) {
+#pragma unroll
+        for (int i = 0; i < XQ; ++i) xr[i] = *reinterpret_cast<const u32x4_t*>(xt + k0 + 8 * i);
+#pragma unroll
+        for (int i = 0; i < WQ; ++i) {
+            const int q = (tid + NT * i) * 8;  // element of the EMAX x DC chunk
+            const int e = q / DC, c = q % DC;
+            wrg[i] = (u32x4_t){0u, 0u, 0u, 0u};
+            if (tid + NT * i < WP && e < E) wrg[i] = *reinterpret_cast<const u32x4_t*>(wr + (size_t)e * d + k0 + c);
+        }
+    };
+    auto stash = [&](int b) {
+#pragma unroll
+        for (int i = 0; i < WQ; ++i) {
+            if (tid + NT * i >= WP) continue;
+            const int q = (tid + NT * i) * 8;
+            *reinterpret_cast<u32x4_t*>(&wsh[b][q / DC][q % DC]) = wrg[i];
+        }
+    };
+
+    float acc[CPL];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) acc[c] = 0.0f;
+
+    // One chunk: for every 8 columns, widen x once and advance each of the
+    // first NC chains by 8 fused multiply-adds (ascending columns).
+    auto chunk = [&](auto NCC, int b) {
+        constexpr int NC = decltype(NCC)::value;
+#pragma unroll
+        for (int i = 0; i < XQ; ++i) {
+            const u32x4_t u = xr[i];
+            const float x0 = __uint_as_float(u.x << 16), x1 = __uint_as_float(u.x & 0xffff0000u);
+            const float x2 = __uint_as_float(u.y << 16), x3 = __uint_as_float(u.y & 0xffff0000u);
+            const float x4 = __uint_as_float(u.z << 16), x5 = __uint_as_float(u.z & 0xffff0000u);
+            const float x6 = __uint_as_float(u.w << 16), x7 = __uint_as_float(u.w & 0xffff0000u);
+#pragma unroll
+            for (int c = 0; c < NC; ++c) {
+                const u32x4_t w = *reinterpret_cast<const u32x4_t*>(&wsh[b][ec[c]][8 * i]);
+                float a = acc[c];
+                a = fmaf(x0, __uint_as_float(w.x << 16), a);
+                a = fmaf(x1, __uint_as_float(w.x & 0xffff0000u), a);
+                a = fmaf(x2, __uint_as_float(w.y << 16), a);
+                a = fmaf(x3, __uint_as_float(w.y & 0xffff0000u), a);
+                a = fmaf(x4, __uint_as_float(w.z << 16), a);
+                a = fmaf(x5, __uint_as_float(w.z & 0xffff0000u), a);
+                a = fmaf(x6, __uint_as_float(w.w << 16), a);
+                a = fmaf(x7, __uint_as_float(w.w & 0xffff0000u), a);
+                acc[c] = a;
+            }
+            // Keep the compiler from hoisting every fragment read of the chunk
+            // (registers, not latency, bound this kernel's occupancy).
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+    int nmax = 0;  // chains any lane of this wave runs (uniform)
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) nmax += __ballot(on[c]) != 0 ? 1 : 0;
+
+    u32x4_t xn[XQ];
+    fetch(0);
+    stash(0);
     __syncthreads();
     int buf = 0;
-    for (int d0 = 0; d0 < d; d0 += DC) {
-        if (d0 + DC < d) MOE_FETCH(d0 + DC);  // next chunk in flight during this one
+    const int nch = d / DC;
+    for (int ch = 0; ch < nch; ++ch) {
+        // Next chunk in flight during this one: its x into xn, its weights
+        // into registers (stored to the other buffer after the chains).
+        if (ch + 1 < nch) {
+            const int k1 = (ch + 1) * DC;
 #pragma unroll
-        for (int k = 0; k < KP; ++k) {
-            const int q = threadIdx.x + kRepairThreads * k;
-            if (q < P) {
-                const int tl = ptok[q];
-                const int e = cand[tl][q - poff[tl]];
-                float a = acc[k];
+            for (int i = 0; i < XQ; ++i) xn[i] = *reinterpret_cast<const u32x4_t*>(xt + k1 + 8 * i);
 #pragma unroll
-                for (int i = 0; i < DC; i += 8) {
-                    float xv[8], wv[8];
-                    load8(&xs[buf][tl][i], xv);
-                    load8(&ws[buf][e][i], wv);
-#pragma unroll
-                    for (int u = 0; u < 8; ++u) a = fmaf(xv[u], wv[u], a);
-                }
-                acc[k] = a;
+            for (int i = 0; i < WQ; ++i) {
+                const int q = (tid + NT * i) * 8;
+                const int e = q / DC, c = q % DC;
+                wrg[i] = (u32x4_t){0u, 0u, 0u, 0u};
+                if (tid + NT * i < WP && e < E) wrg[i] = *reinterpret_cast<const u32x4_t*>(wr + (size_t)e * d + k1 + c);
             }
         }
-        if (d0 + DC < d) MOE_STASH(buf ^ 1);
+        static_assert(CPL == 1 || CPL == 4, "chain counts handled below");
+        if constexpr (CPL == 1) {
+            if (nmax >= 1) chunk(std::integral_constant<int, 1>{}, buf);
+        } else {
+            switch (nmax) {
+                case 4: chunk(std::integral_constant<int, 4>{}, buf); break;
+                case 3: chunk(std::integral_constant<int, 3>{}, buf); break;
+                case 2: chunk(std::integral_constant<int, 2>{}, buf); break;
+                case 1: chunk(std::integral_constant<int, 1>{}, buf); break;
+                default: break;
+            }
+        }
+        if (ch + 1 < nch) {
+            stash(buf ^ 1);
+#pragma unroll
+            for (int i = 0; i < XQ; ++i) xr[i] = xn[i];
+        }
         __syncthreads();
         buf ^= 1;
     }
-#undef MOE_FETCH
-#undef MOE_STASH
+
+    // Selection: every slot's exact sigmoid and expert go to LDS (the ring is
+    // free after the last barrier), then the token's first lane takes the K
+    // largest keys (ties to the lower expert) and the gates.
+    float* ssig = reinterpret_cast<float*>(lds);
+    int* sexp = reinterpret_cast<int*>(ssig + TPB * NS);
 #pragma unroll
-    for (int k = 0; k < KP; ++k) {
-        const int q = threadIdx.x + kRepairThreads * k;
-        if (q < P) sex[q] = sigmoid_fp32(acc[k]);
+    for (int c = 0; c < CPL; ++c) {
+        const int j = g + LPT * c;
+        if (on[c]) {
+            ssig[tl * NS + j] = sigmoid_fp32(acc[c]);
+            sexp[tl * NS + j] = ec[c];
+        }
     }
     __syncthreads();
-
-    // Phase C: exact top-K among the candidates and the gates (a wave per token).
-    for (int tl = wave; tl < RB; tl += kRepairWaves) {
-        const int t = t0 + tl;
-        const int nc = ncand[tl];
-        if (t >= T || nc == 0) continue;  // overflow tokens are routed by the exact kernel
-        const int e = lane < nc ? (int)cand[tl][lane] : 0x7fffffff;
-        const float sg = lane < nc ? sex[poff[tl] + lane] : 0.0f;
-        const float key = lane < nc ? (bias ? sg + bias[e] : sg) : -INFINITY;
-        bool taken = false;
-        float csig[kMaxK];
-        int cidx[kMaxK];
+    if (g != 0 || t >= T || nc == 0) return;
+    uint32_t taken = 0;
+    float csig[kMaxK];
+    int cidx[kMaxK];
 #pragma unroll
-        for (int j = 0; j < kMaxK; ++j) {
-            csig[j] = 0.0f;
-            cidx[j] = 0;
-            if (j >= K) continue;
-            float bk = taken ? -INFINITY : key;
-            int be = taken ? 0x7fffffff : e;
-            float bs = sg;
-#pragma unroll
-            for (int off = kWave / 2; off > 0; off >>= 1) {
-                const float ok = __shfl_xor(bk, off);
-                const int oe = __shfl_xor(be, off);
-                const float os = __shfl_xor(bs, off);
-                if (ok > bk || (ok == bk && oe < be)) {
-                    bk = ok;
-                    be = oe;
-                    bs = os;
-                }
+    for (int j = 0; j < kMaxK; ++j) {
+        csig[j] = 0.0f;
+        cidx[j] = 0;
+        if (j >= K) continue;
+        float bk = -INFINITY, bs = 0.0f;
+        int be = 0x7fffffff, bq = -1;
+        for (int q = 0; q < nc; ++q) {
+            if ((taken >> q) & 1u) continue;
+            const float sg = ssig[tl * NS + q];
+            const int e = sexp[tl * NS + q];
+            const float key = bias ? sg + bias[e] : sg;
+            if (key > bk || (key == bk && e < be)) {
+                bk = key;
+                be = e;
+                bs = sg;
+                bq = q;
             }
-            if (be == e && lane < nc) taken = true;
-            csig[j] = bs;
-            cidx[j] = be;
         }
-        float den = csig[0];
-#pragma unroll
-        for (int j = 1; j < kMaxK; ++j)
-            if (j < K) den = den + csig[j];
-        int my_e = 0;
-        float my_g = 0.0f;
-#pragma unroll
-        for (int j = 0; j < kMaxK; ++j)
-            if (j == lane && j < K) {
-                my_e = cidx[j];
-                my_g = csig[j] / den;
-            }
-        if (lane < K) {
-            topk_idx[(size_t)t * K + lane] = my_e;
-            topk_gate[(size_t)t * K + lane] = my_g;
-        }
+        if (bq >= 0) taken |= 1u << bq;
+        csig[j] = bs;
+        cidx[j] = be;
     }
+    float den = csig[0];
+#pragma unroll
+    for (int j = 1; j < kMaxK; ++j)
+        if (j < K) den = den + csig[j];
+#pragma unroll
+    for (int j = 0; j < kMaxK; ++j)
+        if (j < K) {
+            topk_idx[(size_t)t * K + j] = cidx[j];
+            topk_gate[(size_t)t * K + j] = csig[j] / den;
+        }
 }
 
 // Exact routing of the queued tokens: all E logits by the FMA chain, then
@@ -613,6 +668,8 @@ hipError_t launch_topk(const moe_desc_t& d, const float* scores, const float* bi
 
 namespace moe {
 
+int router_cand_slots(int K) { return K <= 8 ? 16 : 32; }
+
 float router_fast_bound_constant(int d) {
     const double u = 1.0 / 16777216.0;
     const double gamma = d * u / (1.0 - d * u);
@@ -621,28 +678,45 @@ float router_fast_bound_constant(int d) {
 
 hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, const void* x,
                                      const void* w_router, const float* bias, float* xnorm, float* wnorm,
-                                     int32_t* ovf_count, int32_t* ovf_list, int32_t* topk_idx,
-                                     float* topk_gate, hipStream_t s) {
+                                     uint16_t* cand, int32_t* ncand, int32_t* ovf_count, int32_t* ovf_list,
+                                     int32_t* topk_idx, float* topk_gate, hipStream_t s) {
     const bf16_t* xb = static_cast<const bf16_t*>(x);
     const bf16_t* wb = static_cast<const bf16_t*>(w_router);
     hipLaunchKernelGGL(k_row_norms, dim3((d.T + 3) / 4), dim3(256), 0, s, xb, d.T, d.d, xnorm, ovf_count);
     hipLaunchKernelGGL(k_row_norms, dim3((d.E + 3) / 4), dim3(256), 0, s, wb, d.E, d.d, wnorm, nullptr);
     const float cst = router_fast_bound_constant(d.d);
-    // Blocks of 128 tokens for large batches (router weights streamed once per
-    // block), 32 for small ones (enough blocks to fill the GPU). Router weight
-    // chunks of 32 columns while E <= 256, else 16.
-#define MOE_REPAIR(RBv, DCv, EMv, PERv)                                                                    \
-    hipLaunchKernelGGL((k_router_repair<RBv, DCv, EMv, PERv>), dim3((d.T + RBv - 1) / RBv), dim3(kRepairThreads), \
-                       0, s, s_fast, xnorm, wnorm, bias, xb, wb, d.T, d.d, d.E, d.K, cst, topk_idx, topk_gate,  \
-                       ovf_count, ovf_list)
-    const bool big = d.T >= 16384;
-    const int per = (d.E + kWave - 1) / kWave;
-    if (per <= 1) { if (big) MOE_REPAIR(128, 32, 256, 1); else MOE_REPAIR(32, 32, 256, 1); }
-    else if (per <= 2) { if (big) MOE_REPAIR(128, 32, 256, 2); else MOE_REPAIR(32, 32, 256, 2); }
-    else if (per <= 4) { if (big) MOE_REPAIR(128, 32, 256, 4); else MOE_REPAIR(32, 32, 256, 4); }
-    else if (per <= 8) { if (big) MOE_REPAIR(128, 16, 512, 8); else MOE_REPAIR(32, 16, 512, 8); }
-    else { if (big) MOE_REPAIR(128, 16, 1024, 16); else MOE_REPAIR(32, 16, 1024, 16); }
-#undef MOE_REPAIR
+    const int ns = router_cand_slots(d.K);
+    // Candidates: 16 lanes per token (64 for more than 256 experts).
+#define MOE_CAND(LPAv, PERv, NSv)                                                                           \
+    hipLaunchKernelGGL((k_router_cand<LPAv, PERv, NSv>), dim3((d.T + 256 / LPAv - 1) / (256 / LPAv)),        \
+                       dim3(256), 0, s, s_fast, xnorm, wnorm, bias, d.T, d.E, d.K, cst, cand, ncand, ovf_count, \
+                       ovf_list)
+    if (d.E <= 64) { if (ns == 16) MOE_CAND(16, 4, 16); else MOE_CAND(16, 4, 32); }
+    else if (d.E <= 256) { if (ns == 16) MOE_CAND(16, 16, 16); else MOE_CAND(16, 16, 32); }
+    else { if (ns == 16) MOE_CAND(64, 16, 16); else MOE_CAND(64, 16, 32); }
+#undef MOE_CAND
+    // Exact chains: 256 (or 128) tokens per block of 1024 threads while that
+    // still gives a block per CU, then 64 tokens per block, then 16 tokens
+    // with one chain per lane for small batches.
+#define MOE_CHAIN(TPBv, LPTv, CPLv, EMv, DCv)                                                               \
+    hipLaunchKernelGGL((k_router_chain<TPBv, LPTv, CPLv, EMv, DCv>), dim3((d.T + TPBv - 1) / TPBv),          \
+                       dim3(TPBv * LPTv), 0, s, xb, wb, bias, cand, ncand, d.T, d.d, d.E, d.K, topk_idx, topk_gate)
+#define MOE_CHAIN_E(TPBv, LPTv, CPLv, DCv)                                                                     \
+    do {                                                                                                    \
+        if (d.E <= 64) MOE_CHAIN(TPBv, LPTv, CPLv, 64, DCv);                                                \
+        else if (d.E <= 256) MOE_CHAIN(TPBv, LPTv, CPLv, 256, DCv);                                         \
+        else MOE_CHAIN(TPBv, LPTv, CPLv, 1024, 16);                                                         \
+    } while (0)
+    const int big_tpb = ns == 16 ? 256 : 128;
+    if (d.T >= 256 * big_tpb) {
+        if (ns == 16) MOE_CHAIN_E(256, 4, 4, 64); else MOE_CHAIN_E(128, 8, 4, 64);
+    } else if (d.T >= 256 * 64) {
+        if (ns == 16) MOE_CHAIN_E(64, 4, 4, 64); else MOE_CHAIN_E(64, 8, 4, 64);
+    } else {
+        if (ns == 16) MOE_CHAIN_E(16, 16, 1, 128); else MOE_CHAIN_E(8, 32, 1, 128);
+    }
+#undef MOE_CHAIN_E
+#undef MOE_CHAIN
     hipLaunchKernelGGL(k_router_exact_list, dim3(64), dim3(256), 0, s, xb, wb, bias, d.d, d.E, d.K, ovf_count,
                        ovf_list, topk_idx, topk_gate);
     return hipGetLastError();
