@@ -23,6 +23,9 @@
 
 #include <math.h>
 
+#include <type_traits>
+#include <utility>
+
 namespace moe {
 namespace {
 
@@ -388,6 +391,259 @@ void k_gemm_bf16(const GemmArgs a) {
     }
 }
 
+// Compile-time loop: f(std::integral_constant<int, 0>{}) ... f(<N - 1>).
+template <typename F, int... Is>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, Is...>) {
+    (f(std::integral_constant<int, Is>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// bf16 grouped / dense GEMM, 256 x 256 tiles, four waves of 128 x 128 (one
+// wave per SIMD, accumulators in the 256 accumulation registers), 64-wide K
+// slabs (whole 128-byte row pieces per copy).
+//
+// A CU's global -> LDS copy path takes about as long to move a slab as the
+// MFMAs take to consume it, so copies must leave at an even pace: every K
+// step of 16 MFMAs carries exactly four copies (one after every fourth MFMA)
+// and eight fragment reads for the next K step, in an order fixed by hand.
+// The token operand has a ring of three slabs and the weight operand a ring
+// of two (together the whole 160 KB of LDS), so token copies get more than a
+// slab of lead and weight copies, mostly L2 hits, half a slab. One barrier per
+// slab sits before its last K step: every wave has read the whole slab by
+// then (its buffers can be refilled from that last step on) and has seen its
+// own copies of the next slab land (its first fragments are read during that
+// last step). Row ids come from the global row map, so no LDS is spent on them.
+template <int EPI, bool GROUPED>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void k_gemm_sp(const GemmArgs a) {
+    constexpr int BM = 256, BN = 256, NW = 4, WT = 128, FB = WT / 32;
+    constexpr int BK = 64, CPR = 8, ROWB = 128, KS = 4;
+    constexpr int SLAB = BM * ROWB;           // 32 KB per operand and slab
+    constexpr int AST = 3, WST = 2;           // ring depths
+    constexpr int WBASE = AST * SLAB;         // weight ring after the token ring
+    constexpr int AP = BM * CPR / kWave / NW;  // 8 token copy pieces per wave and slab
+    constexpr int BP = BN * CPR / kWave / NW;  // 8 weight copy pieces
+    static_assert(AP == 8 && BP == 8, "copy schedule is written for 8 + 8 pieces");
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[AST * SLAB + WST * SLAB];
+
+    const TileCoord tc = locate_tile<GROUPED>(a, BM, BN);
+    if (!tc.valid) return;
+    const int tid = threadIdx.x;
+    const int lane = tid & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+    const int wm = wave >> 1, wn = wave & 1;
+    const int Kd = a.Kdim;
+    const int nk = Kd / BK;
+
+    auto row_id = [&](int r) {  // operand / output row id of tile row r (pad rows repeat the last)
+        const int p = tc.row0 + (r < tc.rows ? r : tc.rows - 1);
+        if (EPI == EPI_GELU_STORE && a.row_mode == ROWS_GATHER_TOKENS) return a.row_map[p] / a.route_k;
+        if (EPI == EPI_SCATTER_SLOT) return a.row_map[p];
+        return p;
+    };
+
+    const __amdgpu_buffer_rsrc_t xres = make_rsrc(a.A, a.a_bytes);
+    const __amdgpu_buffer_rsrc_t wres =
+        make_rsrc(static_cast<const bf16_t*>(a.B) + (size_t)tc.e * a.b_group_stride, (uint32_t)a.N * Kd * 2);
+    const __amdgpu_buffer_rsrc_t xnull = make_rsrc(a.A, 0);
+    const __amdgpu_buffer_rsrc_t wnull =
+        make_rsrc(static_cast<const bf16_t*>(a.B) + (size_t)tc.e * a.b_group_stride, 0);
+    uint32_t xv[AP], wv[BP];
+#pragma unroll
+    for (int i = 0; i < AP; ++i) {
+        const int sl = (wave + NW * i) * kWave + lane;
+        const int r = sl / CPR, pch = sl % CPR;
+        const int c = pch ^ ((r >> 1) & 7);
+        const int xrow = EPI == EPI_GELU_STORE ? row_id(r) : tc.row0 + (r < tc.rows ? r : tc.rows - 1);
+        xv[i] = (uint32_t)xrow * (uint32_t)(Kd * 2) + c * 16;
+    }
+#pragma unroll
+    for (int i = 0; i < BP; ++i) {
+        const int sl = (wave + NW * i) * kWave + lane;
+        const int r = sl / CPR, pch = sl % CPR;
+        const int c = pch ^ ((r >> 1) & 7);
+        wv[i] = (uint32_t)(tc.n0 + r) * (uint32_t)(Kd * 2) + c * 16;
+    }
+
+    f32x16_t acc[FB][FB];
+#pragma unroll
+    for (int j = 0; j < FB; ++j)
+#pragma unroll
+        for (int i = 0; i < FB; ++i)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[j][i][v] = 0.0f;
+
+    const int fr = lane & 31;
+    const int fk = lane >> 5;
+    const int lane_sw = (fr >> 1) & 7;
+    uint32_t xoff[KS], woff[KS];
+    const uint32_t base = lds_address(smem);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+        const uint32_t k = fr * ROWB + (((ks * 2 + fk) ^ lane_sw) << 4);
+        xoff[ks] = base + (wm * WT) * ROWB + k;
+        woff[ks] = base + WBASE + (wn * WT) * ROWB + k;
+    }
+
+    // Slab m's copy source: real slabs through the sized resources, slabs
+    // past the last through the zero-size ones at an in-range offset.
+    auto slab_src = [&](int m, uint32_t& soff, __amdgpu_buffer_rsrc_t& xr, __amdgpu_buffer_rsrc_t& wr) {
+        const bool real = m < nk;
+        soff = (uint32_t)(real ? m : nk - 1) * BK * 2;
+        xr = real ? xres : xnull;
+        wr = real ? wres : wnull;
+    };
+    // Copy piece L (constant) of this wave: token operand (IS_A) or weights.
+    auto copy_a = [&](auto LC, int stage, uint32_t soff, __amdgpu_buffer_rsrc_t xr) {
+        constexpr int L = decltype(LC)::value;
+        copy16_to_lds(xr, xv[L], soff, smem + stage * SLAB + (wave + NW * L) * 1024);
+    };
+    auto copy_w = [&](auto LC, int stage, uint32_t soff, __amdgpu_buffer_rsrc_t wr) {
+        constexpr int L = decltype(LC)::value;
+        copy16_to_lds(wr, wv[L], soff, smem + WBASE + stage * SLAB + (wave + NW * L) * 1024);
+    };
+
+    bf16x8_t xf[2][FB], wf[2][FB];
+    auto read_frag = [&](auto NBC, auto QC, uint32_t abase, uint32_t wbase, int ks) {
+        constexpr int nb = decltype(NBC)::value, q = decltype(QC)::value;
+        if constexpr (q < FB) xf[nb][q] = lds_read16<q * 32 * ROWB>(xoff[ks] + abase);
+        else wf[nb][q - FB] = lds_read16<(q - FB) * 32 * ROWB>(woff[ks] + wbase);
+    };
+    auto settle = [&](auto CBC) {
+        constexpr int cb = decltype(CBC)::value;
+        wait_lgkmcnt0();
+#pragma unroll
+        for (int i = 0; i < FB; ++i) tie(xf[cb][i]);
+#pragma unroll
+        for (int j = 0; j < FB; ++j) tie(wf[cb][j]);
+    };
+    // One K step: 16 MFMAs on buffer CB, fragment q of the next K step after
+    // MFMA q (q < 8), copy number q / 4 of the step's four after MFMA q when
+    // q % 4 == 1. COPY(c) issues the step's c-th copy.
+    auto kstep = [&](auto CBC, uint32_t rabase, uint32_t rwbase, int rks, auto&& copy) {
+        constexpr int cb = decltype(CBC)::value;
+        static_for<FB * FB>([&](auto QC) {
+            constexpr int q = decltype(QC)::value;
+            constexpr int j = q / FB, i = q % FB;
+            acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[cb][j], xf[cb][i], acc[j][i], 0, 0, 0);
+            if constexpr (q < 2 * FB)
+                read_frag(std::integral_constant<int, cb ^ 1>{}, QC, rabase, rwbase, rks);
+            if constexpr (q % 4 == 1) copy(std::integral_constant<int, q / 4>{});
+            __builtin_amdgcn_sched_barrier(0);
+        });
+    };
+
+    // Prologue: token slab 0, weight slab 0, token slab 1, the first half of
+    // weight slab 1 (what the loop would have issued before step 0); wait for
+    // slab 0 of both operands; read its first fragments.
+    {
+        uint32_t so;
+        __amdgpu_buffer_rsrc_t xr, wr;
+        slab_src(0, so, xr, wr);
+        static_for<AP>([&](auto LC) { copy_a(LC, 0, so, xr); });
+        static_for<BP>([&](auto LC) { copy_w(LC, 0, so, wr); });
+        slab_src(1, so, xr, wr);
+        static_for<AP>([&](auto LC) { copy_a(LC, 1, so, xr); });
+        static_for<BP / 2>([&](auto LC) { copy_w(LC, 1, so, wr); });
+    }
+    wait_vmcnt<AP + BP / 2>();
+    barrier_no_fence();
+    static_for<2 * FB>([&](auto QC) { read_frag(std::integral_constant<int, 0>{}, QC, 0u, 0u, 0); });
+
+    int as = 0, ws = 0;  // ring slots of slab kt
+    for (int kt = 0; kt < nk; ++kt) {
+        const uint32_t abase = (uint32_t)as * SLAB, wbase = (uint32_t)ws * SLAB;
+        const int as1 = as == AST - 1 ? 0 : as + 1, as2 = as1 == AST - 1 ? 0 : as1 + 1;
+        const int ws1 = ws ^ 1;
+        uint32_t so1, so2, so2w;
+        __amdgpu_buffer_rsrc_t xr1, wr1, xr2, wr2, xr2w, wr2w;
+        slab_src(kt + 1, so1, xr1, wr1);
+        slab_src(kt + 2, so2, xr2, wr2);
+        (void)xr1; (void)xr2w; (void)wr2;
+        so2w = so2; wr2w = wr2;
+        // K step 0: second half of weight slab kt + 1.
+        settle(std::integral_constant<int, 0>{});
+        kstep(std::integral_constant<int, 0>{}, abase, wbase, 1, [&](auto CC) {
+            copy_w(std::integral_constant<int, BP / 2 + decltype(CC)::value>{}, ws1, so1, wr1);
+        });
+        // K steps 1 and 2: token slab kt + 2.
+        settle(std::integral_constant<int, 1>{});
+        kstep(std::integral_constant<int, 1>{}, abase, wbase, 2, [&](auto CC) {
+            copy_a(std::integral_constant<int, decltype(CC)::value>{}, as2, so2, xr2);
+        });
+        settle(std::integral_constant<int, 0>{});
+        kstep(std::integral_constant<int, 0>{}, abase, wbase, 3, [&](auto CC) {
+            copy_a(std::integral_constant<int, 4 + decltype(CC)::value>{}, as2, so2, xr2);
+        });
+        settle(std::integral_constant<int, 1>{});
+        // Token and weight slab kt + 1 have landed for this wave (the token
+        // slab kt + 2 copies may still be in flight); after the barrier, for
+        // every wave, and every wave is done reading slab kt.
+        wait_vmcnt<AP>();
+        barrier_no_fence();
+        // K step 3: first fragments of slab kt + 1; first half of weight slab
+        // kt + 2 into the weight buffer of slab kt.
+        kstep(std::integral_constant<int, 1>{}, (uint32_t)as1 * SLAB, (uint32_t)ws1 * SLAB, 0, [&](auto CC) {
+            copy_w(std::integral_constant<int, decltype(CC)::value>{}, ws, so2w, wr2w);
+        });
+        as = as1;
+        ws = ws1;
+    }
+
+    // Epilogue (as in k_gemm_bf16): row ids to LDS, then per 32-row block
+    // activate / convert into the wave's LDS area, read back as 16-byte row
+    // pieces, store whole lines.
+    constexpr bool OUT_F32 = EPI == EPI_STORE_F32;
+    constexpr int OES = OUT_F32 ? 4 : 2;
+    constexpr int SEG = WT * OES;
+    constexpr int RSTR = SEG + 16;
+    constexpr int CPRO = SEG / 16;
+    constexpr int PIECES = 32 * CPRO / kWave;
+    static_assert(1024 + NW * 32 * RSTR <= AST * SLAB + WST * SLAB, "epilogue staging must fit");
+    __syncthreads();
+    int32_t* srow = reinterpret_cast<int32_t*>(smem);
+    if (EPI == EPI_SCATTER_SLOT)
+        for (int r = tid; r < BM; r += NW * kWave) srow[r] = row_id(r);
+    __syncthreads();
+    uint8_t* stg = smem + 1024 + wave * 32 * RSTR;
+#pragma unroll
+    for (int i = 0; i < FB; ++i) {
+#pragma unroll
+        for (int j = 0; j < FB; ++j)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                float v0 = acc[j][i][4 * g + 0], v1 = acc[j][i][4 * g + 1];
+                float v2 = acc[j][i][4 * g + 2], v3 = acc[j][i][4 * g + 3];
+                uint8_t* dst = stg + fr * RSTR + (j * 32 + 8 * g + 4 * fk) * OES;
+                if (OUT_F32) {
+                    *reinterpret_cast<float4*>(dst) = make_float4(v0, v1, v2, v3);
+                } else {
+                    if (EPI == EPI_GELU_STORE) {
+                        v0 = gelu_as(v0); v1 = gelu_as(v1); v2 = gelu_as(v2); v3 = gelu_as(v3);
+                    }
+                    *reinterpret_cast<uint2*>(dst) = pack4_bf16(v0, v1, v2, v3);
+                }
+            }
+        wave_sync_lds();
+#pragma unroll
+        for (int k = 0; k < PIECES; ++k) {
+            const int q = lane + kWave * k;
+            const int rr = q / CPRO, pc = q % CPRO;
+            const int r = wm * WT + i * 32 + rr;
+            const uint4 v = *reinterpret_cast<const uint4*>(stg + rr * RSTR + pc * 16);
+            if (r < tc.rows) {
+                const size_t orow = EPI == EPI_SCATTER_SLOT ? (size_t)srow[r] : (size_t)(tc.row0 + r);
+                uint8_t* out = static_cast<uint8_t*>(a.C) + (orow * a.N + tc.n0 + wn * WT) * OES + pc * 16;
+                *reinterpret_cast<uint4*>(out) = v;
+            }
+        }
+        wave_sync_lds();
+    }
+}
+
 // fp32 path (used by the fp32 layer): 64x64 tiles on the vector ALUs, 4x4
 // outputs per thread, K slabs of 16 staged through LDS.
 template <int EPI, bool GROUPED>
@@ -468,6 +724,16 @@ hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
+
+template <int EPI, bool GROUPED>
+hipError_t launch_sp(const GemmArgs& a, hipStream_t s) {
+    const int n_n = a.N / 256;
+    const long long total = (long long)a.max_tiles * n_n;
+    const long long grid = (total + kNumXcd - 1) / kNumXcd * kNumXcd;
+    hipLaunchKernelGGL((k_gemm_sp<EPI, GROUPED>), dim3((unsigned)grid), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
 template <int EPI, bool GROUPED>
 hipError_t launch_f32(const GemmArgs& a, hipStream_t s) {
     const int n_n = a.N / 64;
@@ -490,7 +756,7 @@ hipError_t launch_f32(const GemmArgs& a, hipStream_t s) {
 template <int EPI, bool GROUPED>
 hipError_t dispatch_bf16(int bm, const GemmArgs& a, hipStream_t s) {
     if (bm == 256) {
-        if (a.N % 256 == 0) return launch_bf16<256, 256, 2, 4, 64, 2, 1, EPI, GROUPED>(a, s);
+        if (a.N % 256 == 0) return launch_sp<EPI, GROUPED>(a, s);
         if (a.N % 128 == 0) return launch_bf16<256, 128, 2, 2, 64, 2, 1, EPI, GROUPED>(a, s);
         return launch_bf16<256, 64, 4, 1, 64, 2, 1, EPI, GROUPED>(a, s);
     }
