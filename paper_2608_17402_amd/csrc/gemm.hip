@@ -79,22 +79,23 @@ __device__ __forceinline__ TileCoord locate_tile(const GemmArgs& a, int bm, int 
     return tc;
 }
 
-// GELU for the bf16 path: 0.5 x (1 + erf(x / sqrt 2)) with erf from
-// Abramowitz & Stegun 7.1.26 (|error| <= 1.5e-7, far below the bf16 rounding
-// of the activation), built from the hardware reciprocal and exp2.
+// GELU for the bf16 path, from Abramowitz & Stegun 7.1.26 (|error of erf| <=
+// 1.5e-7, far below the bf16 rounding of the activation), built from the
+// hardware reciprocal and exp2. With Q = erfc(|x| / sqrt 2) / 2, the identity
+// GELU(x) = max(x, 0) - |x| Q holds for either sign of x; A&S give
+// erfc(z) = t P(t) exp(-z^2), t = 1 / (1 + p z), so Q = t P(t) / 2 *
+// exp(-x^2 / 2). The 1/sqrt 2 of z and the 1/2 are folded into p and the
+// coefficients; exp(-x^2 / 2) is exp2(-x^2 log2(e) / 2).
 __device__ __forceinline__ float gelu_as(float x) {
-    const float z = x * 0.70710678118654752f;
-    const float az = fabsf(z);
-    const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, az, 1.0f));
-    float p = fmaf(1.061405429f, t, -1.453152027f);
-    p = fmaf(p, t, 1.421413741f);
-    p = fmaf(p, t, -0.284496736f);
-    p = fmaf(p, t, 0.254829592f);
-    p *= t;
-    const float e = __builtin_amdgcn_exp2f((az * az) * -1.44269504088896341f);
-    const float erf_v = copysignf(fmaf(-p, e, 1.0f), z);
-    const float hx = 0.5f * x;
-    return fmaf(hx, erf_v, hx);
+    const float ax = fabsf(x);
+    const float t = __builtin_amdgcn_rcpf(fmaf(0.23164189f, ax, 1.0f));
+    float q = fmaf(0.5307027f, t, -0.72657603f);
+    q = fmaf(q, t, 0.7107069f);
+    q = fmaf(q, t, -0.14224836f);
+    q = fmaf(q, t, 0.1274148f);
+    q *= t;
+    const float e = __builtin_amdgcn_exp2f((x * -0.7213475f) * x);
+    return fmaf(-ax, q * e, fmaxf(x, 0.0f));
 }
 
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
@@ -644,6 +645,429 @@ void k_gemm_sp(const GemmArgs a) {
     }
 }
 
+// Memory operations of the persistent kernel's epilogue, as inline assembly.
+// The compiler's wait bookkeeping does not see them. Loads and stores can
+// retire out of order relative to each other on this target, so a store the
+// compiler knew about would turn each later wait for a load result into a full
+// drain of the slab copies in flight. The kernel waits for them explicitly.
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+// (The s_nop is the wait state a store of more than 8 bytes needs before its
+// data registers may be overwritten; the compiler cannot see that here.)
+__device__ __forceinline__ void store16_asm(void* p, u32x4_t v) {
+    asm volatile("global_store_dwordx4 %0, %1, off\n\ts_nop 0" ::"v"(p), "v"(v) : "memory");
+}
+__device__ __forceinline__ void lds_write8_asm(uint32_t addr, u32x2_t v) {
+    asm volatile("ds_write_b64 %0, %1" ::"v"(addr), "v"(v) : "memory");
+}
+__device__ __forceinline__ void lds_write16_asm(uint32_t addr, u32x4_t v) {
+    asm volatile("ds_write_b128 %0, %1" ::"v"(addr), "v"(v) : "memory");
+}
+__device__ __forceinline__ u32x4_t lds_read16u_asm(uint32_t addr) {
+    u32x4_t r;
+    asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(addr));
+    return r;
+}
+__device__ __forceinline__ void tie(u32x4_t& v) { asm volatile("" : "+v"(v)); }
+// One accumulator moved to a vector register at this point of the program
+// (volatile: not hoisted, so only one staged block's values are live at once).
+__device__ __forceinline__ float acc_read(float x) {
+    float v;
+    asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v) : "a"(x));
+    return v;
+}
+
+// Persistent form of k_gemm_sp: one workgroup per CU walks its share of the
+// tiles (the XCD-aware order of locate_tile, a stride of gridDim / 8 tiles
+// apart), and the slab pipeline runs on across tile boundaries. While the last
+// two slabs of one tile are multiplied, the first two slabs of the next are
+// already being copied, so a tile costs its K loop plus its epilogue. The
+// per-tile start-up of the one-tile-per-workgroup kernel disappears: dispatch,
+// the tile-table and row-map reads, and the first copies' latency.
+//
+// The epilogue stages each wave's 32-row blocks through the token-ring slot
+// of the tile's last slab. That is the only slot not being filled at that
+// moment: the next tile's first slab sits in the next slot and its second is
+// still landing in the one after. Row pieces are XOR-swizzled instead of
+// padded so that four waves' staging fits in one 32 KB slot. Tile metadata
+// flows through a short pipeline: tile-table entries are read two tiles ahead,
+// and gathered token rows (fc1) and output slots (fc2) one tile ahead. Their
+// loads are issued where the wait the compiler places before their first use
+// falls after long independent work.
+//
+// Token operand without gathering: its buffer resource starts at the tile's
+// first row and spans its valid rows, so pad rows read as zeros. Gathered rows
+// repeat the tile's last valid row, as in k_gemm_sp. Requires K >= 128 (at
+// least two slabs per tile).
+template <int EPI, bool GROUPED>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void k_gemm_pp(const GemmArgs a) {
+    constexpr int BM = 256, BN = 256, NW = 4, WT = 128, FB = WT / 32;
+    constexpr int BK = 64, CPR = 8, ROWB = 128, KS = 4;
+    constexpr int SLAB = BM * ROWB;            // 32 KB per operand and slab
+    constexpr int AST = 3, WST = 2;            // ring depths
+    constexpr int WBASE = AST * SLAB;          // weight ring after the token ring
+    constexpr int AP = BM * CPR / kWave / NW;  // 8 token copy pieces per wave and slab
+    constexpr int BP = BN * CPR / kWave / NW;  // 8 weight copy pieces
+    static_assert(AP == 8 && BP == 8, "copy schedule is written for 8 + 8 pieces");
+    constexpr bool GATHER = GROUPED && EPI == EPI_GELU_STORE;
+    constexpr bool SCATTER = EPI == EPI_SCATTER_SLOT;
+    constexpr bool OUT_F32 = EPI == EPI_STORE_F32;
+    constexpr int OES = OUT_F32 ? 4 : 2;
+    constexpr int NH = OUT_F32 ? 2 : 1;        // column halves per staged block (256-byte rows)
+    constexpr int STG_WAVE = 32 * 256;         // staging bytes per wave
+    static_assert(NW * STG_WAVE == SLAB, "staging must fill exactly one token slot");
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[AST * SLAB + WST * SLAB];
+
+    const int n_n = a.N / BN;
+    const int total =
+        (GROUPED ? __builtin_amdgcn_readfirstlane(*a.n_tiles) : (a.dense_rows + BM - 1) / BM) * n_n;
+    const int per = (total + kNumXcd - 1) / kNumXcd;
+    const int xcd = blockIdx.x % kNumXcd;
+    const int wpx = gridDim.x / kNumXcd;  // workgroups per XCD: the tile stride
+    const int lid_end = min(total, (xcd + 1) * per);
+    int lid = xcd * per + (int)blockIdx.x / kNumXcd;
+    if (lid >= lid_end) return;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+    const int wm = wave >> 1, wn = wave & 1;
+    const int Kd = a.Kdim;
+    const int nk = Kd / BK;
+    const uint32_t rowbytes = (uint32_t)Kd * 2;
+
+    struct Tile {
+        int e, row0, rows, n0;
+    };
+    // Tile-table entry of tile l (grouped): read through the vector path (the
+    // kernel's own stores keep the compiler from proving the table constant).
+    // Indices past this workgroup's share read its last tile instead.
+    auto tile_entry = [&](int l) {
+        TileDesc d{};
+        if (GROUPED) d = a.tiles[min(l, lid_end - 1) / n_n];
+        return d;
+    };
+    // Tile l from its table entry; the entry is the same for every lane, so it
+    // goes back to scalar registers.
+    auto tile_of = [&](int l, const TileDesc& d) {
+        Tile t;
+        const int mt = l / n_n;
+        t.n0 = (l - mt * n_n) * BN;
+        if (GROUPED) {
+            t.e = __builtin_amdgcn_readfirstlane(d.e);
+            t.row0 = __builtin_amdgcn_readfirstlane(d.row0);
+            t.rows = __builtin_amdgcn_readfirstlane(d.rows);
+        } else {
+            t.e = 0;
+            t.row0 = mt * BM;
+            t.rows = min(BM, a.dense_rows - t.row0);
+        }
+        return t;
+    };
+    auto tile_at = [&](int l) { return tile_of(l, tile_entry(l)); };
+    const bf16_t* const Bw = static_cast<const bf16_t*>(a.B);
+    const bf16_t* const Ax = static_cast<const bf16_t*>(a.A);
+    auto wres_of = [&](const Tile& t) {
+        return make_rsrc(Bw + (size_t)t.e * a.b_group_stride + (size_t)t.n0 * Kd, (uint32_t)BN * rowbytes);
+    };
+    auto xres_of = [&](const Tile& t) {
+        if (GATHER) return make_rsrc(Ax, a.a_bytes);
+        return make_rsrc(Ax + (size_t)t.row0 * Kd, (uint32_t)t.rows * rowbytes);
+    };
+    const __amdgpu_buffer_rsrc_t xnull = make_rsrc(Ax, 0);
+    const __amdgpu_buffer_rsrc_t wnull = make_rsrc(Bw, 0);
+
+    // Row offsets of this lane's copy pieces: row r of the slab, 16-byte chunk
+    // c (swizzled). The weight offsets (and the token offsets without
+    // gathering) are the same for every tile.
+    auto piece_rc = [&](int i, int& r, int& c) {
+        const int sl = (wave + NW * i) * kWave + lane;
+        r = sl / CPR;
+        c = (sl % CPR) ^ ((r >> 1) & 7);
+    };
+    uint32_t wv[BP];
+#pragma unroll
+    for (int i = 0; i < BP; ++i) {
+        int r, c;
+        piece_rc(i, r, c);
+        wv[i] = (uint32_t)r * rowbytes + c * 16;
+    }
+    // Gathered token rows: slot -> token, rows past the tile's end repeat its last row.
+    auto load_tokens = [&](const Tile& t, int32_t (&tok)[AP]) {
+#pragma unroll
+        for (int i = 0; i < AP; ++i) {
+            int r, c;
+            piece_rc(i, r, c);
+            tok[i] = a.row_map[t.row0 + min(r, t.rows - 1)];
+        }
+    };
+    auto token_offsets = [&](const int32_t (&tok)[AP], uint32_t (&xv)[AP]) {
+#pragma unroll
+        for (int i = 0; i < AP; ++i) {
+            int r, c;
+            piece_rc(i, r, c);
+            xv[i] = (uint32_t)(tok[i] / a.route_k) * rowbytes + c * 16;
+        }
+    };
+    // Output slot of staged piece k of 32-row block i (fc2 scatter).
+    int32_t orow[FB][8];
+    auto load_slots = [&](const Tile& t) {
+#pragma unroll
+        for (int i = 0; i < FB; ++i)
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int r = wm * WT + i * 32 + (lane >> 4) + 4 * k;
+                orow[i][k] = a.row_map[t.row0 + min(r, t.rows - 1)];
+            }
+    };
+
+    // Current tile (c), next (n) and the one after (nn, table entry only).
+    Tile tc = tile_at(lid);
+    bool has_n = lid + wpx < lid_end;
+    Tile tn = has_n ? tile_at(lid + wpx) : tc;
+    bool has_nn = lid + 2 * wpx < lid_end;
+    Tile tnn = has_nn ? tile_at(lid + 2 * wpx) : tn;
+    // Table entry three tiles ahead, read one tile before it is needed.
+    TileDesc ent3 = tile_entry(lid + 3 * wpx);
+    __amdgpu_buffer_rsrc_t xres_c = xres_of(tc), wres_c = wres_of(tc);
+    __amdgpu_buffer_rsrc_t xres_n = has_n ? xres_of(tn) : xnull;
+    __amdgpu_buffer_rsrc_t wres_n = has_n ? wres_of(tn) : wnull;
+    uint32_t xv_c[AP], xv_n[AP];
+    int32_t tok[AP];
+    if (GATHER) {
+        load_tokens(tc, tok);
+        token_offsets(tok, xv_c);
+        load_tokens(tn, tok);
+        token_offsets(tok, xv_n);
+    }
+    if (SCATTER) load_slots(tc);
+
+    f32x16_t acc[FB][FB];
+#pragma unroll
+    for (int j = 0; j < FB; ++j)
+#pragma unroll
+        for (int i = 0; i < FB; ++i)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[j][i][v] = 0.0f;
+
+    const int fr = lane & 31;
+    const int fk = lane >> 5;
+    const int lane_sw = (fr >> 1) & 7;
+    uint32_t xoff[KS], woff[KS];
+    const uint32_t base = lds_address(smem);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+        const uint32_t k = fr * ROWB + (((ks * 2 + fk) ^ lane_sw) << 4);
+        xoff[ks] = base + (wm * WT) * ROWB + k;
+        woff[ks] = base + WBASE + (wn * WT) * ROWB + k;
+    }
+
+    auto copy_a = [&](auto LC, int stage, uint32_t soff, __amdgpu_buffer_rsrc_t xr, const uint32_t (&xv)[AP]) {
+        constexpr int L = decltype(LC)::value;
+        copy16_to_lds(xr, xv[L], soff, smem + stage * SLAB + (wave + NW * L) * 1024);
+    };
+    auto copy_w = [&](auto LC, int stage, uint32_t soff, __amdgpu_buffer_rsrc_t wr) {
+        constexpr int L = decltype(LC)::value;
+        copy16_to_lds(wr, wv[L], soff, smem + WBASE + stage * SLAB + (wave + NW * L) * 1024);
+    };
+
+    bf16x8_t xf[2][FB], wf[2][FB];
+    auto read_frag = [&](auto NBC, auto QC, uint32_t abase, uint32_t wbase, int ks) {
+        constexpr int nb = decltype(NBC)::value, q = decltype(QC)::value;
+        if constexpr (q < FB) xf[nb][q] = lds_read16<q * 32 * ROWB>(xoff[ks] + abase);
+        else wf[nb][q - FB] = lds_read16<(q - FB) * 32 * ROWB>(woff[ks] + wbase);
+    };
+    auto settle = [&](auto CBC) {
+        constexpr int cb = decltype(CBC)::value;
+        wait_lgkmcnt0();
+#pragma unroll
+        for (int i = 0; i < FB; ++i) tie(xf[cb][i]);
+#pragma unroll
+        for (int j = 0; j < FB; ++j) tie(wf[cb][j]);
+    };
+    // One K step: 16 MFMAs on buffer CB, fragment q of the next K step after
+    // MFMA q (q < 8), copy q / 4 of the step's four after MFMA q when q % 4 == 1.
+    auto kstep = [&](auto CBC, uint32_t rabase, uint32_t rwbase, int rks, auto&& copy) {
+        constexpr int cb = decltype(CBC)::value;
+        static_for<FB * FB>([&](auto QC) {
+            constexpr int q = decltype(QC)::value;
+            constexpr int j = q / FB, i = q % FB;
+            acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[cb][j], xf[cb][i], acc[j][i], 0, 0, 0);
+            if constexpr (q < 2 * FB)
+                read_frag(std::integral_constant<int, cb ^ 1>{}, QC, rabase, rwbase, rks);
+            if constexpr (q % 4 == 1) copy(std::integral_constant<int, q / 4>{});
+            __builtin_amdgcn_sched_barrier(0);
+        });
+    };
+
+    // Epilogue of tile t from the accumulators, staged through the token slot
+    // `stslot`: per 32-row block (and 64-column half for fp32 output) each
+    // lane writes its row's runs into the wave's 8 KB, then reads back 16-byte
+    // row pieces (16 lanes per 256-byte row) and stores whole lines.
+    auto epilogue = [&](const Tile& t, int stslot) {
+        const uint32_t stg = base + (uint32_t)stslot * SLAB + (uint32_t)wave * STG_WAVE;
+        const uint32_t wrow = stg + (uint32_t)fr * 256u;
+        const int sw = fr & 15;
+        uint8_t* const cbase = static_cast<uint8_t*>(a.C);
+#pragma unroll
+        for (int i = 0; i < FB; ++i) {
+#pragma unroll
+            for (int h = 0; h < NH; ++h) {
+                __builtin_amdgcn_sched_barrier(0);
+                if (OUT_F32) {
+#pragma unroll
+                    for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+                        for (int g = 0; g < 4; ++g) {
+                            const int j = 2 * h + jj;
+                            const u32x4_t v = {__float_as_uint(acc_read(acc[j][i][4 * g + 0])),
+                                               __float_as_uint(acc_read(acc[j][i][4 * g + 1])),
+                                               __float_as_uint(acc_read(acc[j][i][4 * g + 2])),
+                                               __float_as_uint(acc_read(acc[j][i][4 * g + 3]))};
+                            const int chunk = 8 * jj + 2 * g + fk;
+                            lds_write16_asm(wrow + ((uint32_t)(chunk ^ sw) << 4), v);
+                        }
+                } else {
+#pragma unroll
+                    for (int j = 0; j < FB; ++j)
+#pragma unroll
+                        for (int g = 0; g < 4; ++g) {
+                            float v0 = acc_read(acc[j][i][4 * g + 0]), v1 = acc_read(acc[j][i][4 * g + 1]);
+                            float v2 = acc_read(acc[j][i][4 * g + 2]), v3 = acc_read(acc[j][i][4 * g + 3]);
+                            if (EPI == EPI_GELU_STORE) {
+                                v0 = gelu_as(v0); v1 = gelu_as(v1); v2 = gelu_as(v2); v3 = gelu_as(v3);
+                            }
+                            const int chunk = 4 * j + g;
+                            const uint2 pk = pack4_bf16(v0, v1, v2, v3);
+                            lds_write8_asm(wrow + ((uint32_t)(chunk ^ sw) << 4) + (uint32_t)fk * 8u,
+                                           (u32x2_t){pk.x, pk.y});
+                        }
+                }
+                u32x4_t v[8];
+#pragma unroll
+                for (int k = 0; k < 8; ++k) {
+                    const int rr = (lane >> 4) + 4 * k;
+                    const int pc = lane & 15;
+                    v[k] = lds_read16u_asm(stg + (uint32_t)rr * 256u + ((uint32_t)(pc ^ (rr & 15)) << 4));
+                }
+                wait_lgkmcnt0();
+#pragma unroll
+                for (int k = 0; k < 8; ++k) tie(v[k]);
+#pragma unroll
+                for (int k = 0; k < 8; ++k) {
+                    const int rr = (lane >> 4) + 4 * k;
+                    const int r = wm * WT + i * 32 + rr;
+                    if (r < t.rows) {
+                        const size_t orw = SCATTER ? (size_t)orow[i][k] : (size_t)(t.row0 + r);
+                        uint8_t* out = cbase + (orw * a.N + t.n0 + wn * WT + h * 64) * OES + (lane & 15) * 16;
+                        store16_asm(out, v[k]);
+                    }
+                }
+            }
+        }
+    };
+
+    // Prologue: token slab 0, weight slab 0, token slab 1, the first half of
+    // weight slab 1; wait for slab 0 of both operands; read its first fragments.
+    static_for<AP>([&](auto LC) { copy_a(LC, 0, 0u, xres_c, GATHER ? xv_c : wv); });
+    static_for<BP>([&](auto LC) { copy_w(LC, 0, 0u, wres_c); });
+    static_for<AP>([&](auto LC) { copy_a(LC, 1, (uint32_t)BK * 2, xres_c, GATHER ? xv_c : wv); });
+    static_for<BP / 2>([&](auto LC) { copy_w(LC, 1, (uint32_t)BK * 2, wres_c); });
+    wait_vmcnt<AP + BP / 2>();
+    barrier_no_fence();
+    static_for<2 * FB>([&](auto QC) { read_frag(std::integral_constant<int, 0>{}, QC, 0u, 0u, 0); });
+
+    int as = 0, ws = 0;  // ring slots of the slab being multiplied
+    for (;;) {
+        int kt = 0;
+        do {  // nk >= 2 slabs: written as do-while so the compiler counts the copies
+            const uint32_t abase = (uint32_t)as * SLAB, wbase = (uint32_t)ws * SLAB;
+            const int as1 = as == AST - 1 ? 0 : as + 1, as2 = as1 == AST - 1 ? 0 : as1 + 1;
+            const int ws1 = ws ^ 1;
+            // Slabs kt + 1 and kt + 2 may belong to the next tile.
+            const bool n1 = kt + 1 >= nk, n2 = kt + 2 >= nk;
+            const uint32_t so1 = (uint32_t)(n1 ? kt + 1 - nk : kt + 1) * (BK * 2);
+            const uint32_t so2 = (uint32_t)(n2 ? kt + 2 - nk : kt + 2) * (BK * 2);
+            const __amdgpu_buffer_rsrc_t wr1 = n1 ? wres_n : wres_c;
+            const __amdgpu_buffer_rsrc_t xr2 = n2 ? xres_n : xres_c;
+            const __amdgpu_buffer_rsrc_t wr2 = n2 ? wres_n : wres_c;
+            uint32_t xv2[AP];
+#pragma unroll
+            for (int i = 0; i < AP; ++i) xv2[i] = GATHER ? (n2 ? xv_n[i] : xv_c[i]) : wv[i];
+            // K step 0: second half of weight slab kt + 1.
+            settle(std::integral_constant<int, 0>{});
+            kstep(std::integral_constant<int, 0>{}, abase, wbase, 1, [&](auto CC) {
+                copy_w(std::integral_constant<int, BP / 2 + decltype(CC)::value>{}, ws1, so1, wr1);
+            });
+            // K steps 1 and 2: token slab kt + 2.
+            settle(std::integral_constant<int, 1>{});
+            kstep(std::integral_constant<int, 1>{}, abase, wbase, 2, [&](auto CC) {
+                copy_a(std::integral_constant<int, decltype(CC)::value>{}, as2, so2, xr2, xv2);
+            });
+            settle(std::integral_constant<int, 0>{});
+            kstep(std::integral_constant<int, 0>{}, abase, wbase, 3, [&](auto CC) {
+                copy_a(std::integral_constant<int, 4 + decltype(CC)::value>{}, as2, so2, xr2, xv2);
+            });
+            settle(std::integral_constant<int, 1>{});
+            // Token and weight slab kt + 1 have landed for this wave (only the
+            // eight token copies of slab kt + 2 may be younger); after the
+            // barrier, for every wave, and every wave is done reading slab kt.
+            wait_vmcnt<AP>();
+            barrier_no_fence();
+            // K step 3: first fragments of slab kt + 1; first half of weight
+            // slab kt + 2 into the weight slot of slab kt.
+            kstep(std::integral_constant<int, 1>{}, (uint32_t)as1 * SLAB, (uint32_t)ws1 * SLAB, 0, [&](auto CC) {
+                copy_w(std::integral_constant<int, decltype(CC)::value>{}, ws, so2, wr2);
+            });
+            as = as1;
+            ws = ws1;
+        } while (++kt < nk);
+
+        // The last K step also read the next tile's first fragments; let them
+        // land (their registers are reused by the epilogue) and read them again
+        // after it.
+        settle(std::integral_constant<int, 0>{});
+        // Gathered rows of the tile after next: read now, used after the epilogue.
+        if (GATHER && has_nn) load_tokens(tnn, tok);
+        // The last slab's token slot is free (and read by no wave any more).
+        epilogue(tc, as == 0 ? AST - 1 : as - 1);
+        if (!has_n) break;
+
+        // Advance: n -> c, nn -> n, and the table entry of the tile after that.
+        lid += wpx;
+        tc = tn;
+        xres_c = xres_n;
+        wres_c = wres_n;
+        has_n = has_nn;
+        tn = tnn;
+        xres_n = has_n ? xres_of(tn) : xnull;
+        wres_n = has_n ? wres_of(tn) : wnull;
+        if (GATHER) {
+#pragma unroll
+            for (int i = 0; i < AP; ++i) xv_c[i] = xv_n[i];
+            if (has_n) token_offsets(tok, xv_n);
+        }
+        has_nn = lid + 2 * wpx < lid_end;
+        if (has_nn) tnn = tile_of(lid + 2 * wpx, ent3);
+        ent3 = tile_entry(lid + 3 * wpx);
+        if (SCATTER) load_slots(tc);
+#pragma unroll
+        for (int j = 0; j < FB; ++j)
+#pragma unroll
+            for (int i = 0; i < FB; ++i)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) acc[j][i][v] = 0.0f;
+        // Every wave has read its staged rows before the next tile's token
+        // copies refill that slot.
+        barrier_no_fence();
+        static_for<2 * FB>([&](auto QC) {
+            read_frag(std::integral_constant<int, 0>{}, QC, (uint32_t)as * SLAB, (uint32_t)ws * SLAB, 0);
+        });
+    }
+    wait_vmcnt<0>();
+}
+
 // fp32 path (used by the fp32 layer): 64x64 tiles on the vector ALUs, 4x4
 // outputs per thread, K slabs of 16 staged through LDS.
 template <int EPI, bool GROUPED>
@@ -725,6 +1149,29 @@ hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
 }
 
 
+// Workgroups of the persistent kernel: one per CU (a multiple of the XCD
+// count), fewer when the grid-sizing bound on the tiles is smaller.
+int persistent_grid(long long tile_bound) {
+    static int cus[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+    if (cus[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < kNumXcd)
+            n = 256;
+        cus[dev] = n / kNumXcd * kNumXcd;
+    }
+    const long long bound = (tile_bound + kNumXcd - 1) / kNumXcd * kNumXcd;
+    return (int)(bound < cus[dev] ? bound : cus[dev]);
+}
+
+template <int EPI, bool GROUPED>
+hipError_t launch_pp(const GemmArgs& a, hipStream_t s) {
+    const int grid = persistent_grid((long long)a.max_tiles * (a.N / 256));
+    hipLaunchKernelGGL((k_gemm_pp<EPI, GROUPED>), dim3((unsigned)grid), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
 template <int EPI, bool GROUPED>
 hipError_t launch_sp(const GemmArgs& a, hipStream_t s) {
     const int n_n = a.N / 256;
@@ -756,7 +1203,11 @@ hipError_t launch_f32(const GemmArgs& a, hipStream_t s) {
 template <int EPI, bool GROUPED>
 hipError_t dispatch_bf16(int bm, const GemmArgs& a, hipStream_t s) {
     if (bm == 256) {
-        if (a.N % 256 == 0) return launch_sp<EPI, GROUPED>(a, s);
+        if (a.N % 256 == 0) {
+            const bool gather_ok = !(GROUPED && EPI == EPI_GELU_STORE) || a.row_mode == ROWS_GATHER_TOKENS;
+            if (a.Kdim >= 128 && gather_ok) return launch_pp<EPI, GROUPED>(a, s);
+            return launch_sp<EPI, GROUPED>(a, s);
+        }
         if (a.N % 128 == 0) return launch_bf16<256, 128, 2, 2, 64, 2, 1, EPI, GROUPED>(a, s);
         return launch_bf16<256, 64, 4, 1, 64, 2, 1, EPI, GROUPED>(a, s);
     }
