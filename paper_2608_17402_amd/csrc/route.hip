@@ -372,7 +372,7 @@ __global__ __launch_bounds__(TPB* LPT) void k_router_chain(const bf16_t* __restr
     constexpr int WP = EMAX * DC / 8;        // 16-byte router-weight pieces per chunk
     constexpr int WQ = (WP + NT - 1) / NT;   // per thread
     static_assert(NS <= 32, "at most 32 candidate slots");
-    constexpr int RING = 2 * EMAX * ROW * 2, SEL = TPB * NS * 8;
+    constexpr int RING = 2 * EMAX * ROW * 2, SEL = TPB * (NS * 12 + kMaxK * 8);
     __shared__ __attribute__((aligned(16))) uint8_t lds[RING > SEL ? RING : SEL];
     auto wsh = reinterpret_cast<bf16_t(*)[EMAX][ROW]>(lds);
 
@@ -391,6 +391,9 @@ __global__ __launch_bounds__(TPB* LPT) void k_router_chain(const bf16_t* __restr
         ec[c] = on[c] ? (int)cand[(size_t)t * NS + j] : 0;
     }
     const bf16_t* xt = x + (size_t)(t < T ? t : 0) * d;
+    float bc[CPL];  // selection bias of each chain's expert, read while the chains run
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) bc[c] = (bias && on[c]) ? bias[ec[c]] : 0.0f;
 
     u32x4_t xr[XQ], wrg[WQ];
     auto fetch = [&](int k0) {
@@ -493,57 +496,54 @@ __global__ __launch_bounds__(TPB* LPT) void k_router_chain(const bf16_t* __restr
         buf ^= 1;
     }
 
-    // Selection: every slot's exact sigmoid and expert go to LDS (the ring is
-    // free after the last barrier), then the token's first lane takes the K
-    // largest keys (ties to the lower expert) and the gates.
-    float* ssig = reinterpret_cast<float*>(lds);
+    // Selection: every candidate's exact key, sigmoid and expert go to LDS (the
+    // ring is free after the last barrier). Each lane ranks its own candidates
+    // among the token's in (key descending, expert ascending) order, the order
+    // of taking the K largest keys one by one; ranks below K are the slots.
+    // Then every lane of the token forms the gate denominator in slot order
+    // and writes its slots.
+    float* skey = reinterpret_cast<float*>(lds);
+    float* ssig = skey + TPB * NS;
     int* sexp = reinterpret_cast<int*>(ssig + TPB * NS);
+    float* osig = reinterpret_cast<float*>(sexp + TPB * NS);
+    int* oexp = reinterpret_cast<int*>(osig + TPB * kMaxK);
+    float kc[CPL], sc[CPL];
 #pragma unroll
     for (int c = 0; c < CPL; ++c) {
         const int j = g + LPT * c;
+        sc[c] = 0.0f;
+        kc[c] = 0.0f;
         if (on[c]) {
-            ssig[tl * NS + j] = sigmoid_fp32(acc[c]);
+            sc[c] = sigmoid_fp32(acc[c]);
+            kc[c] = bias ? sc[c] + bc[c] : sc[c];
+            skey[tl * NS + j] = kc[c];
+            ssig[tl * NS + j] = sc[c];
             sexp[tl * NS + j] = ec[c];
         }
     }
     __syncthreads();
-    if (g != 0 || t >= T || nc == 0) return;
-    uint32_t taken = 0;
-    float csig[kMaxK];
-    int cidx[kMaxK];
 #pragma unroll
-    for (int j = 0; j < kMaxK; ++j) {
-        csig[j] = 0.0f;
-        cidx[j] = 0;
-        if (j >= K) continue;
-        float bk = -INFINITY, bs = 0.0f;
-        int be = 0x7fffffff, bq = -1;
+    for (int c = 0; c < CPL; ++c) {
+        if (!on[c]) continue;
+        int rank = 0;  // the candidate itself compares neither greater nor lower
         for (int q = 0; q < nc; ++q) {
-            if ((taken >> q) & 1u) continue;
-            const float sg = ssig[tl * NS + q];
-            const int e = sexp[tl * NS + q];
-            const float key = bias ? sg + bias[e] : sg;
-            if (key > bk || (key == bk && e < be)) {
-                bk = key;
-                be = e;
-                bs = sg;
-                bq = q;
-            }
+            const float kq = skey[tl * NS + q];
+            const int eq = sexp[tl * NS + q];
+            rank += (kq > kc[c] || (kq == kc[c] && eq < ec[c])) ? 1 : 0;
         }
-        if (bq >= 0) taken |= 1u << bq;
-        csig[j] = bs;
-        cidx[j] = be;
+        if (rank < K) {
+            osig[tl * kMaxK + rank] = sc[c];
+            oexp[tl * kMaxK + rank] = ec[c];
+        }
     }
-    float den = csig[0];
-#pragma unroll
-    for (int j = 1; j < kMaxK; ++j)
-        if (j < K) den = den + csig[j];
-#pragma unroll
-    for (int j = 0; j < kMaxK; ++j)
-        if (j < K) {
-            topk_idx[(size_t)t * K + j] = cidx[j];
-            topk_gate[(size_t)t * K + j] = csig[j] / den;
-        }
+    __syncthreads();
+    if (t >= T || nc == 0) return;
+    float den = osig[tl * kMaxK];
+    for (int j = 1; j < K; ++j) den = den + osig[tl * kMaxK + j];
+    for (int j = g; j < K; j += LPT) {
+        topk_idx[(size_t)t * K + j] = oexp[tl * kMaxK + j];
+        topk_gate[(size_t)t * K + j] = osig[tl * kMaxK + j] / den;
+    }
 }
 
 // Exact routing of the queued tokens: all E logits by the FMA chain, then
