@@ -713,8 +713,11 @@ void k_gemm_pp(const GemmArgs a) {
     constexpr bool GATHER = GROUPED && EPI == EPI_GELU_STORE;
     constexpr bool SCATTER = EPI == EPI_SCATTER_SLOT;
     constexpr bool OUT_F32 = EPI == EPI_STORE_F32;
+    constexpr bool COMBINE = EPI == EPI_COMBINE;
+    constexpr bool STAGE_F32 = OUT_F32 || COMBINE;  // accumulators staged as fp32
     constexpr int OES = OUT_F32 ? 4 : 2;
-    constexpr int NH = OUT_F32 ? 2 : 1;        // column halves per staged block (256-byte rows)
+    constexpr int NH = STAGE_F32 ? 2 : 1;      // column halves per staged block (256-byte rows)
+    static_assert(!(COMBINE && GROUPED), "the fused combine is a dense (shared expert) epilogue");
     constexpr int STG_WAVE = 32 * 256;         // staging bytes per wave
     static_assert(NW * STG_WAVE == SLAB, "staging must fill exactly one token slot");
     __shared__ __attribute__((aligned(1024))) uint8_t smem[AST * SLAB + WST * SLAB];
@@ -901,6 +904,87 @@ void k_gemm_pp(const GemmArgs a) {
         });
     };
 
+    // Fused combine (K = 8) for one staged fp32 block of the shared expert's
+    // output S: 32 rows x 64 columns, pieces of 8 columns (lanes 8 r + c take
+    // row r, column piece c; four rows per lane). Per piece, in the order of
+    // the separate combine: acc = 0, acc = fma(g_j, O_j, acc) for j = 0..7,
+    // acc = fma(lambda, S, acc), one rounding to bf16.
+    auto combine_block = [&](const Tile& t, uint32_t stg, int i, int h) {
+        constexpr int KC = 8;
+        const int cp = lane & 7;
+        const bf16_t* const eo = static_cast<const bf16_t*>(a.eo);
+        // y rows of this tile; stores of pad rows fall outside and are dropped,
+        // so the four pieces need no branch and can be scheduled together.
+        const __amdgpu_buffer_rsrc_t yres =
+            make_rsrc(static_cast<uint8_t*>(a.C) + (size_t)t.row0 * a.N * 2, (uint32_t)t.rows * a.N * 2);
+        u32x4_t s0[4], s1[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int rr = (lane >> 3) + 8 * k;
+            s0[k] = lds_read16u_asm(stg + (uint32_t)rr * 256u + ((uint32_t)((2 * cp) ^ (rr & 15)) << 4));
+            s1[k] = lds_read16u_asm(stg + (uint32_t)rr * 256u + ((uint32_t)((2 * cp + 1) ^ (rr & 15)) << 4));
+        }
+        // No memory clobber: the loads below may be scheduled across it.
+        asm volatile("s_waitcnt lgkmcnt(0)");
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            tie(s0[k]);
+            tie(s1[k]);
+        }
+        // Two pieces per step: both pieces' loads are issued before either is
+        // used (twenty 16-byte loads in flight per lane).
+#pragma unroll
+        for (int kp = 0; kp < 4; kp += 2) {
+            float4 g[2][2];
+            u32x4_t o[2][KC];
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                const int rr = (lane >> 3) + 8 * (kp + u);
+                const int tok = t.row0 + min(wm * WT + i * 32 + rr, t.rows - 1);
+                const int c0 = t.n0 + wn * WT + h * 64 + cp * 8;
+                g[u][0] = *reinterpret_cast<const float4*>(a.gate + (size_t)tok * KC);
+                g[u][1] = *reinterpret_cast<const float4*>(a.gate + (size_t)tok * KC + 4);
+#pragma unroll
+                for (int j = 0; j < KC; ++j)
+                    o[u][j] = *reinterpret_cast<const u32x4_t*>(eo + ((size_t)tok * KC + j) * a.N + c0);
+            }
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                const int k = kp + u;
+                const int r = wm * WT + i * 32 + (lane >> 3) + 8 * k;
+                const int c0 = t.n0 + wn * WT + h * 64 + cp * 8;
+                const float gj[KC] = {g[u][0].x, g[u][0].y, g[u][0].z, g[u][0].w,
+                                      g[u][1].x, g[u][1].y, g[u][1].z, g[u][1].w};
+                float acc8[8];
+#pragma unroll
+                for (int q = 0; q < 8; ++q) acc8[q] = 0.0f;
+#pragma unroll
+                for (int j = 0; j < KC; ++j)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        acc8[2 * q] = fmaf(gj[j], __uint_as_float(o[u][j][q] << 16), acc8[2 * q]);
+                        acc8[2 * q + 1] = fmaf(gj[j], __uint_as_float(o[u][j][q] & 0xffff0000u), acc8[2 * q + 1]);
+                    }
+                const float sv[8] = {__uint_as_float(s0[k].x), __uint_as_float(s0[k].y), __uint_as_float(s0[k].z),
+                                     __uint_as_float(s0[k].w), __uint_as_float(s1[k].x), __uint_as_float(s1[k].y),
+                                     __uint_as_float(s1[k].z), __uint_as_float(s1[k].w)};
+                u32x4_t out;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    uint32_t lo = __float_as_uint(fmaf(a.lambda, sv[2 * q], acc8[2 * q]));
+                    uint32_t hi = __float_as_uint(fmaf(a.lambda, sv[2 * q + 1], acc8[2 * q + 1]));
+                    lo += 0x7fffu + ((lo >> 16) & 1u);  // round to nearest even (finite values)
+                    hi += 0x7fffu + ((hi >> 16) & 1u);
+                    out[q] = (lo >> 16) | (hi & 0xffff0000u);
+                }
+                // y is written only here and read by nothing in this kernel, so
+                // the store needs no memory clobber.
+                const uint32_t yoff = ((uint32_t)r * (uint32_t)a.N + (uint32_t)c0) * 2u;
+                asm volatile("buffer_store_dwordx4 %0, %1, %2, 0 offen\n\ts_nop 0" ::"v"(out), "v"(yoff), "s"(yres));
+            }
+        }
+    };
+
     // Epilogue of tile t from the accumulators, staged through the token slot
     // `stslot`: per 32-row block (and 64-column half for fp32 output) each
     // lane writes its row's runs into the wave's 8 KB, then reads back 16-byte
@@ -915,7 +999,7 @@ void k_gemm_pp(const GemmArgs a) {
 #pragma unroll
             for (int h = 0; h < NH; ++h) {
                 __builtin_amdgcn_sched_barrier(0);
-                if (OUT_F32) {
+                if (STAGE_F32) {
 #pragma unroll
                     for (int jj = 0; jj < 2; ++jj)
 #pragma unroll
@@ -943,6 +1027,10 @@ void k_gemm_pp(const GemmArgs a) {
                             lds_write8_asm(wrow + ((uint32_t)(chunk ^ sw) << 4) + (uint32_t)fk * 8u,
                                            (u32x2_t){pk.x, pk.y});
                         }
+                }
+                if constexpr (COMBINE) {
+                    combine_block(t, stg, i, h);
+                    continue;
                 }
                 u32x4_t v[8];
 #pragma unroll
@@ -1032,6 +1120,11 @@ void k_gemm_pp(const GemmArgs a) {
         if (GATHER && has_nn) load_tokens(tnn, tok);
         // The last slab's token slot is free (and read by no wave any more).
         epilogue(tc, as == 0 ? AST - 1 : as - 1);
+        // The combine's loads land in registers the next K loop reuses; a wait
+        // the compiler sees (vmcnt(0)) retires them here, once per tile,
+        // instead of the conservative waits it would otherwise put at the head
+        // of every K step.
+        if (COMBINE) __builtin_amdgcn_s_waitcnt(0xF70);
         if (!has_n) break;
 
         // Advance: n -> c, nn -> n, and the table entry of the tile after that.
@@ -1229,6 +1322,10 @@ hipError_t dispatch(const moe_desc_t& d, int epilogue, int bm, const GemmArgs& a
             case EPI_STORE_F32:
                 if (!GROUPED) return dispatch_bf16<EPI_STORE_F32, false>(bm, a, s);
                 break;
+            case EPI_COMBINE:
+                if (!GROUPED && gemm_combine_fusable(d, bm, a.N, a.Kdim) && a.route_k == d.K)
+                    return launch_pp<EPI_COMBINE, false>(a, s);
+                break;
         }
     } else {
         if (bm != 64) return hipErrorInvalidValue;
@@ -1257,6 +1354,11 @@ int gemm_dense_bm(int32_t dtype, int64_t rows, int32_t n) {
     // 256-row tiles only when they still give a few workgroups per CU.
     const int64_t tiles = (rows + 255) / 256 * (n / 256 > 0 ? n / 256 : 1);
     return tiles >= 512 ? 256 : 64;
+}
+
+bool gemm_combine_fusable(const moe_desc_t& d, int bm, int n, int kdim) {
+    // The persistent 256 x 256 kernel with its K = 8 combine epilogue.
+    return d.dtype == MOE_BF16 && d.K == 8 && bm == 256 && n % 256 == 0 && kdim >= 128;
 }
 
 hipError_t launch_gemm(const moe_desc_t& d, int epilogue, int bm, const GemmArgs& a, hipStream_t s) {

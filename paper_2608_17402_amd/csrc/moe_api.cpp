@@ -219,8 +219,18 @@ static moe_status_t enqueue_routed_mlp(const moe_desc_t& d, const WorkspacePlan&
 }
 
 // Shared expert over all T tokens in token order, fp32 output for the combine.
+// With `fuse` (expert outputs, gates and y given) and a shape the fused
+// epilogue supports, fc2 also performs the combine and writes y; *fused tells
+// whether it did (the separate combine is then skipped).
+struct CombineArgs {
+    const void* expert_out;
+    const float* gate;
+    void* y;
+};
 static moe_status_t enqueue_shared_mlp(const moe_desc_t& d, const WorkspacePlan& p, void* ws, const void* x,
-                                       const void* w1s, const void* w2s, float* sout, hipStream_t s) {
+                                       const void* w1s, const void* w2s, float* sout, hipStream_t s,
+                                       const CombineArgs* fuse = nullptr, bool* fused = nullptr) {
+    if (fused) *fused = false;
     const int bm = gemm_dense_bm(d.dtype, d.T, d.h_shared < d.d ? d.h_shared : d.d);
     GemmArgs g{};
     g.A = x;
@@ -241,6 +251,16 @@ static moe_status_t enqueue_shared_mlp(const moe_desc_t& d, const WorkspacePlan&
     g2.N = d.d;
     g2.Kdim = d.h_shared;
     g2.a_bytes = (uint32_t)((size_t)d.T * d.h_shared * elem_size(d.dtype));
+    if (fuse && fused && gemm_combine_fusable(d, bm, g2.N, g2.Kdim)) {
+        g2.C = fuse->y;
+        g2.gate = fuse->gate;
+        g2.eo = fuse->expert_out;
+        g2.lambda = d.lambda;
+        g2.route_k = d.K;
+        HIP_CHECK(launch_gemm(d, EPI_COMBINE, bm, g2, s), "shared fc2 gemm with the combine");
+        *fused = true;
+        return MOE_OK;
+    }
     HIP_CHECK(launch_gemm(d, EPI_STORE_F32, bm, g2, s), "shared fc2 gemm");
     return MOE_OK;
 }
@@ -374,7 +394,11 @@ MOE_API moe_status_t moe_layer_forward(const moe_desc_t* desc, const void* x, co
                              p.n_hist_blocks, s),
               "permute");
     CHECK(enqueue_routed_mlp(d, p, workspace, x, slots, offsets, w1, w2, eout, s, events));
-    if (d.h_shared) CHECK(enqueue_shared_mlp(d, p, workspace, x, w1s, w2s, sout, s));
-    HIP_CHECK(launch_combine(d, eout, gate, sout, 1, y, s), "combine");
+    bool fused = false;
+    if (d.h_shared) {
+        const CombineArgs c{eout, gate, y};
+        CHECK(enqueue_shared_mlp(d, p, workspace, x, w1s, w2s, sout, s, &c, &fused));
+    }
+    if (!fused) HIP_CHECK(launch_combine(d, eout, gate, sout, 1, y, s), "combine");
     return ok();
 }

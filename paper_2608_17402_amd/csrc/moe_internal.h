@@ -38,6 +38,8 @@ enum GemmEpilogue : int {
     EPI_GELU_STORE = 0,     // C[p, :] = act(GELU(acc)) at the sorted position p
     EPI_SCATTER_SLOT = 1,   // C[sorted_slots[p], :] = acc  (expert_out in slot order)
     EPI_STORE_F32 = 2,      // C[p, :] = acc as fp32 (shared expert output)
+    EPI_COMBINE = 3,        // C[p, :] = y_p = out(sum_j gate[p, j] eo[p K + j, :] + lambda acc): the
+                            // gate-weighted combine fused into the shared expert's fc2 (dense only)
 };
 
 struct GemmArgs {
@@ -55,6 +57,9 @@ struct GemmArgs {
     int32_t max_tiles;         // upper bound on the number of M-tiles (grid sizing)
     int64_t b_group_stride;    // elements between consecutive experts' weights
     uint32_t a_bytes;          // bytes of the A operand buffer (bounds of its buffer resource)
+    const float* gate;         // EPI_COMBINE: gates [rows, route_k]
+    const void* eo;            // EPI_COMBINE: expert outputs [rows * route_k, N] in slot order
+    float lambda;              // EPI_COMBINE: shared-expert weight
 };
 
 // Offsets (bytes) of every workspace region for one descriptor.
@@ -95,6 +100,8 @@ hipError_t launch_permute(const moe_desc_t& d, const int32_t* topk_idx, int32_t*
 hipError_t launch_build_tiles(int32_t E, int32_t bm, int32_t max_tiles, const int32_t* offsets,
                               TileDesc* tiles, int32_t* n_tiles, hipStream_t s);
 hipError_t launch_gemm(const moe_desc_t& d, int epilogue, int bm, const GemmArgs& a, hipStream_t s);
+// Whether launch_gemm(EPI_COMBINE) supports this dense GEMM (M-tile bm, N columns, K = kdim).
+bool gemm_combine_fusable(const moe_desc_t& d, int bm, int n, int kdim);
 hipError_t launch_combine(const moe_desc_t& d, const void* expert_out, const float* gate,
                           const void* shared, int shared_is_f32, void* y, hipStream_t s);
 

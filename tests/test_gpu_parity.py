@@ -298,3 +298,26 @@ def test_full_size_route_and_sampled_layer(name):
                                    inp.f32("w2s"), cfg.K, cfg.lam, True, tokens=tok)
     assert np.array_equal(o_idx, ref_idx[tok])
     check_close(host(y)[tok], y_ref, True, f"{name} sampled y")
+
+
+@pytest.mark.slow
+def test_shared_fc2_with_fused_combine_ragged_tail():
+    """ViT-G shape at a token count where the shared expert runs on 256-row
+    tiles, so its fc2 also performs the gate-weighted combine, with a partial
+    last tile: sampled tokens (including every token of the tail tile) match
+    the oracle, and a repeat is bit-identical."""
+    cfg = get_config("c4").with_tokens(89 * 256 - 179)
+    inp = make_inputs(cfg)
+    lay = DeviceLayer(inp)
+    y, idx, gate = lay.forward()
+    y2, _, _ = lay.forward()
+    torch.cuda.synchronize()
+    assert np.array_equal(host(y).view(np.uint16), host(y2).view(np.uint16))
+    x, wr = inp.f32("x"), inp.f32("w_router")
+    rng = np.random.default_rng(1)
+    tail = np.arange(88 * 256, cfg.T)
+    tok = np.unique(np.r_[0, rng.choice(88 * 256, 24, replace=False), tail[::4], cfg.T - 1]).astype(np.int32)
+    o_idx, _, y_ref = oracle.layer(x, wr, inp.bias, inp.f32("w1"), inp.f32("w2"), inp.f32("w1s"),
+                                   inp.f32("w2s"), cfg.K, cfg.lam, True, tokens=tok)
+    assert np.array_equal(host(idx)[tok], o_idx)
+    check_close(host(y)[tok], y_ref, True, "fused-combine sampled y")
