@@ -5,6 +5,9 @@ this package. The GPU path never does.
 """
 
 from .oracle import (  # noqa: F401
+    BIAS_SIGN,
+    BIAS_ZSCORE,
+    bias_update,
     build_oracle,
     combine,
     expert_rows,

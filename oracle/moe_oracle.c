@@ -14,6 +14,8 @@
  *   layer output         y = sum_T g'_e E_e(x) + lambda * shared(x)   Eq. (6)
  *   permutation          sort slots by expert, bincount, cumsum       App. "MoE Kernel", Algorithm 1 Phase 1
  *   expert MLP           E(x) = W2 GELU(W1 x), no linear biases
+ *   bias update          b_e -= alpha sign(t_e - mu)  or  alpha (t_e - mu) / sigma
+ *                                                       Sec. 3.2 "Load Balancing", Eqs. (8)-(9)
  *
  * Precision. Everything that is a plain definition (expert MLPs, combine) is
  * evaluated in double precision. Routing decides integers (which experts a
@@ -36,6 +38,17 @@
  *   - in a bf16 layer the expert activation GELU(W1 x) is materialised in bf16
  *     (round to nearest even) before fc2, as the paper's kernel writes its
  *     activation tile to a buffer; nothing else is rounded here.
+ *   - bias update: t_e is the number of tokens routed to expert e (the
+ *     permutation's counts), mu their mean over the E experts, sigma their
+ *     standard deviation over the E experts (the whole population: divided
+ *     by E); sign(0) = 0; when sigma = 0 (all counts equal) the z-score
+ *     update changes nothing. The sign decision is exact (E t_e against the
+ *     integer sum); the sign update is one fp32 add of -alpha, +alpha or
+ *     nothing. The z-score update is evaluated in double precision in a fixed
+ *     order (mean by one division, variance summed over e ascending with a
+ *     separate multiply and add, correctly rounded square root) and rounded
+ *     to fp32 once, so an implementation following the same order agrees
+ *     bit for bit.
  *
  * Build: gcc -O2 -mfma -ffp-contract=off -fopenmp -fPIC -shared (no fast-math).
  */
@@ -312,5 +325,37 @@ void oracle_layer(int n_tok, const int32_t *tok, int T, int d, int E, int K, int
         free(o);
         free(idx);
         free(g);
+    }
+}
+
+/* Loss-free balancing bias update (Sec. 3.2 "Load Balancing"): rule 0 is the
+ * sign update of Eq. (8), rule 1 the z-score update of Eq. (9). counts[E]
+ * are the tokens routed to each expert in this iteration; bias[E] is updated
+ * in place with step alpha. */
+void oracle_bias_update(int E, const int32_t *counts, float *bias, float alpha, int rule) {
+    long long total = 0;
+    for (int e = 0; e < E; ++e) total += counts[e];
+    if (rule == 0) {
+        for (int e = 0; e < E; ++e) {
+            long long scaled = (long long)E * counts[e]; /* compare t_e with total / E exactly */
+            if (scaled > total) bias[e] = bias[e] - alpha;
+            else if (scaled < total) bias[e] = bias[e] + alpha;
+        }
+        return;
+    }
+    double mu = (double)total / (double)E;
+    double var = 0.0;
+    for (int e = 0; e < E; ++e) {
+        double dev = (double)counts[e] - mu;
+        double sq = dev * dev;
+        var = var + sq;
+    }
+    var = var / (double)E;
+    double sigma = sqrt(var);
+    if (sigma == 0.0) return;
+    for (int e = 0; e < E; ++e) {
+        double z = ((double)counts[e] - mu) / sigma;
+        double step = (double)alpha * z;
+        bias[e] = (float)((double)bias[e] - step);
     }
 }

@@ -66,6 +66,7 @@ def _load():
             "oracle_expert_rows": ([I, I, I, P, P, P, I, P], None),
             "oracle_combine": ([I, I, I, P, P, P, D, P], None),
             "oracle_layer": ([I, P, I, I, I, I, I, I, F, I, P, P, P, P, P, P, P, P, P, P], None),
+            "oracle_bias_update": ([I, P, P, F, I], None),
         }
         for name, (args, res) in sigs.items():
             fn = getattr(lib, name)
@@ -199,3 +200,18 @@ def layer(x, wr, bias, w1, w2, w1s, w2s, K: int, lam: float, act_bf16: bool, tok
                          _ptr(x), _ptr(wr), _ptr(bias), _ptr(w1), _ptr(w2), _ptr(w1s), _ptr(w2s),
                          _ptr(idx), _ptr(gate), _ptr(y))
     return idx, gate, y
+
+
+BIAS_SIGN = 0
+BIAS_ZSCORE = 1
+
+
+def bias_update(counts, bias, alpha: float, rule: int) -> np.ndarray:
+    """Loss-free balancing update of the selection bias (Sec. 3.2 "Load
+    Balancing", Eq. (8) for rule BIAS_SIGN, Eq. (9) for BIAS_ZSCORE) from the
+    per-expert token counts of one iteration. Returns the new fp32 bias."""
+    c = np.ascontiguousarray(counts, dtype=np.int32)
+    b = np.array(bias, dtype=np.float32, copy=True)
+    assert c.shape == b.shape and c.ndim == 1
+    _load().oracle_bias_update(int(c.size), _ptr(c), _ptr(b), float(alpha), int(rule))
+    return b

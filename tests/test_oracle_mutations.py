@@ -40,6 +40,14 @@ MUTANTS = {
     "shared_dropped": ("y[c] += (double)lambda * o[c];", "y[c] += 0.0 * o[c];"),
     "combine_ignores_lambda": ("if (shared) acc += lambda * shared[(size_t)t * d + c];",
                                "if (shared) acc += shared[(size_t)t * d + c];"),
+    "bias_sign_flipped": ("if (scaled > total) bias[e] = bias[e] - alpha;",
+                          "if (scaled > total) bias[e] = bias[e] + alpha;"),
+    "bias_sign_zero_moves": ("else if (scaled < total) bias[e] = bias[e] + alpha;",
+                             "else bias[e] = bias[e] + alpha;"),
+    "zscore_sample_deviation": ("var = var / (double)E;", "var = var / (double)(E - 1);"),
+    "zscore_no_mean": ("double dev = (double)counts[e] - mu;", "double dev = (double)counts[e];"),
+    "zscore_wrong_direction": ("bias[e] = (float)((double)bias[e] - step);",
+                               "bias[e] = (float)((double)bias[e] + step);"),
 }
 
 

@@ -397,3 +397,54 @@ def test_layer_stages_compose_to_layer():
 def test_bf16_round64_helper_agrees():
     v = np.random.default_rng(9).standard_normal(1000)
     assert np.array_equal(bf16_round64(v), oracle.round_bf16(v))
+
+
+# ---- Loss-free balancing bias update (Sec. 3.2 "Load Balancing", Eqs. (8)-(9))
+
+
+def test_bias_update_zscore_closed_form():
+    # counts {1, 2, 3}: mean 2, population deviation sqrt(2/3), so the z-scores
+    # are -sqrt(3/2), 0, +sqrt(3/2); the overloaded expert's bias goes down.
+    out = oracle.bias_update([1, 2, 3], [0.0, 0.0, 0.0], 1.0, oracle.BIAS_ZSCORE)
+    z = math.sqrt(1.5)
+    assert out.tolist() == [np.float32(z), np.float32(0.0), np.float32(-z)]
+    out = oracle.bias_update([1, 2, 3], [0.5, -0.25, 0.125], 0.125, oracle.BIAS_ZSCORE)
+    want = np.array([0.5 + 0.125 * z, -0.25, 0.125 - 0.125 * z]).astype(np.float32)
+    assert np.array_equal(out, want)
+
+
+def test_bias_update_zscore_uses_population_deviation():
+    rng = np.random.default_rng(7)
+    for E in (8, 64, 256):
+        counts = rng.integers(0, 5000, size=E).astype(np.int32)
+        out = -oracle.bias_update(counts, np.zeros(E, np.float32), 1.0, oracle.BIAS_ZSCORE).astype(np.float64)
+        # z-scores over the whole population: mean 0 and mean square 1
+        assert abs(out.sum()) < 1e-4 and abs((out ** 2).mean() - 1.0) < 1e-6
+        c = counts.astype(np.float64)
+        ref = (c - c.mean()) / c.std(ddof=0)
+        assert np.max(np.abs(out - ref)) <= 1e-6 * max(1.0, np.max(np.abs(ref)))
+        b = rng.normal(0, 0.05, E).astype(np.float32)
+        got = oracle.bias_update(counts, b, 0.01, oracle.BIAS_ZSCORE)
+        want = (b.astype(np.float64) - 0.01 * np.float64(np.float32(1)) * ref).astype(np.float32)
+        assert np.max(np.abs(got.astype(np.float64) - want)) <= np.spacing(np.abs(want)).max()
+
+
+def test_bias_update_sign_rule():
+    b = np.array([0.5, 0.5, 0.5, 0.5], np.float32)
+    out = oracle.bias_update([5, 1, 3, 3], b, 0.25, oracle.BIAS_SIGN)
+    assert out.tolist() == [0.25, 0.75, 0.5, 0.5]
+    # a fractional mean (1.5): both experts move, in opposite directions
+    out = oracle.bias_update([1, 2], [0.0, 0.0], 0.125, oracle.BIAS_SIGN)
+    assert out.tolist() == [0.125, -0.125]
+    # the update is one fp32 add of -alpha or +alpha
+    b = np.array([0.1, 0.1], np.float32)
+    out = oracle.bias_update([3, 0], b, np.float32(0.3), oracle.BIAS_SIGN)
+    assert out.tolist() == [np.float32(np.float32(0.1) - np.float32(0.3)), np.float32(np.float32(0.1) + np.float32(0.3))]
+
+
+def test_bias_update_balanced_load_changes_nothing():
+    b = np.array([0.3, -0.2, 0.0, 1e-3], np.float32)
+    for rule in (oracle.BIAS_SIGN, oracle.BIAS_ZSCORE):
+        assert np.array_equal(oracle.bias_update([7, 7, 7, 7], b, 0.5, rule), b)
+        assert np.array_equal(oracle.bias_update([0, 0, 0, 0], b, 0.5, rule), b)
+    assert np.array_equal(oracle.bias_update([9], [0.25], 1.0, oracle.BIAS_ZSCORE), np.float32([0.25]))
