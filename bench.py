@@ -69,11 +69,10 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=15.0,
                    help="target CPU time of the oracle sample")
     p.add_argument("--stage-reps", type=int, default=10)
-    p.add_argument("--mode", choices=("layer", "gemm", "copy", "read"), default="layer",
+    p.add_argument("--mode", choices=("layer", "gemm", "copy"), default="layer",
                    help="layer: the benchmark; gemm: only the routed grouped GEMMs of --config, repeated "
                         "(hardware-counter runs); copy: a plain device copy of --copy-mib MiB "
-                        "(calibration of the byte counters); read: a library reduction over --copy-mib MiB "
-                        "(the achievable HBM read rate, for context)")
+                        "(calibration of the byte counters)")
     p.add_argument("--copy-mib", type=int, default=1024)
     return p.parse_args()
 
@@ -165,18 +164,6 @@ def main():
         ms = time_calls(lambda: b.copy_(a), args.steps)
         print(json.dumps({"mode": "copy", "bytes_read_per_launch": n, "bytes_written_per_launch": n,
                           "avg_us": round(ms * 1e3, 2), "gbs": round(2 * n / (ms * 1e-3) / 1e9, 1)}), flush=True)
-        return
-
-    if args.mode == "read":
-        # Achievable HBM read rate on this machine, for context: a library
-        # reduction over a buffer far larger than the caches.
-        n = args.copy_mib << 20
-        a = torch.ones(n // 2, dtype=torch.bfloat16, device="cuda")
-        for _ in range(args.warmup):
-            a.sum(dtype=torch.float32)
-        ms = time_calls(lambda: a.sum(dtype=torch.float32), args.steps)
-        print(json.dumps({"mode": "read", "bytes_read_per_launch": n, "avg_us": round(ms * 1e3, 2),
-                          "gbs": round(n / (ms * 1e-3) / 1e9, 1)}), flush=True)
         return
 
     cfg = get_config(args.config)

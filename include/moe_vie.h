@@ -158,6 +158,29 @@ moe_status_t moe_layer_forward(const moe_desc_t *desc, const void *x, const void
                                float *topk_gate_out, void *workspace, size_t workspace_bytes,
                                void *const *events, void *stream);
 
+/* Rules of moe_bias_update. */
+typedef enum { MOE_BIAS_SIGN = 0, MOE_BIAS_ZSCORE = 1 } moe_bias_rule_t;
+
+/* Loss-free load balancing (Sec. 3.2 "Load Balancing"): update the selection
+ * bias in place from one iteration's token counts.
+ *   counts [E] int32 in: tokens routed to each expert (as moe_permute
+ *          produces them; non-negative)
+ *   bias   [E] fp32 in/out
+ *   alpha  step size, finite and >= 0
+ *   rule   MOE_BIAS_SIGN:   b_e <- b_e - alpha * sign(t_e - mu)      (Eq. (8))
+ *          MOE_BIAS_ZSCORE: b_e <- b_e - alpha * (t_e - mu) / sigma  (Eq. (9))
+ * mu is the mean of the E counts and sigma their standard deviation over the
+ * E experts (divided by E). sign(0) = 0; sigma = 0 (all counts equal) leaves
+ * the bias unchanged. The sign is decided exactly (E t_e against the sum of
+ * the counts) and applied as one fp32 add of -alpha or +alpha. The z-score
+ * rule is evaluated in double precision in a fixed order - mu = sum / E;
+ * variance = (sum over e = 0..E-1 of (t_e - mu)^2, each square and each add
+ * rounded) / E; sigma = correctly rounded sqrt; z = (t_e - mu) / sigma;
+ * b_e - alpha z - and rounded to fp32 once, so it is reproducible bit for bit.
+ * Only desc->E is used (desc must still be valid). No workspace. */
+moe_status_t moe_bias_update(const moe_desc_t *desc, const int32_t *counts, float *bias, float alpha,
+                             int32_t rule, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

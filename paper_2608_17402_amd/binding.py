@@ -26,7 +26,9 @@ STATUS = {0: "MOE_OK", 1: "MOE_ERR_INVALID_ARG", 2: "MOE_ERR_UNSUPPORTED", 3: "M
 
 # Public entry points declared in include/moe_vie.h.
 EXPORTS = ("moe_status_string", "moe_last_error", "moe_workspace_size", "moe_route", "moe_permute",
-           "moe_grouped_mlp", "moe_combine", "moe_layer_forward")
+           "moe_grouped_mlp", "moe_combine", "moe_layer_forward", "moe_bias_update")
+MOE_BIAS_SIGN = 0
+MOE_BIAS_ZSCORE = 1
 
 
 class MoeDesc(ctypes.Structure):
@@ -82,6 +84,8 @@ def load(path: Optional[str] = None):
     lib.moe_combine.restype = st
     lib.moe_layer_forward.argtypes = [D, P, P, P, P, P, P, P, P, P, P, P, S, P, P]
     lib.moe_layer_forward.restype = st
+    lib.moe_bias_update.argtypes = [D, P, P, ctypes.c_float, ctypes.c_int32, P]
+    lib.moe_bias_update.restype = st
     if path is None:
         _lib = lib
     return lib
@@ -179,6 +183,13 @@ def moe_layer_forward(desc, x, w_router, bias, w1, w2, w1s, w2s, y, topk_idx_out
                                     _ptr(topk_gate_out, "topk_gate_out", torch.float32),
                                     _ptr(workspace, "workspace"), workspace.numel(), ev, _stream(stream)),
            "moe_layer_forward")
+
+
+def moe_bias_update(desc, counts, bias, alpha: float, rule: int, stream=None):
+    """Loss-free balancing update of `bias` in place from per-expert `counts`."""
+    _check(load().moe_bias_update(ctypes.byref(desc), _ptr(counts, "counts", torch.int32),
+                                  _ptr(bias, "bias", torch.float32), float(alpha), int(rule), _stream(stream)),
+           "moe_bias_update")
 
 
 class HipEvents:

@@ -402,3 +402,18 @@ MOE_API moe_status_t moe_layer_forward(const moe_desc_t* desc, const void* x, co
     if (!fused) HIP_CHECK(launch_combine(d, eout, gate, sout, 1, y, s), "combine");
     return ok();
 }
+
+MOE_API moe_status_t moe_bias_update(const moe_desc_t* desc, const int32_t* counts, float* bias, float alpha,
+                                     int32_t rule, void* stream) {
+    CHECK(check_desc(desc));
+    CHECK(check_ptr(counts, "counts"));
+    CHECK(check_ptr(bias, "bias"));
+    if (!(alpha >= 0.0f) || !(alpha <= 3.402823466e38f))
+        return fail(MOE_ERR_INVALID_ARG, "alpha must be finite and >= 0");
+    if (rule != MOE_BIAS_SIGN && rule != MOE_BIAS_ZSCORE)
+        return fail(MOE_ERR_INVALID_ARG, "rule must be MOE_BIAS_SIGN or MOE_BIAS_ZSCORE");
+    (void)hipGetLastError();
+    HIP_CHECK(launch_bias_update(desc->E, counts, bias, alpha, rule, static_cast<hipStream_t>(stream)),
+              "bias update");
+    return ok();
+}

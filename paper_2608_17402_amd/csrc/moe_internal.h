@@ -102,6 +102,8 @@ hipError_t launch_build_tiles(int32_t E, int32_t bm, int32_t max_tiles, const in
 hipError_t launch_gemm(const moe_desc_t& d, int epilogue, int bm, const GemmArgs& a, hipStream_t s);
 // Whether launch_gemm(EPI_COMBINE) supports this dense GEMM (M-tile bm, N columns, K = kdim).
 bool gemm_combine_fusable(const moe_desc_t& d, int bm, int n, int kdim);
+hipError_t launch_bias_update(int32_t E, const int32_t* counts, float* bias, float alpha, int32_t rule,
+                              hipStream_t s);
 hipError_t launch_combine(const moe_desc_t& d, const void* expert_out, const float* gate,
                           const void* shared, int shared_is_f32, void* y, hipStream_t s);
 

@@ -29,7 +29,7 @@ def lib():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for n in ("moe_route", "moe_permute", "moe_grouped_mlp", "moe_combine", "moe_layer_forward",
-              "moe_workspace_size", "moe_status_string", "moe_last_error"):
+              "moe_bias_update", "moe_workspace_size", "moe_status_string", "moe_last_error"):
         assert n in names
     assert set(names) == set(binding.EXPORTS)
 
@@ -109,3 +109,21 @@ def test_entry_points_reject_bad_pointers_before_any_launch(lib):
     assert lib.moe_layer_forward(ctypes.byref(desc0), fake, fake, None, fake, fake, None, None, fake, None,
                                  None, fake, S(need), half, None) == 1
     assert b"events" in lib.moe_last_error()
+
+
+def test_bias_update_rejects_bad_arguments(lib):
+    desc = binding.make_desc(100, 64, 8, 2, 64)
+    P = ctypes.c_void_p
+    fake = P(1 << 20)
+    d = ctypes.byref(desc)
+    assert lib.moe_bias_update(d, None, fake, ctypes.c_float(0.1), 1, None) == 1
+    assert b"counts" in lib.moe_last_error()
+    assert lib.moe_bias_update(d, fake, None, ctypes.c_float(0.1), 1, None) == 1
+    assert lib.moe_bias_update(d, fake, fake, ctypes.c_float(float("nan")), 1, None) == 1
+    assert b"alpha" in lib.moe_last_error()
+    assert lib.moe_bias_update(d, fake, fake, ctypes.c_float(-1.0), 0, None) == 1
+    assert lib.moe_bias_update(d, fake, fake, ctypes.c_float(float("inf")), 0, None) == 1
+    assert lib.moe_bias_update(d, fake, fake, ctypes.c_float(0.1), 2, None) == 1
+    assert b"rule" in lib.moe_last_error()
+    bad = binding.make_desc(100, 64, 8, 0, 64)
+    assert lib.moe_bias_update(ctypes.byref(bad), fake, fake, ctypes.c_float(0.1), 0, None) == 1

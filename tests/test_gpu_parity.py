@@ -321,3 +321,44 @@ def test_shared_fc2_with_fused_combine_ragged_tail():
                                    inp.f32("w2s"), cfg.K, cfg.lam, True, tokens=tok)
     assert np.array_equal(host(idx)[tok], o_idx)
     check_close(host(y)[tok], y_ref, True, "fused-combine sampled y")
+
+
+@pytest.mark.parametrize("E", [1, 3, 8, 64, 256, 1024])
+def test_bias_update_bit_exact(E):
+    """Loss-free balancing update (Eqs. (8)-(9)) through the C ABI against the
+    oracle, bit for bit: random loads, a skewed load, a balanced load."""
+    rng = np.random.default_rng(100 + E)
+    desc = binding.make_desc(64, 64, E, 1, 64)
+    for rule in (binding.MOE_BIAS_SIGN, binding.MOE_BIAS_ZSCORE):
+        for case in ("random", "skewed", "balanced"):
+            if case == "random":
+                counts = rng.integers(0, 20000, size=E)
+            elif case == "skewed":
+                counts = (rng.zipf(1.2, size=E) % 65536) * 8
+            else:
+                counts = np.full(E, 77)
+            counts = counts.astype(np.int32)
+            b = rng.normal(0, 0.05, E).astype(np.float32)
+            alpha = float(np.float32(rng.uniform(1e-4, 0.1)))
+            db = dev(b)
+            binding.moe_bias_update(desc, dev(counts), db, alpha, rule)
+            torch.cuda.synchronize()
+            want = oracle.bias_update(counts, b, alpha, rule)
+            assert np.array_equal(host(db).view(np.uint32), want.view(np.uint32)), (rule, case)
+
+
+def test_bias_update_from_permute_counts(small):
+    """Route, permute and update the bias on the GPU; the counts and the new
+    bias match the oracle's."""
+    cfg, inp, lay, _, ref_idx, _ = small
+    idx, _ = lay.route()
+    counts, _, _ = lay.permute(idx)
+    rc, _, _ = oracle.permute(ref_idx, cfg.E)
+    assert np.array_equal(host(counts), rc)
+    b0 = inp.bias if inp.bias is not None else np.zeros(cfg.E, np.float32)
+    for rule in (binding.MOE_BIAS_SIGN, binding.MOE_BIAS_ZSCORE):
+        db = dev(np.asarray(b0, np.float32))
+        binding.moe_bias_update(lay.desc, counts, db, 1e-3, rule)
+        torch.cuda.synchronize()
+        want = oracle.bias_update(rc, b0, np.float32(1e-3), rule)
+        assert np.array_equal(host(db).view(np.uint32), want.view(np.uint32))
