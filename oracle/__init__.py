@@ -20,5 +20,6 @@ from .oracle import (  # noqa: F401
     route,
     scores,
     sigmoid,
+    silu,
     topk_from_scores,
 )

@@ -14,6 +14,7 @@
  *   layer output         y = sum_T g'_e E_e(x) + lambda * shared(x)   Eq. (6)
  *   permutation          sort slots by expert, bincount, cumsum       App. "MoE Kernel", Algorithm 1 Phase 1
  *   expert MLP           E(x) = W2 GELU(W1 x), no linear biases
+ *   SwiGLU expert MLP    E(x) = W2 (SiLU(W1 x) * (W3 x))   App. "MoE Kernel", Algorithm 1 Phase 2
  *   bias update          b_e -= alpha sign(t_e - mu)  or  alpha (t_e - mu) / sigma
  *                                                       Sec. 3.2 "Load Balancing", Eqs. (8)-(9)
  *
@@ -226,15 +227,28 @@ double oracle_round_bf16(double v) {
     return ldexp(q, ex - 8);
 }
 
-/* One expert MLP applied to one input row: out = W2 act(W1 x).
- *   x[d], w1[h, d] (row e of W1 is hidden unit e), w2[d, h], hid[h] scratch. */
-static void expert_row(int d, int h, const float *x, const float *w1, const float *w2,
+/* SiLU (swish): v * Sigmoid(v) = v / (1 + exp(-v)). */
+double oracle_silu(double v) { return v / (1.0 + exp(-v)); }
+
+/* One expert MLP applied to one input row: out = W2 act(W1 x), with
+ *   GELU experts (swiglu = 0):   act(W1 x) = GELU(W1 x), w1[h, d];
+ *   SwiGLU experts (swiglu = 1): act = SiLU(W1 x) * (W3 x) elementwise, w1 holds
+ *                                W1 (gate) rows 0..h-1 then W3 (up) rows h..2h-1.
+ *   x[d], w2[d, h], hid[h] scratch; row k of W1 / W3 is hidden unit k. */
+static void expert_row(int d, int h, int swiglu, const float *x, const float *w1, const float *w2,
                        int act_bf16, double *hid, double *out) {
     for (int k = 0; k < h; ++k) {
         const float *w = w1 + (size_t)k * d;
         double a = 0.0;
         for (int i = 0; i < d; ++i) a += (double)w[i] * (double)x[i];
-        a = oracle_gelu(a);
+        if (swiglu) {
+            const float *wu = w1 + ((size_t)h + k) * d;
+            double up = 0.0;
+            for (int i = 0; i < d; ++i) up += (double)wu[i] * (double)x[i];
+            a = oracle_silu(a) * up;
+        } else {
+            a = oracle_gelu(a);
+        }
         hid[k] = act_bf16 ? oracle_round_bf16(a) : a;
     }
     for (int c = 0; c < d; ++c) {
@@ -245,17 +259,28 @@ static void expert_row(int d, int h, const float *x, const float *w1, const floa
     }
 }
 
-/* out[n, :] = W2 act(W1 rows[n, :]) for n rows through one expert's weights. */
-void oracle_expert_rows(int n, int d, int h, const float *rows, const float *w1,
+static void expert_rows(int n, int d, int h, int swiglu, const float *rows, const float *w1,
                         const float *w2, int act_bf16, double *out) {
 #pragma omp parallel
     {
         double *hid = (double *)malloc(sizeof(double) * (size_t)h);
 #pragma omp for schedule(static)
         for (int r = 0; r < n; ++r)
-            expert_row(d, h, rows + (size_t)r * d, w1, w2, act_bf16, hid, out + (size_t)r * d);
+            expert_row(d, h, swiglu, rows + (size_t)r * d, w1, w2, act_bf16, hid, out + (size_t)r * d);
         free(hid);
     }
+}
+
+/* out[n, :] = W2 act(W1 rows[n, :]) for n rows through one expert's weights. */
+void oracle_expert_rows(int n, int d, int h, const float *rows, const float *w1,
+                        const float *w2, int act_bf16, double *out) {
+    expert_rows(n, d, h, 0, rows, w1, w2, act_bf16, out);
+}
+
+/* The same with a SwiGLU expert: w13[2h, d] (gate rows, then up rows). */
+void oracle_expert_rows_swiglu(int n, int d, int h, const float *rows, const float *w13,
+                               const float *w2, int act_bf16, double *out) {
+    expert_rows(n, d, h, 1, rows, w13, w2, act_bf16, out);
 }
 
 /* --------------------------------------------------------------- combine */
@@ -285,11 +310,11 @@ void oracle_combine(int T, int d, int K, const double *expert_out, const float *
  *   idx_out[n_tok, K], gate_out[n_tok, K] (either may be NULL), y_out[n_tok, d].
  * Shapes: x[T, d], wr[E, d], bias[E] or NULL, w1[E, h, d], w2[E, d, h],
  * w1s[hs, d], w2s[d, hs] (hs == 0: no shared expert, w1s/w2s ignored). */
-void oracle_layer(int n_tok, const int32_t *tok, int T, int d, int E, int K, int h, int hs,
+static void layer(int n_tok, const int32_t *tok, int d, int E, int K, int h, int hs, int swiglu,
                   float lambda, int act_bf16, const float *x, const float *wr, const float *bias,
                   const float *w1, const float *w2, const float *w1s, const float *w2s,
                   int32_t *idx_out, float *gate_out, double *y_out) {
-    (void)T;
+    const size_t w1_rows = swiglu ? 2 * (size_t)h : (size_t)h; /* rows of one expert's W1 (and W3) */
 #pragma omp parallel
     {
         int hmax = h > hs ? h : hs;
@@ -309,11 +334,12 @@ void oracle_layer(int n_tok, const int32_t *tok, int T, int d, int E, int K, int
             for (int c = 0; c < d; ++c) y[c] = 0.0;
             for (int j = 0; j < K; ++j) {
                 int e = idx[j];
-                expert_row(d, h, xt, w1 + (size_t)e * h * d, w2 + (size_t)e * d * h, act_bf16, hid, o);
+                expert_row(d, h, swiglu, xt, w1 + (size_t)e * w1_rows * d, w2 + (size_t)e * d * h, act_bf16,
+                           hid, o);
                 for (int c = 0; c < d; ++c) y[c] += (double)g[j] * o[c];
             }
             if (hs > 0) {
-                expert_row(d, hs, xt, w1s, w2s, act_bf16, hid, o);
+                expert_row(d, hs, swiglu, xt, w1s, w2s, act_bf16, hid, o);
                 for (int c = 0; c < d; ++c) y[c] += (double)lambda * o[c];
             }
             if (idx_out) memcpy(idx_out + (size_t)p * K, idx, sizeof(int32_t) * (size_t)K);
@@ -326,6 +352,26 @@ void oracle_layer(int n_tok, const int32_t *tok, int T, int d, int E, int K, int
         free(idx);
         free(g);
     }
+}
+
+void oracle_layer(int n_tok, const int32_t *tok, int T, int d, int E, int K, int h, int hs,
+                  float lambda, int act_bf16, const float *x, const float *wr, const float *bias,
+                  const float *w1, const float *w2, const float *w1s, const float *w2s,
+                  int32_t *idx_out, float *gate_out, double *y_out) {
+    (void)T;
+    layer(n_tok, tok, d, E, K, h, hs, 0, lambda, act_bf16, x, wr, bias, w1, w2, w1s, w2s, idx_out, gate_out,
+          y_out);
+}
+
+/* The layer with SwiGLU experts (routed and shared): w13[E, 2h, d] and
+ * w13s[2hs, d] hold the gate rows then the up rows of each expert. */
+void oracle_layer_swiglu(int n_tok, const int32_t *tok, int T, int d, int E, int K, int h, int hs,
+                         float lambda, int act_bf16, const float *x, const float *wr, const float *bias,
+                         const float *w13, const float *w2, const float *w13s, const float *w2s,
+                         int32_t *idx_out, float *gate_out, double *y_out) {
+    (void)T;
+    layer(n_tok, tok, d, E, K, h, hs, 1, lambda, act_bf16, x, wr, bias, w13, w2, w13s, w2s, idx_out, gate_out,
+          y_out);
 }
 
 /* Loss-free balancing bias update (Sec. 3.2 "Load Balancing"): rule 0 is the

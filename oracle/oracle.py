@@ -67,6 +67,9 @@ def _load():
             "oracle_combine": ([I, I, I, P, P, P, D, P], None),
             "oracle_layer": ([I, P, I, I, I, I, I, I, F, I, P, P, P, P, P, P, P, P, P, P], None),
             "oracle_bias_update": ([I, P, P, F, I], None),
+            "oracle_silu": ([D], D),
+            "oracle_expert_rows_swiglu": ([I, I, I, P, P, P, I, P], None),
+            "oracle_layer_swiglu": ([I, P, I, I, I, I, I, I, F, I, P, P, P, P, P, P, P, P, P, P], None),
         }
         for name, (args, res) in sigs.items():
             fn = getattr(lib, name)
@@ -159,14 +162,24 @@ def permute(topk_idx, E: int):
     return counts, offsets, slots
 
 
-def expert_rows(rows, w1, w2, act_bf16: bool) -> np.ndarray:
-    """W2 act(W1 r) for each row r of rows [n, d]; w1 [h, d], w2 [d, h]. float64 [n, d]."""
+def silu(v) -> np.ndarray:
+    """SiLU v / (1 + exp(-v)) in double precision (elementwise)."""
+    f = _load().oracle_silu
+    return np.vectorize(lambda z: f(float(z)), otypes=[np.float64])(np.asarray(v, dtype=np.float64))
+
+
+def expert_rows(rows, w1, w2, act_bf16: bool, act: str = "gelu") -> np.ndarray:
+    """W2 act(W1 r) for each row r of rows [n, d]; w2 [d, h]. float64 [n, d].
+    act "gelu": w1 [h, d]; act "swiglu": w1 [2h, d] holds the gate rows then the
+    up rows and act(.) = SiLU(gate) * up."""
     rows, w1, w2 = _f32(rows), _f32(w1), _f32(w2)
     n, d = rows.shape
-    h = w1.shape[0]
-    assert w1.shape == (h, d) and w2.shape == (d, h)
+    h = w2.shape[1]
+    assert w1.shape == ((2 * h if act == "swiglu" else h), d) and w2.shape == (d, h)
     out = np.empty((n, d), dtype=np.float64)
-    _load().oracle_expert_rows(n, d, h, _ptr(rows), _ptr(w1), _ptr(w2), int(bool(act_bf16)), _ptr(out))
+    fn = _load().oracle_expert_rows_swiglu if act == "swiglu" else _load().oracle_expert_rows
+    assert act in ("gelu", "swiglu")
+    fn(n, d, h, _ptr(rows), _ptr(w1), _ptr(w2), int(bool(act_bf16)), _ptr(out))
     return out
 
 
@@ -183,22 +196,25 @@ def combine(expert_out, gate, shared, lam: float) -> np.ndarray:
     return y
 
 
-def layer(x, wr, bias, w1, w2, w1s, w2s, K: int, lam: float, act_bf16: bool, tokens=None):
+def layer(x, wr, bias, w1, w2, w1s, w2s, K: int, lam: float, act_bf16: bool, tokens=None, act: str = "gelu"):
     """The whole layer for the listed tokens (all tokens when None).
-    Returns (topk_idx [n, K], topk_gate [n, K], y [n, d] float64)."""
+    act "swiglu": w1 [E, 2h, d] and w1s [2h_s, d] hold the gate rows then the up
+    rows of each expert. Returns (topk_idx [n, K], topk_gate [n, K], y [n, d] float64)."""
+    assert act in ("gelu", "swiglu")
     x, wr, bias, w1, w2 = _f32(x), _f32(wr), _f32(bias), _f32(w1), _f32(w2)
     w1s, w2s = _f32(w1s), _f32(w2s)
     T, d = x.shape
-    E, h = w1.shape[0], w1.shape[1]
-    hs = 0 if w1s is None else w1s.shape[0]
+    E, h = w2.shape[0], w2.shape[2]
+    hs = 0 if w2s is None else w2s.shape[1]
     tok = None if tokens is None else np.ascontiguousarray(tokens, dtype=np.int32)
     n = T if tok is None else tok.size
     idx = np.empty((n, K), dtype=np.int32)
     gate = np.empty((n, K), dtype=np.float32)
     y = np.empty((n, d), dtype=np.float64)
-    _load().oracle_layer(n, _ptr(tok), T, d, E, K, h, hs, float(lam), int(bool(act_bf16)),
-                         _ptr(x), _ptr(wr), _ptr(bias), _ptr(w1), _ptr(w2), _ptr(w1s), _ptr(w2s),
-                         _ptr(idx), _ptr(gate), _ptr(y))
+    fn = _load().oracle_layer_swiglu if act == "swiglu" else _load().oracle_layer
+    fn(n, _ptr(tok), T, d, E, K, h, hs, float(lam), int(bool(act_bf16)),
+       _ptr(x), _ptr(wr), _ptr(bias), _ptr(w1), _ptr(w2), _ptr(w1s), _ptr(w2s),
+       _ptr(idx), _ptr(gate), _ptr(y))
     return idx, gate, y
 
 

@@ -48,6 +48,11 @@ MUTANTS = {
     "zscore_no_mean": ("double dev = (double)counts[e] - mu;", "double dev = (double)counts[e];"),
     "zscore_wrong_direction": ("bias[e] = (float)((double)bias[e] - step);",
                                "bias[e] = (float)((double)bias[e] + step);"),
+    "silu_wrong_sign": ("return v / (1.0 + exp(-v));", "return v / (1.0 + exp(v));"),
+    "swiglu_gate_up_swapped": ("a = oracle_silu(a) * up;", "a = oracle_silu(up) * a;"),
+    "swiglu_up_reads_gate_rows": ("const float *wu = w1 + ((size_t)h + k) * d;", "const float *wu = w1 + (size_t)k * d;"),
+    "swiglu_expert_stride": ("const size_t w1_rows = swiglu ? 2 * (size_t)h : (size_t)h;",
+                             "const size_t w1_rows = (size_t)h;"),
 }
 
 

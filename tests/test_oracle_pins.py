@@ -448,3 +448,79 @@ def test_bias_update_balanced_load_changes_nothing():
         assert np.array_equal(oracle.bias_update([7, 7, 7, 7], b, 0.5, rule), b)
         assert np.array_equal(oracle.bias_update([0, 0, 0, 0], b, 0.5, rule), b)
     assert np.array_equal(oracle.bias_update([9], [0.25], 1.0, oracle.BIAS_ZSCORE), np.float32([0.25]))
+
+
+# ---- SwiGLU experts (App. "MoE Kernel", Algorithm 1 Phase 2: SiLU(gate) * up)
+
+
+def test_silu_known_values_and_identities():
+    from scipy.special import expit
+
+    assert oracle.silu([0.0])[0] == 0.0
+    assert abs(oracle.silu([1.0])[0] - 0.7310585786300049) < 1e-15  # logistic(1) = e / (1 + e)
+    v = np.linspace(-30, 30, 601)
+    s = oracle.silu(v)
+    assert np.max(np.abs(s - v * expit(v))) < 1e-13 * np.maximum(1, np.abs(v)).max()
+    assert np.max(np.abs(oracle.silu(-v) - (s - v))) < 1e-12  # silu(-v) = silu(v) - v
+    eps = 1e-6
+    assert abs((oracle.silu([eps])[0] - oracle.silu([-eps])[0]) / (2 * eps) - 0.5) < 1e-9  # slope 1/2 at 0
+
+
+@pytest.mark.parametrize("act_bf16", [False, True])
+def test_swiglu_expert_closed_form(act_bf16):
+    from scipy.special import expit
+
+    rng = np.random.default_rng(15)
+    d = 32
+    x = rng.standard_normal((7, d)).astype(np.float32)
+    c = 0.625
+    w13 = np.concatenate([np.eye(d), c * np.eye(d)]).astype(np.float32)  # gate = I, up = c I
+    out = oracle.expert_rows(x, w13, np.eye(d, dtype=np.float32), act_bf16, act="swiglu")
+    xd = x.astype(np.float64)
+    a = xd * expit(xd) * (c * xd)
+    if act_bf16:
+        a = oracle.round_bf16(a)
+    assert np.max(np.abs(out - a)) < 1e-15
+
+
+@pytest.mark.parametrize("act_bf16", [False, True])
+def test_swiglu_expert_matches_float64_matmul(act_bf16):
+    from scipy.special import expit
+
+    rng = np.random.default_rng(16)
+    d, h = 40, 24  # non-square: a transposed operand cannot pass
+    x = rng.standard_normal((13, d)).astype(np.float32)
+    w13 = (rng.standard_normal((2 * h, d)) * 0.3).astype(np.float32)
+    w2 = (rng.standard_normal((d, h)) * 0.3).astype(np.float32)
+    out = oracle.expert_rows(x, w13, w2, act_bf16, act="swiglu")
+    xd = x.astype(np.float64)
+    g = xd @ w13[:h].astype(np.float64).T
+    u = xd @ w13[h:].astype(np.float64).T
+    hid = g * expit(g) * u
+    if act_bf16:
+        hid = bf16_round64(hid)
+    ref = hid @ w2.astype(np.float64).T
+    tol = 1e-12 if not act_bf16 else 1e-2
+    assert np.max(np.abs(out - ref)) < tol
+    if act_bf16:
+        assert np.mean(np.abs(out - ref) < 1e-12) > 0.95
+
+
+def test_swiglu_layer_identical_experts_and_shared():
+    rng = np.random.default_rng(17)
+    x, wr, b, w1, w2, w1s, w2s = _tiny_layer(32, K=3)
+    E, h, d = w1.shape
+    hs = w1s.shape[0]
+    w13 = (rng.standard_normal((E, 2 * h, d)) * 0.2).astype(np.float32)
+    w13[:] = w13[0]
+    w2[:] = w2[0]
+    w13s = (rng.standard_normal((2 * hs, d)) * 0.2).astype(np.float32)
+    idx, _, y = oracle.layer(x, wr, b, w13, w2, w13s, w2s, 3, 0.5, False, act="swiglu")
+    ref = oracle.expert_rows(x, w13[0], w2[0], False, act="swiglu") + \
+        0.5 * oracle.expert_rows(x, w13s, w2s, False, act="swiglu")
+    assert np.max(np.abs(y - ref)) < 1e-6  # gates sum to 1 up to fp32 rounding
+    gi, _, _ = oracle.layer(x, wr, b, w1, w2, w1s, w2s, 3, 0.5, False)
+    assert np.array_equal(idx, gi)  # routing does not depend on the expert type
+    w2[:] = 0
+    _, _, y0 = oracle.layer(x, wr, b, w13, w2, w13s, w2s, 3, 1.0, False, act="swiglu")
+    assert np.max(np.abs(y0 - oracle.expert_rows(x, w13s, w2s, False, act="swiglu"))) < 1e-12
