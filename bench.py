@@ -7,8 +7,9 @@ One step is one moe_layer_forward (route, permute, grouped routed experts,
 shared expert, combine) over a seeded synthetic batch already resident in
 HBM. Prints ONE JSON line: whole-layer tokens/s over the K timed steps, the
 roofline of the dominant kernel pair (the routed grouped GEMM, fc1 + fc2),
-per-stage times, the single-image (weight-read bound) layer, and the CPU
-oracle timed on a bounded sample of the same workload.
+per-stage times, the single-image (weight-read bound) layer, the SwiGLU-expert
+layers (the paper's H layer and the single-image shape), and the CPU oracle
+timed on a bounded sample of the same workload.
 """
 
 from __future__ import annotations
@@ -65,6 +66,8 @@ def parse():
     p.add_argument("--config", default="vitg_skew_bf16")
     p.add_argument("--single-image-config", default="single_image_bf16")
     p.add_argument("--no-single-image", action="store_true")
+    p.add_argument("--swiglu-configs", default="vith_swiglu_bf16,single_image_swiglu_bf16",
+                   help="SwiGLU-expert layers measured beside the main workload (comma-separated, '' for none)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=15.0,
                    help="target CPU time of the oracle sample")
@@ -90,7 +93,7 @@ def main():
     import torch
 
     from paper_2608_17402_amd import binding
-    from workloads import get_config, make_inputs
+    from workloads import get_config, make_inputs, pad_last_dim
 
     torch.cuda.set_device(0)
     binding.load()
@@ -109,10 +112,15 @@ def main():
             t0 = time.perf_counter()
             inp = make_inputs(cfg)
             self.inp = inp
-            self.desc = binding.make_desc(cfg.T, cfg.d, cfg.E, cfg.K, cfg.h, cfg.h_shared, cfg.lam, cfg.dtype)
+            swiglu = cfg.act == "swiglu"
+            flags = binding.MOE_FLAG_SWIGLU if swiglu else 0
+            self.desc = binding.make_desc(cfg.T, cfg.d, cfg.E, cfg.K, cfg.h, cfg.h_shared, cfg.lam, cfg.dtype,
+                                          flags=flags)
             self.dt = binding.torch_dtype(self.desc)
             self.x, self.wr, self.b = dev(inp.x), dev(inp.w_router), dev(inp.bias)
-            self.w1, self.w2, self.w1s, self.w2s = dev(inp.w1), dev(inp.w2), dev(inp.w1s), dev(inp.w2s)
+            # SwiGLU: stacked gate/up rows as drawn; second layer with rows padded to 64 columns.
+            pad = pad_last_dim if swiglu else (lambda a: a)
+            self.w1, self.w2, self.w1s, self.w2s = dev(inp.w1), dev(pad(inp.w2)), dev(inp.w1s), dev(pad(inp.w2s))
             self.ws = binding.alloc_workspace(self.desc)
             T, K, E, d = cfg.T, cfg.K, cfg.E, cfg.d
             self.y = torch.empty(T, d, dtype=self.dt, device="cuda")
@@ -206,7 +214,7 @@ def main():
     # Per-stage times (the stage entry points run the same kernels).
     stages_ms = {k: time_calls(f, args.stage_reps) for k, f in lay.stages().items()}
     gemm_ms = fc1_ms + fc2_ms
-    routed_flops = 4.0 * cfg.T * cfg.K * cfg.d * cfg.h
+    routed_flops = 2.0 * cfg.n_mats * cfg.T * cfg.K * cfg.d * cfg.h
     achieved = routed_flops / (gemm_ms * 1e-3) / 1e12
     roofline = {
         "kernel": "routed grouped GEMM: the fc1+GELU and fc2 kernels of one layer step",
@@ -233,38 +241,73 @@ def main():
         "timed_wall_s": round(wall, 3),
     }
 
-    if not args.no_single_image:
-        c5 = get_config(args.single_image_config)
-        si = Layer(c5)
+    def measure(c, reps):
+        """Whole-layer time and the routed grouped GEMM pair (HIP events that
+        moe_layer_forward records around fc1 and fc2) of layer config c."""
+        L = Layer(c)
         for _ in range(3):
-            si.forward()
-        reps = max(args.steps, 20)
-        hev = binding.HipEvents(3 * reps)
+            L.forward()
+        ev = binding.HipEvents(3 * reps)
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         for i in range(reps):
-            si.forward(hev.handles[3 * i:3 * i + 3])
+            L.forward(ev.handles[3 * i:3 * i + 3])
         e1.record(stream)
         torch.cuda.synchronize()
-        si_ms = e0.elapsed_time(e1) / reps
-        si_gemm_ms = sum(hev.elapsed_ms(3 * i, 3 * i + 2) for i in range(reps)) / reps
-        hev.close()
-        si_stages = {k: time_calls(f, max(args.stage_reps, 20)) for k, f in si.stages().items()}
-        w_bytes = c5.routed_weight_bytes()
-        gbs = w_bytes / (si_gemm_ms * 1e-3) / 1e9
-        out["single_image"] = {
-            "workload": c5.name, "tokens": c5.T, "us_per_layer": round(si_ms * 1e3, 1),
-            "tokens_per_s": round(c5.T / (si_ms * 1e-3), 1),
+        l_ms = e0.elapsed_time(e1) / reps
+        f1 = sum(ev.elapsed_ms(3 * i, 3 * i + 1) for i in range(reps)) / reps
+        f2 = sum(ev.elapsed_ms(3 * i + 1, 3 * i + 2) for i in range(reps)) / reps
+        ev.close()
+        return L, l_ms, f1, f2
+
+    def hbm_line(c, L, l_ms, g_ms):
+        w_bytes = c.routed_weight_bytes()
+        gbs = w_bytes / (g_ms * 1e-3) / 1e9
+        return {
+            "workload": c.name, "tokens": c.T, "act": c.act, "us_per_layer": round(l_ms * 1e3, 1),
+            "tokens_per_s": round(c.T / (l_ms * 1e-3), 1),
             "roofline": {"kernel": "routed grouped GEMM (fc1+fc2), expert weights read once", "bound": "hbm",
                          "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                         "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": traffic_bytes(c5.name),
+                         "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": traffic_bytes(c.name),
                          "algorithmic_bytes_per_launch": w_bytes,
-                         "avg_launch_us": round(si_gemm_ms * 1e3, 2)},
-            "layer_weight_gbs": round((w_bytes + c5.shared_weight_bytes()) / (si_ms * 1e-3) / 1e9, 1),
-            "stages_us": {k: round(v * 1e3, 1) for k, v in si_stages.items()},
+                         "avg_launch_us": round(g_ms * 1e3, 2)},
+            "layer_weight_gbs": round((w_bytes + c.shared_weight_bytes()) / (l_ms * 1e-3) / 1e9, 1),
         }
+
+    def mfma_line(c, l_ms, f1, f2):
+        fl = 2.0 * c.n_mats * c.T * c.K * c.d * c.h
+        tf = fl / ((f1 + f2) * 1e-3) / 1e12
+        return {
+            "workload": c.name, "tokens": c.T, "act": c.act, "us_per_layer": round(l_ms * 1e3, 1),
+            "tokens_per_s": round(c.T / (l_ms * 1e-3), 1),
+            "layer_gemm_tflops": round(c.gemm_flops() / (l_ms * 1e-3) / 1e12, 2),
+            "roofline": {"kernel": "routed grouped GEMM (fc1 with its activation, fc2)", "bound": "mfma",
+                         "achieved": round(tf, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                         "frac": round(tf / PEAK_BF16_TFLOPS, 4), "traffic": traffic_bytes(c.name),
+                         "algorithmic_flops_per_launch": fl, "avg_launch_us": round((f1 + f2) * 1e3, 2),
+                         "fc1_us": round(f1 * 1e3, 2), "fc2_us": round(f2 * 1e3, 2)},
+        }
+
+    if not args.no_single_image:
+        c5 = get_config(args.single_image_config)
+        reps = max(args.steps, 20)
+        si, si_ms, f1, f2 = measure(c5, reps)
+        si_stages = {k: time_calls(f, max(args.stage_reps, 20)) for k, f in si.stages().items()}
+        out["single_image"] = hbm_line(c5, si, si_ms, f1 + f2)
+        out["single_image"]["stages_us"] = {k: round(v * 1e3, 1) for k, v in si_stages.items()}
         del si
+
+    sw_names = [n for n in args.swiglu_configs.split(",") if n]
+    if sw_names:
+        out["swiglu"] = {}
+        for name in sw_names:
+            c = get_config(name)
+            L, l_ms, f1, f2 = measure(c, max(args.steps, 20))
+            # ~32 rows per expert is weight-read bound; large batches are MFMA bound.
+            weight_bound = c.T * c.K / c.E < 256
+            out["swiglu"][name] = hbm_line(c, L, l_ms, f1 + f2) if weight_bound else mfma_line(c, l_ms, f1, f2)
+            del L
 
     if not args.no_cpu_baseline:
         import oracle

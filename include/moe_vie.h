@@ -9,6 +9,10 @@
  *   g'_e   = Sigmoid(s_e) / sum_{i in sel} Sigmoid(s_i)     for e in sel
  *   y      = sum_{e in sel} g'_e E_e(x) + lambda * E_shared(x)
  *   E(x)   = W2 GELU(W1 x)                           fc1 -> exact-erf GELU -> fc2
+ * or, with MOE_FLAG_SWIGLU, SwiGLU experts (appendix "MoE Kernel",
+ * Algorithm 1, Phase 2, and the SwiGLU MLPs of appendix "Implementation
+ * Details"):
+ *   E(x)   = W2 (SiLU(W1 x) * (W3 x)),  SiLU(v) = v / (1 + exp(-v))
  * The five stages (route, permute, grouped expert MLP, combine) are exposed
  * separately and fused in moe_layer_forward.
  *
@@ -21,12 +25,20 @@
  *    round-to-nearest-even). Biases and gates are fp32, indices int32.
  *  - Weights use the nn.Linear layout [out, in]: W_r [E, d], W1 [E, h, d],
  *    W2 [E, d, h], shared W1s [h_s, d], W2s [d, h_s].
+ *  - SwiGLU experts (MOE_FLAG_SWIGLU) pass the gate and up projections
+ *    stacked, "w13" [E, 2h, d]: rows 0..h-1 are W1 (gate), rows h..2h-1 are
+ *    W3 (up); the shared expert likewise [2 h_s, d]. The second layer is
+ *    stored with its rows padded to ldh = h rounded up to a multiple of 64:
+ *    W2 [E, d, ldh] and W2s [d, ldh_s]; columns h..ldh-1 may hold any finite
+ *    values (they multiply activation columns that are exactly zero). h and
+ *    h_s may then be any value in [1, 8192].
  *  - A "slot" is one (token, choice) pair, slot id n = t*K + j, j < K.
  *  - Every call is asynchronous on `stream` (a hipStream_t; NULL is the
  *    default stream) and never synchronises with the host.
  *  - Arguments are validated on the host before anything is enqueued; a call
  *    that returns an error has enqueued nothing. Inputs must be finite.
- *  - Pointers must be 16-byte aligned; d, h and h_s must be multiples of 64.
+ *  - Pointers must be 16-byte aligned; d must be a multiple of 64, and so
+ *    must h and h_s for GELU experts.
  *  - Calls on one stream are ordered; calls that share output or workspace
  *    buffers must not overlap on different streams.
  */
@@ -54,11 +66,13 @@ typedef enum { MOE_F32 = 0, MOE_BF16 = 1 } moe_dtype_t;
 #define MOE_FLAG_EXACT_ROUTER 1 /* compute every router logit by the exact chain
                                    (no MFMA pre-pass); the routing result is the
                                    same bit for bit, only the work differs */
+#define MOE_FLAG_SWIGLU 2       /* SwiGLU experts (bf16 layers only): see below */
 
 /* Layer descriptor. Limits: 1 <= T, T*K < 2^31; 1 <= K <= 16; K <= E <= 1024;
- * 64 <= d <= 8192, 64 <= h <= 8192, 0 <= h_shared <= 8192 (0 = no shared
- * expert), all multiples of 64; T*d, T*K*h and T*h_shared elements below
- * 4 GiB; flags a combination of MOE_FLAG_* bits. */
+ * 64 <= d <= 8192 a multiple of 64; h and h_shared (0 = no shared expert)
+ * at most 8192 and, for GELU experts, multiples of 64 and >= 64; T*d,
+ * T*K*ldh and T*ldh_s elements below 4 GiB (ldh = h for GELU experts); flags
+ * a combination of MOE_FLAG_* bits (MOE_FLAG_SWIGLU needs dtype MOE_BF16). */
 typedef struct {
     int32_t T;        /* tokens                                   */
     int32_t d;        /* model width                              */
@@ -119,11 +133,14 @@ moe_status_t moe_permute(const moe_desc_t *desc, const int32_t *topk_idx, int32_
  * fc2 experts and no routing weight applied).
  *   x            [T, d] layer dtype: token rows, gathered via slot / K
  *   sorted_slots [T*K], offsets [E+1]: as produced by moe_permute
- *   w1 [E, h, d], w2 [E, d, h] layer dtype
+ *   w1 [E, h, d], w2 [E, d, h] layer dtype (SwiGLU: w1 = w13 [E, 2h, d],
+ *                w2 [E, d, ldh], see the conventions above)
  *   expert_out   [T*K, d] layer dtype out, row n = W2[e] GELU(W1[e] x_t) for
- *                slot n = t*K + j routed to expert e
- * For bf16 the activation GELU(W1 x) is rounded to bf16 before fc2;
- * accumulation is fp32. The shared expert can be run through this call with
+ *                slot n = t*K + j routed to expert e (SwiGLU:
+ *                W2[e] (SiLU(W1[e] x_t) * (W3[e] x_t)))
+ * For bf16 the activation (GELU(W1 x), or SiLU(W1 x) * W3 x with both
+ * projections accumulated in fp32 in the same kernel) is rounded to bf16
+ * before fc2; accumulation is fp32. The shared expert can be run through this call with
  * a descriptor {E = 1, K = 1, h = h_s}, sorted_slots = 0..T-1, offsets =
  * {0, T}. Uses the workspace. */
 moe_status_t moe_grouped_mlp(const moe_desc_t *desc, const void *x, const int32_t *sorted_slots,
@@ -144,7 +161,8 @@ moe_status_t moe_combine(const moe_desc_t *desc, const void *expert_out, const f
  * routed experts, shared expert (if desc->h_shared > 0) and combine, enqueued
  * back to back on `stream` with no host synchronisation.
  *   x [T, d], w_router [E, d], bias [E] fp32 or NULL, w1 [E, h, d],
- *   w2 [E, d, h], w1s [h_s, d] and w2s [d, h_s] (ignored when h_s == 0)
+ *   w2 [E, d, h], w1s [h_s, d] and w2s [d, h_s] (ignored when h_s == 0);
+ *   SwiGLU: w1 [E, 2h, d], w2 [E, d, ldh], w1s [2 h_s, d], w2s [d, ldh_s]
  *   y [T, d] layer dtype out
  *   topk_idx_out [T, K] int32 and topk_gate_out [T, K] fp32: optional
  *   copies of the routing (NULL = not returned)

@@ -21,6 +21,7 @@ LIB_PATH = os.path.join(_PKG, "libmoevie.so")
 MOE_F32 = 0
 MOE_BF16 = 1
 MOE_FLAG_EXACT_ROUTER = 1
+MOE_FLAG_SWIGLU = 2
 STATUS = {0: "MOE_OK", 1: "MOE_ERR_INVALID_ARG", 2: "MOE_ERR_UNSUPPORTED", 3: "MOE_ERR_WORKSPACE",
           4: "MOE_ERR_HIP"}
 

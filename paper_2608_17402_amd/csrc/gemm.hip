@@ -98,6 +98,20 @@ __device__ __forceinline__ float gelu_as(float x) {
     return fmaf(-ax, q * e, fmaxf(x, 0.0f));
 }
 
+// SiLU(v) = v / (1 + exp(-v)) from the hardware exp2 and reciprocal; for
+// very negative v, exp2 overflows to +inf and the reciprocal to 0, the limit.
+__device__ __forceinline__ float silu_as(float v) {
+    return v * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(v * -1.44269504f));
+}
+
+// SwiGLU activation of one column: SiLU(gate) * up, or 0 past the valid width.
+__device__ __forceinline__ float swiglu_col(float g, float u, bool valid) {
+    return valid ? silu_as(g) * u : 0.0f;
+}
+
+// Epilogues of a first expert layer: their token rows are gathered from x.
+__host__ __device__ constexpr bool fc1_epi(int epi) { return epi == EPI_GELU_STORE || epi == EPI_SWIGLU_STORE; }
+
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
@@ -217,16 +231,21 @@ void k_gemm_bf16(const GemmArgs a) {
         const int rr = r < tc.rows ? r : tc.rows - 1;  // pad rows repeat the last valid row
         const int p = tc.row0 + rr;
         int v = p;
-        if (EPI == EPI_GELU_STORE && a.row_mode == ROWS_GATHER_TOKENS) v = a.row_map[p] / a.route_k;
+        if (fc1_epi(EPI) && a.row_mode == ROWS_GATHER_TOKENS) v = a.row_map[p] / a.route_k;
         if (EPI == EPI_SCATTER_SLOT) v = a.row_map[p];
         srow[r] = v;
     }
     __syncthreads();
 
+    constexpr bool SWIGLU = EPI == EPI_SWIGLU_STORE;
+    constexpr int HW = WTN / 2;  // SwiGLU: activation columns per wave
+    static_assert(!SWIGLU || FN % 2 == 0, "SwiGLU waves hold gate and up blocks in pairs");
     const int Kd = a.Kdim;
     const __amdgpu_buffer_rsrc_t xres = make_rsrc(a.A, a.a_bytes);
+    // SwiGLU: the group's 2 act_n weight rows; reads past them return zeros.
     const __amdgpu_buffer_rsrc_t wres =
-        make_rsrc(static_cast<const bf16_t*>(a.B) + (size_t)tc.e * a.b_group_stride, (uint32_t)a.N * Kd * 2);
+        make_rsrc(static_cast<const bf16_t*>(a.B) + (size_t)tc.e * a.b_group_stride,
+                  (uint32_t)(SWIGLU ? 2 * a.act_n : a.N) * Kd * 2);
 
     constexpr int SWZ_SHIFT = CPR == 8 ? 1 : 2;
     constexpr int SWZ_MASK = CPR - 1;
@@ -238,7 +257,7 @@ void k_gemm_bf16(const GemmArgs a) {
         const int r = sl / CPR, pch = sl % CPR;
         const int c = pch ^ ((r >> SWZ_SHIFT) & SWZ_MASK);
         int xrow;
-        if (EPI == EPI_GELU_STORE) xrow = srow[r];
+        if (fc1_epi(EPI)) xrow = srow[r];
         else xrow = tc.row0 + (r < tc.rows ? r : tc.rows - 1);
         xv[i] = (uint32_t)xrow * (uint32_t)(Kd * 2) + c * 16;
     }
@@ -248,7 +267,16 @@ void k_gemm_bf16(const GemmArgs a) {
         const int sl = (wave + NW * i) * kWave + lane;
         const int r = sl / CPR, pch = sl % CPR;
         const int c = pch ^ ((r >> SWZ_SHIFT) & SWZ_MASK);
-        wv[i] = (uint32_t)(tc.n0 + r) * (uint32_t)(Kd * 2) + c * 16;
+        // SwiGLU: tile column r is wave block r / WTN; its first HW columns
+        // are the gate rows and the last HW the up rows of the same HW
+        // activation columns. Gate rows past act_n read (finite) up rows,
+        // whose activations the epilogue zeroes.
+        int wrow = tc.n0 + r;
+        if (SWIGLU) {
+            const int w = r % WTN;
+            wrow = tc.n0 / 2 + (r / WTN) * HW + w % HW + (w >= HW ? a.act_n : 0);
+        }
+        wv[i] = (uint32_t)wrow * (uint32_t)(Kd * 2) + c * 16;
     }
 
     f32x16_t acc[FN][FM];
@@ -348,7 +376,7 @@ void k_gemm_bf16(const GemmArgs a) {
     // 16-byte row pieces so that consecutive lanes store whole 128-byte lines.
     constexpr bool OUT_F32 = EPI == EPI_STORE_F32;
     constexpr int OES = OUT_F32 ? 4 : 2;           // output element size
-    constexpr int SEG = WTN * OES;                 // bytes of one wave-tile row
+    constexpr int SEG = (SWIGLU ? HW : WTN) * OES; // bytes of one wave-tile row
     constexpr int RSTR = SEG + 16;                 // padded LDS row stride
     constexpr int CPRO = SEG / 16;                 // 16-byte pieces per row
     constexpr int PIECES = 32 * CPRO / kWave;      // pieces per lane per block
@@ -356,24 +384,43 @@ void k_gemm_bf16(const GemmArgs a) {
     static_assert((32 * CPRO) % kWave == 0, "row pieces must split evenly over the wave");
     __syncthreads();  // every wave is done with the stage buffers
     uint8_t* stg = smem + wave * 32 * RSTR;
+    // First output column of this wave's rows (SwiGLU: activation column,
+    // rows act_ld apart).
+    const int ocol0 = SWIGLU ? tc.n0 / 2 + wn * HW : tc.n0 + wn * WTN;
+    const size_t ostride = SWIGLU ? (size_t)a.act_ld : (size_t)a.N;
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
+        if constexpr (SWIGLU) {
 #pragma unroll
-        for (int j = 0; j < FN; ++j)
+            for (int j = 0; j < FN / 2; ++j)
 #pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                float v0 = acc[j][i][4 * g + 0], v1 = acc[j][i][4 * g + 1];
-                float v2 = acc[j][i][4 * g + 2], v3 = acc[j][i][4 * g + 3];
-                uint8_t* dst = stg + fr * RSTR + (j * 32 + 8 * g + 4 * fk) * OES;
-                if (OUT_F32) {
-                    *reinterpret_cast<float4*>(dst) = make_float4(v0, v1, v2, v3);
-                } else {
-                    if (EPI == EPI_GELU_STORE) {
-                        v0 = gelu_as(v0); v1 = gelu_as(v1); v2 = gelu_as(v2); v3 = gelu_as(v3);
-                    }
-                    *reinterpret_cast<uint2*>(dst) = pack4_bf16(v0, v1, v2, v3);
+                for (int g = 0; g < 4; ++g) {
+                    const int c = j * 32 + 8 * g + 4 * fk;
+                    float v[4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        v[q] = swiglu_col(acc[j][i][4 * g + q], acc[j + FN / 2][i][4 * g + q],
+                                          ocol0 + c + q < a.act_n);
+                    *reinterpret_cast<uint2*>(stg + fr * RSTR + c * 2) = pack4_bf16(v[0], v[1], v[2], v[3]);
                 }
-            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    float v0 = acc[j][i][4 * g + 0], v1 = acc[j][i][4 * g + 1];
+                    float v2 = acc[j][i][4 * g + 2], v3 = acc[j][i][4 * g + 3];
+                    uint8_t* dst = stg + fr * RSTR + (j * 32 + 8 * g + 4 * fk) * OES;
+                    if (OUT_F32) {
+                        *reinterpret_cast<float4*>(dst) = make_float4(v0, v1, v2, v3);
+                    } else {
+                        if (EPI == EPI_GELU_STORE) {
+                            v0 = gelu_as(v0); v1 = gelu_as(v1); v2 = gelu_as(v2); v3 = gelu_as(v3);
+                        }
+                        *reinterpret_cast<uint2*>(dst) = pack4_bf16(v0, v1, v2, v3);
+                    }
+                }
+        }
         // Each wave reads back only its own area: a wave-level sync suffices.
         wave_sync_lds();
 #pragma unroll
@@ -382,9 +429,9 @@ void k_gemm_bf16(const GemmArgs a) {
             const int rr = q / CPRO, pc = q % CPRO;
             const int r = wm * WTM + i * 32 + rr;
             const uint4 v = *reinterpret_cast<const uint4*>(stg + rr * RSTR + pc * 16);
-            if (r < tc.rows) {
+            if (r < tc.rows && (!SWIGLU || ocol0 < a.act_ld)) {
                 const size_t orow = EPI == EPI_SCATTER_SLOT ? (size_t)srow[r] : (size_t)(tc.row0 + r);
-                uint8_t* out = static_cast<uint8_t*>(a.C) + (orow * a.N + tc.n0 + wn * WTN) * OES + pc * 16;
+                uint8_t* out = static_cast<uint8_t*>(a.C) + (orow * ostride + ocol0) * OES + pc * 16;
                 *reinterpret_cast<uint4*>(out) = v;
             }
         }
@@ -710,7 +757,8 @@ void k_gemm_pp(const GemmArgs a) {
     constexpr int AP = BM * CPR / kWave / NW;  // 8 token copy pieces per wave and slab
     constexpr int BP = BN * CPR / kWave / NW;  // 8 weight copy pieces
     static_assert(AP == 8 && BP == 8, "copy schedule is written for 8 + 8 pieces");
-    constexpr bool GATHER = GROUPED && EPI == EPI_GELU_STORE;
+    constexpr bool GATHER = GROUPED && fc1_epi(EPI);
+    constexpr bool SWIGLU = EPI == EPI_SWIGLU_STORE;
     constexpr bool SCATTER = EPI == EPI_SCATTER_SLOT;
     constexpr bool OUT_F32 = EPI == EPI_STORE_F32;
     constexpr bool COMBINE = EPI == EPI_COMBINE;
@@ -771,7 +819,13 @@ void k_gemm_pp(const GemmArgs a) {
     auto tile_at = [&](int l) { return tile_of(l, tile_entry(l)); };
     const bf16_t* const Bw = static_cast<const bf16_t*>(a.B);
     const bf16_t* const Ax = static_cast<const bf16_t*>(a.A);
+    // SwiGLU: a tile of BN columns computes activation columns [n0 / 2,
+    // n0 / 2 + 128); the resource starts at gate row n0 / 2 and ends with the
+    // group's last up row, so rows past it read as zeros.
     auto wres_of = [&](const Tile& t) {
+        if (SWIGLU)
+            return make_rsrc(Bw + (size_t)t.e * a.b_group_stride + (size_t)(t.n0 / 2) * Kd,
+                             (uint32_t)(2 * a.act_n - t.n0 / 2) * rowbytes);
         return make_rsrc(Bw + (size_t)t.e * a.b_group_stride + (size_t)t.n0 * Kd, (uint32_t)BN * rowbytes);
     };
     auto xres_of = [&](const Tile& t) {
@@ -789,12 +843,20 @@ void k_gemm_pp(const GemmArgs a) {
         r = sl / CPR;
         c = (sl % CPR) ^ ((r >> 1) & 7);
     };
-    uint32_t wv[BP];
+    // SwiGLU: wave column block wn (tile columns [128 wn, 128 wn + 128)) holds
+    // the gate rows of activation columns [64 wn, 64 wn + 64) of the tile,
+    // then their up rows (act_n rows further on). Gate rows past act_n read
+    // (finite) up rows, whose activations the epilogue zeroes.
+    // Token offsets without gathering (tv) are the plain row layout; for
+    // every epilogue but SwiGLU they equal the weight offsets.
+    uint32_t wv[BP], tv[AP];
 #pragma unroll
     for (int i = 0; i < BP; ++i) {
         int r, c;
         piece_rc(i, r, c);
-        wv[i] = (uint32_t)r * rowbytes + c * 16;
+        const int wrow = SWIGLU ? (r / WT) * (WT / 2) + r % (WT / 2) + ((r % WT) >= WT / 2 ? a.act_n : 0) : r;
+        wv[i] = (uint32_t)wrow * rowbytes + c * 16;
+        tv[i] = (uint32_t)r * rowbytes + c * 16;
     }
     // Gathered token rows: slot -> token, rows past the tile's end repeat its last row.
     auto load_tokens = [&](const Tile& t, int32_t (&tok)[AP]) {
@@ -1012,6 +1074,23 @@ void k_gemm_pp(const GemmArgs a) {
                             const int chunk = 8 * jj + 2 * g + fk;
                             lds_write16_asm(wrow + ((uint32_t)(chunk ^ sw) << 4), v);
                         }
+                } else if (SWIGLU) {
+                    // Blocks j < 2 are gate columns, j + 2 the up columns of
+                    // the same activation columns: 64 per wave row.
+#pragma unroll
+                    for (int j = 0; j < FB / 2; ++j)
+#pragma unroll
+                        for (int g = 0; g < 4; ++g) {
+                            const int c = t.n0 / 2 + wn * (WT / 2) + j * 32 + 8 * g + 4 * fk;
+                            float v[4];
+#pragma unroll
+                            for (int q = 0; q < 4; ++q)
+                                v[q] = swiglu_col(acc_read(acc[j][i][4 * g + q]),
+                                                  acc_read(acc[j + FB / 2][i][4 * g + q]), c + q < a.act_n);
+                            const uint2 pk = pack4_bf16(v[0], v[1], v[2], v[3]);
+                            lds_write8_asm(wrow + ((uint32_t)((4 * j + g) ^ sw) << 4) + (uint32_t)fk * 8u,
+                                           (u32x2_t){pk.x, pk.y});
+                        }
                 } else {
 #pragma unroll
                     for (int j = 0; j < FB; ++j)
@@ -1030,6 +1109,26 @@ void k_gemm_pp(const GemmArgs a) {
                 }
                 if constexpr (COMBINE) {
                     combine_block(t, stg, i, h);
+                    continue;
+                }
+                if constexpr (SWIGLU) {
+                    // 128-byte activation rows: 8 lanes per row, 8 rows per read.
+                    const int ocol = t.n0 / 2 + wn * (WT / 2);
+                    u32x4_t v[4];
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        const int rr = (lane >> 3) + 8 * k;
+                        v[k] = lds_read16u_asm(stg + (uint32_t)rr * 256u + ((uint32_t)((lane & 7) ^ (rr & 15)) << 4));
+                    }
+                    wait_lgkmcnt0();
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) tie(v[k]);
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        const int r = wm * WT + i * 32 + (lane >> 3) + 8 * k;
+                        if (r < t.rows && ocol < a.act_ld)
+                            store16_asm(cbase + ((size_t)(t.row0 + r) * a.act_ld + ocol) * 2 + (lane & 7) * 16, v[k]);
+                    }
                     continue;
                 }
                 u32x4_t v[8];
@@ -1058,9 +1157,9 @@ void k_gemm_pp(const GemmArgs a) {
 
     // Prologue: token slab 0, weight slab 0, token slab 1, the first half of
     // weight slab 1; wait for slab 0 of both operands; read its first fragments.
-    static_for<AP>([&](auto LC) { copy_a(LC, 0, 0u, xres_c, GATHER ? xv_c : wv); });
+    static_for<AP>([&](auto LC) { copy_a(LC, 0, 0u, xres_c, GATHER ? xv_c : tv); });
     static_for<BP>([&](auto LC) { copy_w(LC, 0, 0u, wres_c); });
-    static_for<AP>([&](auto LC) { copy_a(LC, 1, (uint32_t)BK * 2, xres_c, GATHER ? xv_c : wv); });
+    static_for<AP>([&](auto LC) { copy_a(LC, 1, (uint32_t)BK * 2, xres_c, GATHER ? xv_c : tv); });
     static_for<BP / 2>([&](auto LC) { copy_w(LC, 1, (uint32_t)BK * 2, wres_c); });
     wait_vmcnt<AP + BP / 2>();
     barrier_no_fence();
@@ -1082,7 +1181,7 @@ void k_gemm_pp(const GemmArgs a) {
             const __amdgpu_buffer_rsrc_t wr2 = n2 ? wres_n : wres_c;
             uint32_t xv2[AP];
 #pragma unroll
-            for (int i = 0; i < AP; ++i) xv2[i] = GATHER ? (n2 ? xv_n[i] : xv_c[i]) : wv[i];
+            for (int i = 0; i < AP; ++i) xv2[i] = GATHER ? (n2 ? xv_n[i] : xv_c[i]) : tv[i];
             // K step 0: second half of weight slab kt + 1.
             settle(std::integral_constant<int, 0>{});
             kstep(std::integral_constant<int, 0>{}, abase, wbase, 1, [&](auto CC) {
@@ -1311,11 +1410,29 @@ hipError_t dispatch_bf16(int bm, const GemmArgs& a, hipStream_t s) {
     return hipErrorInvalidValue;
 }
 
+// SwiGLU first layer: the virtual column count N follows from the tile shape
+// (each tile of BN columns computes BN / 2 activation columns).
+template <bool GROUPED>
+hipError_t dispatch_swiglu(int bm, GemmArgs a, hipStream_t s) {
+    if (a.act_n < 1 || a.act_ld < a.act_n || a.act_ld % 64) return hipErrorInvalidValue;
+    if (bm == 256) {
+        if (a.Kdim < 128 || (GROUPED && a.row_mode != ROWS_GATHER_TOKENS)) return hipErrorInvalidValue;
+        a.N = 2 * ((a.act_ld + 127) / 128 * 128);
+        return launch_pp<EPI_SWIGLU_STORE, GROUPED>(a, s);
+    }
+    if (bm == 64) {
+        a.N = 2 * a.act_ld;
+        return launch_bf16<64, 128, 2, 2, 64, 3, 2, EPI_SWIGLU_STORE, GROUPED>(a, s);
+    }
+    return hipErrorInvalidValue;
+}
+
 template <bool GROUPED>
 hipError_t dispatch(const moe_desc_t& d, int epilogue, int bm, const GemmArgs& a, hipStream_t s) {
     if (d.dtype == MOE_BF16) {
         switch (epilogue) {
             case EPI_GELU_STORE: return dispatch_bf16<EPI_GELU_STORE, GROUPED>(bm, a, s);
+            case EPI_SWIGLU_STORE: return dispatch_swiglu<GROUPED>(bm, a, s);
             case EPI_SCATTER_SLOT:
                 if (GROUPED) return dispatch_bf16<EPI_SCATTER_SLOT, true>(bm, a, s);
                 break;

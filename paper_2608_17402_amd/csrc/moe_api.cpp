@@ -42,24 +42,29 @@ moe_status_t check_desc(const moe_desc_t* d) {
     if (!d) return fail(MOE_ERR_INVALID_ARG, "desc is NULL");
     if (d->dtype != MOE_F32 && d->dtype != MOE_BF16)
         return fail(MOE_ERR_UNSUPPORTED, "dtype %d is not MOE_F32 or MOE_BF16", d->dtype);
-    if (d->flags & ~MOE_FLAG_EXACT_ROUTER) return fail(MOE_ERR_INVALID_ARG, "unknown flags 0x%x", d->flags);
+    if (d->flags & ~(MOE_FLAG_EXACT_ROUTER | MOE_FLAG_SWIGLU))
+        return fail(MOE_ERR_INVALID_ARG, "unknown flags 0x%x", d->flags);
+    const bool swiglu = d->flags & MOE_FLAG_SWIGLU;
+    if (swiglu && d->dtype != MOE_BF16) return fail(MOE_ERR_UNSUPPORTED, "SwiGLU experts need a bf16 layer");
     if (d->T < 1) return fail(MOE_ERR_INVALID_ARG, "T = %d must be >= 1", d->T);
     if (d->K < 1 || d->K > kMaxK) return fail(MOE_ERR_INVALID_ARG, "K = %d must be in [1, %d]", d->K, kMaxK);
     if (d->E < d->K || d->E > kMaxE)
         return fail(MOE_ERR_INVALID_ARG, "E = %d must be in [K = %d, %d]", d->E, d->K, kMaxE);
     if ((int64_t)d->T * d->K >= ((int64_t)1 << 31))
         return fail(MOE_ERR_INVALID_ARG, "T*K = %lld must be < 2^31", (long long)d->T * d->K);
-    if (!dim_ok(d->d, 64) || !dim_ok(d->h, 64) || (d->h_shared != 0 && !dim_ok(d->h_shared, 64)))
-        return fail(MOE_ERR_INVALID_ARG, "d = %d, h = %d, h_shared = %d out of range [64, 8192]", d->d,
-                    d->h, d->h_shared);
-    if (d->d % 64 || d->h % 64 || d->h_shared % 64)
-        return fail(MOE_ERR_UNSUPPORTED, "d = %d, h = %d, h_shared = %d must be multiples of 64", d->d,
-                    d->h, d->h_shared);
+    const int32_t hmin = swiglu ? 1 : 64;
+    if (!dim_ok(d->d, 64) || !dim_ok(d->h, hmin) || (d->h_shared != 0 && !dim_ok(d->h_shared, hmin)))
+        return fail(MOE_ERR_INVALID_ARG, "d = %d, h = %d, h_shared = %d out of range [%d, 8192]", d->d, d->h,
+                    d->h_shared, hmin);
+    if (d->d % 64) return fail(MOE_ERR_UNSUPPORTED, "d = %d must be a multiple of 64", d->d);
+    if (!swiglu && (d->h % 64 || d->h_shared % 64))
+        return fail(MOE_ERR_UNSUPPORTED, "h = %d, h_shared = %d must be multiples of 64 (GELU experts)", d->h,
+                    d->h_shared);
     if (!std::isfinite(d->lambda)) return fail(MOE_ERR_INVALID_ARG, "lambda is not finite");
     // GEMM operands are addressed through 32-bit buffer offsets.
     const uint64_t es = d->dtype == MOE_BF16 ? 2 : 4, lim = (uint64_t)1 << 32;
-    if ((uint64_t)d->T * d->d * es >= lim || (uint64_t)d->T * d->K * d->h * es >= lim ||
-        (uint64_t)d->T * d->h_shared * es >= lim)
+    if ((uint64_t)d->T * d->d * es >= lim || (uint64_t)d->T * d->K * act_stride(*d, d->h) * es >= lim ||
+        (uint64_t)d->T * act_stride(*d, d->h_shared) * es >= lim)
         return fail(MOE_ERR_UNSUPPORTED, "x, the expert activations or the shared activations exceed 4 GiB");
     return MOE_OK;
 }
@@ -112,6 +117,8 @@ WorkspacePlan plan_workspace(const moe_desc_t& d) {
     const size_t TK = (size_t)d.T * d.K;
     p.n_hist_blocks = permute_blocks((int64_t)TK, d.E);
     p.tile_bm = gemm_tile_bm(d.dtype, (int64_t)TK / d.E);
+    // The SwiGLU first layer runs on 256-row tiles only with two or more K slabs.
+    if ((d.flags & MOE_FLAG_SWIGLU) && d.d < 128) p.tile_bm = 64;
     const size_t busy = TK < (size_t)d.E ? TK : (size_t)d.E;  // experts that can hold a slot
     p.max_tiles = (int32_t)((TK + busy * (p.tile_bm - 1)) / p.tile_bm);
     size_t off = 0;
@@ -134,9 +141,9 @@ WorkspacePlan plan_workspace(const moe_desc_t& d) {
     p.blockhist = take((size_t)p.n_hist_blocks * d.E * 4);
     p.tiles = take((size_t)p.max_tiles * sizeof(TileDesc));
     p.ntiles = take(16);
-    p.act = take(TK * d.h * es);
+    p.act = take(TK * act_stride(d, d.h) * es);
     p.eout = take(TK * d.d * es);
-    p.sact = take((size_t)d.T * d.h_shared * es);
+    p.sact = take((size_t)d.T * act_stride(d, d.h_shared) * es);
     p.sout = take(d.h_shared ? (size_t)d.T * d.d * 4 : 0);
     p.total = off;
     return p;
@@ -195,24 +202,28 @@ static moe_status_t enqueue_routed_mlp(const moe_desc_t& d, const WorkspacePlan&
     g.row_map = sorted_slots;
     g.tiles = tiles;
     g.n_tiles = ntiles;
+    const bool swiglu = d.flags & MOE_FLAG_SWIGLU;
+    const int32_t ldh = act_stride(d, d.h);
     g.N = d.h;
     g.Kdim = d.d;
     g.route_k = d.K;
     g.row_mode = ROWS_GATHER_TOKENS;
     g.max_tiles = p.max_tiles;
-    g.b_group_stride = (int64_t)d.h * d.d;
+    g.b_group_stride = (int64_t)(swiglu ? 2 : 1) * d.h * d.d;
     g.a_bytes = (uint32_t)((size_t)d.T * d.d * elem_size(d.dtype));
-    HIP_CHECK(launch_gemm(d, EPI_GELU_STORE, p.tile_bm, g, s), "fc1 grouped gemm");
+    g.act_n = d.h;
+    g.act_ld = ldh;
+    HIP_CHECK(launch_gemm(d, swiglu ? EPI_SWIGLU_STORE : EPI_GELU_STORE, p.tile_bm, g, s), "fc1 grouped gemm");
     if (events) HIP_CHECK(hipEventRecord(static_cast<hipEvent_t>(events[1]), s), "event record");
     GemmArgs g2 = g;
     g2.A = region<void>(ws, p.act);
     g2.B = w2;
     g2.C = expert_out;
     g2.N = d.d;
-    g2.Kdim = d.h;
+    g2.Kdim = ldh;
     g2.row_mode = ROWS_IDENTITY;
-    g2.b_group_stride = (int64_t)d.d * d.h;
-    g2.a_bytes = (uint32_t)((size_t)d.T * d.K * d.h * elem_size(d.dtype));
+    g2.b_group_stride = (int64_t)d.d * ldh;
+    g2.a_bytes = (uint32_t)((size_t)d.T * d.K * ldh * elem_size(d.dtype));
     HIP_CHECK(launch_gemm(d, EPI_SCATTER_SLOT, p.tile_bm, g2, s), "fc2 grouped gemm");
     if (events) HIP_CHECK(hipEventRecord(static_cast<hipEvent_t>(events[2]), s), "event record");
     return MOE_OK;
@@ -231,7 +242,10 @@ static moe_status_t enqueue_shared_mlp(const moe_desc_t& d, const WorkspacePlan&
                                        const void* w1s, const void* w2s, float* sout, hipStream_t s,
                                        const CombineArgs* fuse = nullptr, bool* fused = nullptr) {
     if (fused) *fused = false;
-    const int bm = gemm_dense_bm(d.dtype, d.T, d.h_shared < d.d ? d.h_shared : d.d);
+    const bool swiglu = d.flags & MOE_FLAG_SWIGLU;
+    const int32_t ldh = act_stride(d, d.h_shared);
+    int bm = gemm_dense_bm(d.dtype, d.T, ldh < d.d ? ldh : d.d);
+    if (swiglu && d.d < 128) bm = 64;  // 256-row SwiGLU tiles need two or more K slabs
     GemmArgs g{};
     g.A = x;
     g.B = w1s;
@@ -243,14 +257,16 @@ static moe_status_t enqueue_shared_mlp(const moe_desc_t& d, const WorkspacePlan&
     g.row_mode = ROWS_IDENTITY;
     g.max_tiles = (d.T + bm - 1) / bm;
     g.a_bytes = (uint32_t)((size_t)d.T * d.d * elem_size(d.dtype));
-    HIP_CHECK(launch_gemm(d, EPI_GELU_STORE, bm, g, s), "shared fc1 gemm");
+    g.act_n = d.h_shared;
+    g.act_ld = ldh;
+    HIP_CHECK(launch_gemm(d, swiglu ? EPI_SWIGLU_STORE : EPI_GELU_STORE, bm, g, s), "shared fc1 gemm");
     GemmArgs g2 = g;
     g2.A = region<void>(ws, p.sact);
     g2.B = w2s;
     g2.C = sout;
     g2.N = d.d;
-    g2.Kdim = d.h_shared;
-    g2.a_bytes = (uint32_t)((size_t)d.T * d.h_shared * elem_size(d.dtype));
+    g2.Kdim = ldh;
+    g2.a_bytes = (uint32_t)((size_t)d.T * ldh * elem_size(d.dtype));
     if (fuse && fused && gemm_combine_fusable(d, bm, g2.N, g2.Kdim)) {
         g2.C = fuse->y;
         g2.gate = fuse->gate;

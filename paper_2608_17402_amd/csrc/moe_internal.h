@@ -40,6 +40,10 @@ enum GemmEpilogue : int {
     EPI_STORE_F32 = 2,      // C[p, :] = acc as fp32 (shared expert output)
     EPI_COMBINE = 3,        // C[p, :] = y_p = out(sum_j gate[p, j] eo[p K + j, :] + lambda acc): the
                             // gate-weighted combine fused into the shared expert's fc2 (dense only)
+    EPI_SWIGLU_STORE = 4,   // C[p, c] = act(SiLU(G[p, c]) * U[p, c]) for c < act_n, 0 for act_n <= c <
+                            // act_ld (C's row stride): B holds per group the act_n gate rows, then
+                            // the act_n up rows. The launcher sets N: a tile of BN columns computes
+                            // BN / 2 activation columns from the matching gate and up rows
 };
 
 struct GemmArgs {
@@ -57,6 +61,8 @@ struct GemmArgs {
     int32_t max_tiles;         // upper bound on the number of M-tiles (grid sizing)
     int64_t b_group_stride;    // elements between consecutive experts' weights
     uint32_t a_bytes;          // bytes of the A operand buffer (bounds of its buffer resource)
+    int32_t act_n;             // EPI_SWIGLU_STORE: activation width h (valid columns)
+    int32_t act_ld;            // EPI_SWIGLU_STORE: activation row stride (h rounded up to 128)
     const float* gate;         // EPI_COMBINE: gates [rows, route_k]
     const void* eo;            // EPI_COMBINE: expert outputs [rows * route_k, N] in slot order
     float lambda;              // EPI_COMBINE: shared-expert weight
@@ -77,6 +83,12 @@ size_t elem_size(int32_t dtype);
 WorkspacePlan plan_workspace(const moe_desc_t& d);
 // M-tile height of the grouped GEMM for groups of `avg_rows` rows on average.
 int gemm_tile_bm(int32_t dtype, int64_t avg_rows);
+// Row stride of an expert activation of hidden width h: h itself for GELU
+// experts, h rounded up to a multiple of 64 for SwiGLU experts (the padding
+// columns hold zeros, and the second layer's weights have the same stride).
+inline int32_t act_stride(const moe_desc_t& d, int32_t h) {
+    return (d.flags & MOE_FLAG_SWIGLU) ? (h + 63) / 64 * 64 : h;
+}
 // M-tile height of a dense GEMM of `rows` rows and `n` output columns.
 int gemm_dense_bm(int32_t dtype, int64_t rows, int32_t n);
 

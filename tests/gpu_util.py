@@ -7,7 +7,7 @@ import numpy as np
 import torch
 
 from paper_2608_17402_amd import binding
-from workloads import bf16_bits_to_f32
+from workloads import bf16_bits_to_f32, pad_last_dim
 
 BF16_MAX_ABS = 2e-2
 BF16_REL_L2 = 5e-3
@@ -33,10 +33,17 @@ def host(t: torch.Tensor) -> np.ndarray:
 
 
 def desc_for(cfg, T=None, **over):
+    flags = binding.MOE_FLAG_SWIGLU if getattr(cfg, "act", "gelu") == "swiglu" else 0
     kw = dict(T=cfg.T if T is None else T, d=cfg.d, E=cfg.E, K=cfg.K, h=cfg.h, h_shared=cfg.h_shared,
-              lam=cfg.lam, dtype=cfg.dtype, flags=0)
+              lam=cfg.lam, dtype=cfg.dtype, flags=flags)
     kw.update(over)
     return binding.make_desc(**kw)
+
+
+def pad_cols(a: np.ndarray | None, mult: int = 64) -> np.ndarray | None:
+    """Zero-pad the last axis to a multiple of `mult` (the second-layer weight
+    layout of SwiGLU experts: rows of ldh = h rounded up to 64)."""
+    return pad_last_dim(a, mult)
 
 
 def check_close(got: np.ndarray, ref: np.ndarray, bf16: bool, what: str = ""):
@@ -65,9 +72,10 @@ class DeviceLayer:
         self.w_router = dev(inp.w_router)
         self.bias = dev(inp.bias)
         self.w1 = dev(inp.w1)
-        self.w2 = dev(inp.w2)
+        swiglu = getattr(self.cfg, "act", "gelu") == "swiglu"
+        self.w2 = dev(pad_cols(inp.w2) if swiglu else inp.w2)
         self.w1s = dev(inp.w1s)
-        self.w2s = dev(inp.w2s)
+        self.w2s = dev(pad_cols(inp.w2s) if swiglu else inp.w2s)
         self.ws = binding.alloc_workspace(self.desc)
         self.dt = binding.torch_dtype(self.desc)
 

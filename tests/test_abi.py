@@ -72,7 +72,11 @@ def test_workspace_size_and_desc_validation(lib):
         "hs%64": (binding.make_desc(10, 64, 8, 2, 64, 65), 2),
         "d>8192": (binding.make_desc(10, 8256, 8, 2, 64), 1),
         "dtype": (binding.make_desc(10, 64, 8, 2, 64, 0, 1.0, 7), 2),
-        "flags": (binding.make_desc(10, 64, 8, 2, 64, 0, 1.0, "bf16", flags=2), 1),
+        "flags": (binding.make_desc(10, 64, 8, 2, 64, 0, 1.0, "bf16", flags=4), 1),
+        "swiglu f32": (binding.make_desc(10, 64, 8, 2, 64, 0, 1.0, "f32", flags=binding.MOE_FLAG_SWIGLU), 2),
+        "swiglu h=0": (binding.make_desc(10, 64, 8, 2, 0, 0, 1.0, "bf16", flags=binding.MOE_FLAG_SWIGLU), 1),
+        "swiglu h>8192": (binding.make_desc(10, 64, 8, 2, 8193, 0, 1.0, "bf16",
+                                            flags=binding.MOE_FLAG_SWIGLU), 1),
         "4GiB": (binding.make_desc(2 ** 21, 1024, 8, 2, 64, 0, 1.0, "bf16"), 2),
         "lambda": (binding.make_desc(10, 64, 8, 2, 64, 0, float("nan")), 1),
         "T*K": (binding.make_desc(2 ** 28, 64, 16, 8, 64), 1),
@@ -81,6 +85,21 @@ def test_workspace_size_and_desc_validation(lib):
         st, _ = _ws(desc)
         assert st == want, name
         assert lib.moe_last_error() != b""
+
+
+def test_swiglu_desc_and_workspace(lib):
+    """SwiGLU experts take any hidden width; the activations are stored with
+    rows padded to a multiple of 64 columns."""
+    sw = binding.MOE_FLAG_SWIGLU
+    st, n = _ws(binding.make_desc(65536, 1280, 31, 7, 854, 854, 1.0, "bf16", flags=sw))
+    assert st == 0
+    # routed activations [T*K, 896] + expert outputs [T*K, d] + shared activations [T, 896]
+    assert n >= 65536 * 7 * (896 + 1280) * 2 + 65536 * 896 * 2
+    st_g, n_g = _ws(binding.make_desc(65536, 1280, 31, 7, 896, 896, 1.0, "bf16"))
+    assert st_g == 0 and n == n_g  # padded SwiGLU activations take what GELU ones of width 896 take
+    for h in (1, 40, 100, 8192):
+        assert _ws(binding.make_desc(100, 64, 8, 2, h, h, 1.0, "bf16", flags=sw))[0] == 0, h
+    assert _ws(binding.make_desc(100, 64, 8, 2, 100, 0, 1.0, "bf16", flags=sw | binding.MOE_FLAG_EXACT_ROUTER))[0] == 0
 
 
 def test_entry_points_reject_bad_pointers_before_any_launch(lib):

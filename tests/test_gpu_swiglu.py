@@ -1,0 +1,147 @@
+"""Parity of the SwiGLU expert path (MOE_FLAG_SWIGLU) with the CPU oracle.
+
+SwiGLU experts compute W2 (SiLU(W1 x) * (W3 x)) (appendix "MoE Kernel",
+Algorithm 1, Phase 2; the MLPs of appendix "Implementation Details"). The
+GPU's first expert layer produces both projections of a tile in one kernel
+and writes only the bf16 activation. Routing is compared bit for bit; expert
+outputs and y within the bf16 tolerance. Hidden widths that are not multiples
+of 64 (the paper's H layer has 854) leave ragged activation columns that the
+kernel must zero: the second-layer weights are given non-zero padding columns,
+so any non-zero padding activation would show up in the output.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import DeviceLayer, check_close, dev, host
+from paper_2608_17402_amd import binding
+from workloads import get_config, make_inputs, pad_last_dim
+from workloads.configs import LayerConfig
+
+pytestmark = pytest.mark.gpu
+
+
+def _synthetic(name, T, d, E, K, h, hs, seed):
+    return LayerConfig(name=name, T=T, d=d, E=E, K=K, h=h, h_shared=hs, dtype="bf16", bias="uniform", seed=seed,
+                       act="swiglu")
+
+
+# Cases small enough for the oracle over every token. The comment names the
+# kernels each one reaches (256-row persistent tiles need >= 512 rows per
+# expert on average and d >= 128; otherwise 64-row tiles).
+SMALL = {
+    # single image, 1.81 GB of routed weights: ~32 rows per expert, 64-row tiles
+    "c6": get_config("single_image_swiglu_bf16"),
+    # the paper's H layer, h = 854 (ldh 896): 256-row persistent tiles for the routed experts
+    "c7_T2400": get_config("vith_swiglu_bf16").with_tokens(2400),
+    # the H layer with few tokens: 64-row tiles, ragged activation columns
+    "c7_T800": get_config("vith_swiglu_bf16").with_tokens(800),
+    # ldh = 320: the last 256-column tile has only one wave column of activations
+    "h300_pp": _synthetic("sw_h300", 3000, 128, 4, 2, 300, 300, seed=21),
+    # d = 64 (one K slab): 64-row tiles only; widths below one tile
+    "h40_d64": _synthetic("sw_h40", 700, 64, 6, 3, 40, 100, seed=22),
+    # the smallest widths
+    "h1": _synthetic("sw_h1", 130, 128, 4, 2, 1, 1, seed=23),
+}
+
+
+def _pad_nonzero(a):
+    """Second-layer weights with their padding columns set to 1.0 (finite,
+    non-zero): they must multiply zero activations."""
+    return pad_last_dim(a, 64, fill=0x3F80)  # bf16 1.0
+
+
+def _device_layer(inp):
+    lay = DeviceLayer(inp)
+    lay.w2 = dev(_pad_nonzero(inp.w2))
+    lay.w2s = dev(_pad_nonzero(inp.w2s))
+    return lay
+
+
+@pytest.fixture(scope="module", params=sorted(SMALL))
+def small(request):
+    cfg = SMALL[request.param]
+    inp = make_inputs(cfg)
+    lay = _device_layer(inp)
+    ref_idx, ref_gate = oracle.route(inp.f32("x"), inp.f32("w_router"), inp.bias, cfg.K)
+    return cfg, inp, lay, ref_idx, ref_gate
+
+
+def test_swiglu_grouped_mlp(small):
+    cfg, inp, lay, ref_idx, _ = small
+    _, ro, rs = oracle.permute(ref_idx, cfg.E)
+    eo = host(lay.grouped_mlp(dev(rs), dev(ro)))
+    x, w1, w2 = inp.f32("x"), inp.f32("w1"), inp.f32("w2")
+    ref = np.zeros((cfg.T * cfg.K, cfg.d))
+    for e in range(cfg.E):
+        seg = rs[ro[e]:ro[e + 1]]
+        if seg.size:
+            ref[seg] = oracle.expert_rows(x[seg // cfg.K], w1[e], w2[e], True, act="swiglu")
+    check_close(eo, ref, True, "swiglu expert_out")
+
+
+def test_swiglu_layer_forward(small):
+    cfg, inp, lay, ref_idx, ref_gate = small
+    y, idx, gate = lay.forward()
+    y2, _, _ = lay.forward(with_routing=False)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(idx), ref_idx) and np.array_equal(host(gate), ref_gate)
+    o_idx, _, y_ref = oracle.layer(inp.f32("x"), inp.f32("w_router"), inp.bias, inp.f32("w1"), inp.f32("w2"),
+                                   inp.f32("w1s"), inp.f32("w2s"), cfg.K, cfg.lam, True, act="swiglu")
+    assert np.array_equal(o_idx, ref_idx)
+    check_close(host(y), y_ref, True, "swiglu layer y")
+    assert np.array_equal(host(y).view(np.uint32), host(y2).view(np.uint32)), "repeat differs"
+
+
+def test_swiglu_shared_expert_through_grouped_mlp():
+    """A SwiGLU shared expert run as one group of every token."""
+    cfg = _synthetic("sw_shared", 333, 256, 4, 2, 64, 170, seed=24)
+    inp = make_inputs(cfg)
+    d1 = binding.make_desc(cfg.T, cfg.d, 1, 1, cfg.h_shared, 0, 1.0, "bf16", flags=binding.MOE_FLAG_SWIGLU)
+    ws = binding.alloc_workspace(d1)
+    slots = torch.arange(cfg.T, dtype=torch.int32, device="cuda")
+    offs = torch.tensor([0, cfg.T], dtype=torch.int32, device="cuda")
+    out = torch.empty(cfg.T, cfg.d, dtype=torch.bfloat16, device="cuda")
+    binding.moe_grouped_mlp(d1, dev(inp.x), slots, offs, dev(inp.w1s)[None], dev(_pad_nonzero(inp.w2s))[None],
+                            out, ws)
+    ref = oracle.expert_rows(inp.f32("x"), inp.f32("w1s"), inp.f32("w2s"), True, act="swiglu")
+    check_close(host(out), ref, True, "swiglu shared via grouped")
+
+
+# Larger shapes, checked on the whole routing and on sampled tokens.
+SAMPLED = {
+    # the paper's H layer at 64 x 1024 tokens: routed and shared experts on
+    # 256-row persistent tiles, K = 7 (separate combine)
+    "vith_full": (get_config("vith_swiglu_bf16"), None),
+    # 512 tiles of the shared expert with ldh_s = 320: dense persistent
+    # tiles whose last column tile holds one wave column of activations
+    "dense_pp_h300": (_synthetic("sw_dense", 512 * 256, 256, 8, 2, 64, 300, seed=25), None),
+    # single-image shape at 22605 tokens: routed and shared persistent tiles,
+    # and K = 8 with d % 256 == 0, so the shared fc2 fuses the combine;
+    # a partial last tile
+    "c6_fused_combine": (get_config("single_image_swiglu_bf16").with_tokens(89 * 256 - 179), 88 * 256),
+}
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name", sorted(SAMPLED))
+def test_swiglu_sampled_layer(name):
+    cfg, tail0 = SAMPLED[name]
+    inp = make_inputs(cfg)
+    lay = _device_layer(inp)
+    y, idx, gate = lay.forward()
+    torch.cuda.synchronize()
+    x, wr = inp.f32("x"), inp.f32("w_router")
+    ref_idx, ref_gate = oracle.route(x, wr, inp.bias, cfg.K)
+    assert np.array_equal(host(idx), ref_idx) and np.array_equal(host(gate), ref_gate)
+    rng = np.random.default_rng(2)
+    tok = [0, cfg.T - 1, *rng.choice(cfg.T, 40, replace=False)]
+    if tail0 is not None:
+        tok += list(range(tail0, cfg.T, 5))
+    tok = np.unique(np.asarray(tok)).astype(np.int32)
+    o_idx, _, y_ref = oracle.layer(x, wr, inp.bias, inp.f32("w1"), inp.f32("w2"), inp.f32("w1s"),
+                                   inp.f32("w2s"), cfg.K, cfg.lam, True, tokens=tok, act="swiglu")
+    assert np.array_equal(o_idx, ref_idx[tok])
+    check_close(host(y)[tok], y_ref, True, f"{name} sampled y")

@@ -15,11 +15,19 @@ def test_bf16_rounding_ties_to_even():
 
 def test_config_table():
     assert [c.name for c in CONFIGS.values()] == [
-        "tiny_f32", "vitb_bf16", "vitl_bf16", "vitg_skew_bf16", "single_image_bf16"]
+        "tiny_f32", "vitb_bf16", "vitl_bf16", "vitg_skew_bf16", "single_image_bf16",
+        "single_image_swiglu_bf16", "vith_swiglu_bf16"]
     assert get_config("c3").T == 65536 and get_config("c5").T == 1025
     for c in CONFIGS.values():
-        assert c.d % 64 == 0 and c.h % 64 == 0 and c.h_shared % 64 == 0
-        assert 1 <= c.K <= c.E
+        assert c.d % 64 == 0 and 1 <= c.K <= c.E
+        assert c.act == "swiglu" or (c.h % 64 == 0 and c.h_shared % 64 == 0)
+    # SwiGLU: three matrices per expert; the single-image layer holds 1.81 GB of routed weights
+    c6 = get_config("c6")
+    assert c6.act == "swiglu" and c6.routed_weight_bytes() == 3 * 256 * 768 * 1536 * 2
+    assert c6.gemm_flops() == 6.0 * 1025 * 1536 * (8 * 768 + 1536)
+    # the paper's H layer: 32 experts of width 854, one shared, 8 active
+    c7 = get_config("vith_swiglu_bf16")
+    assert (c7.d, c7.E + 1, c7.K + 1, c7.h, c7.h_shared) == (1280, 32, 8, 854, 854)
     # useful GEMM flops of the ViT-G layer: 4*T*d*(K*h + h_s)
     assert get_config("c4").gemm_flops() == 4.0 * 65536 * 1536 * (8 * 768 + 1536)
     assert get_config("c5").routed_weight_bytes() == 2 * 256 * 768 * 1536 * 2
@@ -36,6 +44,14 @@ def test_deterministic_and_independent_streams():
     assert a.x.dtype == np.float32 and a.w1.shape == (8, 256, 256) and a.w2.shape == (8, 256, 256)
     assert a.w1s is None and a.w2s is None
     assert np.all(np.abs(a.bias) <= 0.1)
+
+
+def test_swiglu_weight_shapes():
+    cfg = get_config("vith_swiglu_bf16").with_tokens(8)
+    a = make_inputs(cfg, parts=["w1", "w2", "w1s", "w2s"])
+    assert a.w1.shape == (31, 2 * 854, 1280) and a.w2.shape == (31, 1280, 854)
+    assert a.w1s.shape == (2 * 854, 1280) and a.w2s.shape == (1280, 854)
+    assert a.w1.dtype == np.uint16
 
 
 def test_bf16_config_storage_and_prefix():

@@ -13,6 +13,9 @@ never shifts another):
   5  W1s  [h_s, d]      N(0, weight_std)     shared expert fc1 (if h_s > 0)
   6  W2s  [d, h_s]      N(0, weight_std)     shared expert fc2
 
+SwiGLU experts draw W1 as [E, 2h, d] and W1s as [2 h_s, d] (gate rows, then
+up rows) from the same streams.
+
 Normal draws are float32; a bf16 layer stores the round-to-nearest-even bf16 of
 each draw (kept as raw uint16 bit patterns here). x rows are drawn row-major in
 one call, so the first T' rows of a config are the whole x of the same config
@@ -48,6 +51,21 @@ def f32_to_bf16_bits(a: np.ndarray, chunk: int = 1 << 24) -> np.ndarray:
         lsb = (u >> np.uint32(16)) & np.uint32(1)
         out[s:s + chunk] = ((u + np.uint32(0x7FFF) + lsb) >> np.uint32(16)).astype(np.uint16)
     return out.reshape(a.shape)
+
+
+def pad_last_dim(a: Optional[np.ndarray], mult: int = 64, fill: int = 0) -> Optional[np.ndarray]:
+    """Copy of `a` with its last axis padded to a multiple of `mult` with
+    `fill` (raw element value). Second-layer weights of SwiGLU experts are
+    passed to the GPU library in this layout: rows of h rounded up to 64."""
+    if a is None:
+        return None
+    n = a.shape[-1]
+    ld = -(-n // mult) * mult
+    if ld == n:
+        return a
+    out = np.full(a.shape[:-1] + (ld,), fill, dtype=a.dtype)
+    out[..., :n] = a
+    return out
 
 
 def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
@@ -131,13 +149,16 @@ def make_inputs(cfg: LayerConfig, parts: Optional[Iterable[str]] = None,
             out.bias = load_zipf_bias(cfg.E)
         else:
             raise ValueError(f"bias kind {kind!r}")
+    rows = 2 if cfg.act == "swiglu" else 1
+    if cfg.act not in ("gelu", "swiglu"):
+        raise ValueError(f"act {cfg.act!r}")
     if "w1" in want:
-        out.w1 = store(_normal(children[3], (cfg.E, cfg.h, cfg.d), std))
+        out.w1 = store(_normal(children[3], (cfg.E, rows * cfg.h, cfg.d), std))
     if "w2" in want:
         out.w2 = store(_normal(children[4], (cfg.E, cfg.d, cfg.h), std))
     if cfg.h_shared > 0:
         if "w1s" in want:
-            out.w1s = store(_normal(children[5], (cfg.h_shared, cfg.d), std))
+            out.w1s = store(_normal(children[5], (rows * cfg.h_shared, cfg.d), std))
         if "w2s" in want:
             out.w2s = store(_normal(children[6], (cfg.d, cfg.h_shared), std))
     return out
