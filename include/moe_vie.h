@@ -108,8 +108,8 @@ moe_status_t moe_workspace_size(const moe_desc_t *desc, size_t *bytes);
  * the sigmoid is 1/(1 + exp(-s)) with -s clamped to [-87, 87]
  * and evaluated by Cody-Waite reduction with ln2 = 22713*2^-15 + fl32(ln2 -
  * 22713*2^-15) and a degree-7 Taylor polynomial in Horner form; the gate
- * denominator is summed in slot order. For bf16 layers with E a multiple of
- * 64 the logits are first computed with bf16 MFMA; every expert whose key
+ * denominator is summed in slot order. For bf16 layers the logits are first
+ * computed with bf16 MFMA; every expert whose key
  * could still reach the top K under a proven bound on the difference is then
  * recomputed with the exact chain, so the result is the exact one.
  * Uses the workspace. */

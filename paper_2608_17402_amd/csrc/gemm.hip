@@ -109,6 +109,10 @@ __device__ __forceinline__ float swiglu_col(float g, float u, bool valid) {
     return valid ? silu_as(g) * u : 0.0f;
 }
 
+// Weight rows a tile may read: the group's rows (B rows past b_rows, when
+// set, read as zeros through the buffer-resource bound).
+__device__ __forceinline__ int weight_rows(const GemmArgs& a) { return a.b_rows > 0 ? a.b_rows : a.N; }
+
 // Epilogues of a first expert layer: their token rows are gathered from x.
 __host__ __device__ constexpr bool fc1_epi(int epi) { return epi == EPI_GELU_STORE || epi == EPI_SWIGLU_STORE; }
 
@@ -245,7 +249,7 @@ void k_gemm_bf16(const GemmArgs a) {
     // SwiGLU: the group's 2 act_n weight rows; reads past them return zeros.
     const __amdgpu_buffer_rsrc_t wres =
         make_rsrc(static_cast<const bf16_t*>(a.B) + (size_t)tc.e * a.b_group_stride,
-                  (uint32_t)(SWIGLU ? 2 * a.act_n : a.N) * Kd * 2);
+                  (uint32_t)(SWIGLU ? 2 * a.act_n : weight_rows(a)) * Kd * 2);
 
     constexpr int SWZ_SHIFT = CPR == 8 ? 1 : 2;
     constexpr int SWZ_MASK = CPR - 1;
@@ -495,7 +499,7 @@ void k_gemm_sp(const GemmArgs a) {
 
     const __amdgpu_buffer_rsrc_t xres = make_rsrc(a.A, a.a_bytes);
     const __amdgpu_buffer_rsrc_t wres =
-        make_rsrc(static_cast<const bf16_t*>(a.B) + (size_t)tc.e * a.b_group_stride, (uint32_t)a.N * Kd * 2);
+        make_rsrc(static_cast<const bf16_t*>(a.B) + (size_t)tc.e * a.b_group_stride, (uint32_t)weight_rows(a) * Kd * 2);
     const __amdgpu_buffer_rsrc_t xnull = make_rsrc(a.A, 0);
     const __amdgpu_buffer_rsrc_t wnull =
         make_rsrc(static_cast<const bf16_t*>(a.B) + (size_t)tc.e * a.b_group_stride, 0);
@@ -822,11 +826,15 @@ void k_gemm_pp(const GemmArgs a) {
     // SwiGLU: a tile of BN columns computes activation columns [n0 / 2,
     // n0 / 2 + 128); the resource starts at gate row n0 / 2 and ends with the
     // group's last up row, so rows past it read as zeros.
+    // The row counts are uniform; readfirstlane keeps the resource in scalar
+    // registers (the compiler cannot prove it and would wrap every copy in a
+    // waterfall loop).
     auto wres_of = [&](const Tile& t) {
         if (SWIGLU)
             return make_rsrc(Bw + (size_t)t.e * a.b_group_stride + (size_t)(t.n0 / 2) * Kd,
-                             (uint32_t)(2 * a.act_n - t.n0 / 2) * rowbytes);
-        return make_rsrc(Bw + (size_t)t.e * a.b_group_stride + (size_t)t.n0 * Kd, (uint32_t)BN * rowbytes);
+                             (uint32_t)__builtin_amdgcn_readfirstlane(2 * a.act_n - t.n0 / 2) * rowbytes);
+        const int rows = __builtin_amdgcn_readfirstlane(max(0, min(BN, weight_rows(a) - t.n0)));
+        return make_rsrc(Bw + (size_t)t.e * a.b_group_stride + (size_t)t.n0 * Kd, (uint32_t)rows * rowbytes);
     };
     auto xres_of = [&](const Tile& t) {
         if (GATHER) return make_rsrc(Ax, a.a_bytes);

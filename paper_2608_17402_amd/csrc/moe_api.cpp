@@ -111,6 +111,10 @@ T* region(void* ws, size_t off) {
 
 size_t elem_size(int32_t dtype) { return dtype == MOE_BF16 ? 2 : 4; }
 
+// Row stride of the router scores: E rounded up to 64, the column-tile width
+// of the MFMA logits GEMM (columns past E are computed from zero weight rows).
+static int32_t router_ld(const moe_desc_t& d) { return (d.E + 63) / 64 * 64; }
+
 WorkspacePlan plan_workspace(const moe_desc_t& d) {
     WorkspacePlan p;
     const size_t es = elem_size(d.dtype);
@@ -129,7 +133,7 @@ WorkspacePlan plan_workspace(const moe_desc_t& d) {
     };
     p.idx = take(TK * 4);
     p.gate = take(TK * 4);
-    p.scores = take((size_t)d.T * d.E * 4);
+    p.scores = take((size_t)d.T * router_ld(d) * 4);
     p.xnorm = take((size_t)d.T * 4);
     p.wnorm = take((size_t)d.E * 4);
     p.ovf = take((size_t)(d.T + 1) * 4);
@@ -149,9 +153,7 @@ WorkspacePlan plan_workspace(const moe_desc_t& d) {
     return p;
 }
 
-static bool fast_router(const moe_desc_t& d) {
-    return d.dtype == MOE_BF16 && d.E % 64 == 0 && !(d.flags & MOE_FLAG_EXACT_ROUTER);
-}
+static bool fast_router(const moe_desc_t& d) { return d.dtype == MOE_BF16 && !(d.flags & MOE_FLAG_EXACT_ROUTER); }
 
 // Router and gating: exact chain for every logit, or MFMA logits plus exact
 // repair of the candidates (same result).
@@ -169,16 +171,17 @@ static moe_status_t enqueue_route(const moe_desc_t& d, const WorkspacePlan& p, v
     g.B = w_router;
     g.C = scores;
     g.dense_rows = d.T;
-    g.N = d.E;
+    g.N = router_ld(d);
+    g.b_rows = d.E;
     g.Kdim = d.d;
     g.route_k = 1;
     g.row_mode = ROWS_IDENTITY;
-    const int bm = (int64_t)d.T * d.E >= (int64_t)200 * 65536 ? 256 : 64;
+    const int bm = (int64_t)d.T * g.N >= (int64_t)200 * 65536 ? 256 : 64;
     g.max_tiles = (d.T + bm - 1) / bm;
     g.a_bytes = (uint32_t)((size_t)d.T * d.d * 2);
     HIP_CHECK(launch_gemm(d, EPI_STORE_F32, bm, g, s), "router logits gemm");
     int32_t* ovf = region<int32_t>(ws, p.ovf);
-    HIP_CHECK(launch_router_fast_finish(d, scores, x, w_router, bias, region<float>(ws, p.xnorm),
+    HIP_CHECK(launch_router_fast_finish(d, scores, g.N, x, w_router, bias, region<float>(ws, p.xnorm),
                                         region<float>(ws, p.wnorm), region<uint16_t>(ws, p.cand),
                                         region<int32_t>(ws, p.ncand), ovf, ovf + 1, idx, gate, s),
               "router repair");

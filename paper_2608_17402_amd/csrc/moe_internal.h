@@ -60,6 +60,7 @@ struct GemmArgs {
     int32_t row_mode;          // GemmRowMode
     int32_t max_tiles;         // upper bound on the number of M-tiles (grid sizing)
     int64_t b_group_stride;    // elements between consecutive experts' weights
+    int32_t b_rows;            // dense bf16 only: rows of B that exist (0 = N); rows past them read as zeros
     uint32_t a_bytes;          // bytes of the A operand buffer (bounds of its buffer resource)
     int32_t act_n;             // EPI_SWIGLU_STORE: activation width h (valid columns)
     int32_t act_ld;            // EPI_SWIGLU_STORE: activation row stride (h rounded up to 128)
@@ -98,10 +99,11 @@ hipError_t launch_router_scores(const moe_desc_t& d, const void* x, const void* 
 hipError_t launch_topk(const moe_desc_t& d, const float* scores, const float* bias,
                        int32_t* topk_idx, float* topk_gate, hipStream_t s);
 // Fast-router tail: norms, candidate repair with exact recomputation, and the
-// exact fallback for tokens with too many candidates. s_fast = MFMA logits.
+// exact fallback for tokens with too many candidates. s_fast = MFMA logits,
+// rows of ld >= E floats.
 // cand [T][router_cand_slots(K)] and ncand [T] are scratch of the candidate
 // pass.
-hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, const void* x,
+hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, int ld, const void* x,
                                      const void* w_router, const float* bias, float* xnorm, float* wnorm,
                                      uint16_t* cand, int32_t* ncand, int32_t* ovf_count, int32_t* ovf_list,
                                      int32_t* topk_idx, float* topk_gate, hipStream_t s);

@@ -271,7 +271,7 @@ __global__ __launch_bounds__(256) void k_row_norms(const bf16_t* __restrict__ a,
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 // Candidates of each token: LPA lanes per token, lane g holding experts
-// g, g + LPA, ... (PER of them). L = the K-th largest lower end of the key
+// g, g + LPA, ... (PER of them); the MFMA logits have rows of ld >= E. L = the K-th largest lower end of the key
 // intervals; the candidates are the experts whose upper end reaches L, written
 // to cand[t][0 .. NS) with their count in ncand[t]. A token with more than NS
 // candidates gets ncand = -1 and is appended to the overflow queue.
@@ -279,8 +279,8 @@ template <int LPA, int PER, int NS>
 __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s_fast,
                                                     const float* __restrict__ xnorm,
                                                     const float* __restrict__ wnorm,
-                                                    const float* __restrict__ bias, int T, int E, int K,
-                                                    float cst, uint16_t* __restrict__ cand,
+                                                    const float* __restrict__ bias, int T, int E, int ld,
+                                                    int K, float cst, uint16_t* __restrict__ cand,
                                                     int32_t* __restrict__ ncand, int32_t* __restrict__ ovf_count,
                                                     int32_t* __restrict__ ovf_list) {
     static_assert(LPA <= kWave && kWave % LPA == 0, "token groups inside a wave");
@@ -300,7 +300,7 @@ __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s
         hi[m] = -INFINITY;
         if (live && e < E) {
             const float b = bias ? bias[e] : 0.0f;
-            const float key = sigmoid_fast(s_fast[(size_t)t * E + e]) + b;
+            const float key = sigmoid_fast(s_fast[(size_t)t * ld + e]) + b;
             const float delta = 0.25f * (cst * xn * wnorm[e]) + 4e-6f + 1e-6f * fabsf(b);
             lo[m] = key - delta;
             hi[m] = key + delta;
@@ -355,8 +355,8 @@ __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s
 // ascending order. The block's tokens stream their x rows from global memory;
 // the router weights of every expert stream through LDS in chunks of DC
 // columns (bf16, rows padded by 16 bytes against bank conflicts, widened to
-// fp32 in registers), double-buffered with one barrier per chunk. Tokens
-// queued by the candidate kernel are skipped.
+// fp32 in registers), double-buffered with one barrier per chunk; DC must
+// divide d. Tokens queued by the candidate kernel are skipped.
 template <int TPB, int LPT, int CPL, int EMAX, int DC>
 __global__ __launch_bounds__(TPB* LPT) void k_router_chain(const bf16_t* __restrict__ x,
                                                          const bf16_t* __restrict__ wr,
@@ -676,7 +676,7 @@ float router_fast_bound_constant(int d) {
     return (float)((gamma + 4.0 * d * u) * 1.01);
 }
 
-hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, const void* x,
+hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, int ld, const void* x,
                                      const void* w_router, const float* bias, float* xnorm, float* wnorm,
                                      uint16_t* cand, int32_t* ncand, int32_t* ovf_count, int32_t* ovf_list,
                                      int32_t* topk_idx, float* topk_gate, hipStream_t s) {
@@ -689,8 +689,8 @@ hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, c
     // Candidates: 16 lanes per token (64 for more than 256 experts).
 #define MOE_CAND(LPAv, PERv, NSv)                                                                           \
     hipLaunchKernelGGL((k_router_cand<LPAv, PERv, NSv>), dim3((d.T + 256 / LPAv - 1) / (256 / LPAv)),        \
-                       dim3(256), 0, s, s_fast, xnorm, wnorm, bias, d.T, d.E, d.K, cst, cand, ncand, ovf_count, \
-                       ovf_list)
+                       dim3(256), 0, s, s_fast, xnorm, wnorm, bias, d.T, d.E, ld, d.K, cst, cand, ncand,        \
+                       ovf_count, ovf_list)
     if (d.E <= 64) { if (ns == 16) MOE_CAND(16, 4, 16); else MOE_CAND(16, 4, 32); }
     else if (d.E <= 256) { if (ns == 16) MOE_CAND(16, 16, 16); else MOE_CAND(16, 16, 32); }
     else { if (ns == 16) MOE_CAND(64, 16, 16); else MOE_CAND(64, 16, 32); }
@@ -712,8 +712,10 @@ hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, c
         if (ns == 16) MOE_CHAIN_E(256, 4, 4, 64); else MOE_CHAIN_E(128, 8, 4, 64);
     } else if (d.T >= 256 * 64) {
         if (ns == 16) MOE_CHAIN_E(64, 4, 4, 64); else MOE_CHAIN_E(64, 8, 4, 64);
-    } else {
+    } else if (d.d % 128 == 0) {
         if (ns == 16) MOE_CHAIN_E(16, 16, 1, 128); else MOE_CHAIN_E(8, 32, 1, 128);
+    } else {  // the chunk width must divide d (a multiple of 64)
+        if (ns == 16) MOE_CHAIN_E(16, 16, 1, 64); else MOE_CHAIN_E(8, 32, 1, 64);
     }
 #undef MOE_CHAIN_E
 #undef MOE_CHAIN

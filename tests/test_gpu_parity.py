@@ -90,6 +90,29 @@ def test_route_near_ties_take_exact_fallback(dup):
         assert np.all(ref_idx == np.arange(K)[None, :])
 
 
+@pytest.mark.parametrize("E,K", [(1, 1), (5, 3), (31, 7), (63, 8), (65, 8), (100, 16), (200, 4)])
+def test_route_fast_path_any_expert_count(E, K):
+    # The MFMA pre-pass pads the logits to a multiple of 64 columns; routing
+    # must still equal the oracle's and the all-exact path's, bit for bit.
+    from workloads import bf16_bits_to_f32, f32_to_bf16_bits
+
+    T, d = 1500, 320
+    rng = np.random.default_rng(E * 100 + K)
+    x = f32_to_bf16_bits(rng.standard_normal((T, d)).astype(np.float32))
+    wr = f32_to_bf16_bits((rng.standard_normal((E, d)) * 0.05).astype(np.float32))
+    bias = rng.uniform(-0.05, 0.05, E).astype(np.float32)
+    ref_idx, ref_gate = oracle.route(bf16_bits_to_f32(x), bf16_bits_to_f32(wr), bias, K)
+    for flags in (0, binding.MOE_FLAG_EXACT_ROUTER):
+        desc = binding.make_desc(T, d, E, K, 64, flags=flags)
+        ws = binding.alloc_workspace(desc)
+        idx = torch.empty(T, K, dtype=torch.int32, device="cuda")
+        gate = torch.empty(T, K, dtype=torch.float32, device="cuda")
+        binding.moe_route(desc, dev(x), dev(wr), dev(bias), idx, gate, ws)
+        torch.cuda.synchronize()
+        assert np.array_equal(host(idx), ref_idx), flags
+        assert np.array_equal(host(gate), ref_gate), flags
+
+
 def test_permute_exact(small):
     cfg, inp, lay, _, ref_idx, _ = small
     counts, offsets, slots = lay.permute(dev(ref_idx))
