@@ -750,7 +750,7 @@ __device__ __forceinline__ float acc_read(float x) {
 // first row and spans its valid rows, so pad rows read as zeros. Gathered rows
 // repeat the tile's last valid row, as in k_gemm_sp. Requires K >= 128 (at
 // least two slabs per tile).
-template <int EPI, bool GROUPED>
+template <int EPI, bool GROUPED, int KC = 8>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_gemm_pp(const GemmArgs a) {
     constexpr int BM = 256, BN = 256, NW = 4, WT = 128, FB = WT / 32;
@@ -974,13 +974,12 @@ void k_gemm_pp(const GemmArgs a) {
         });
     };
 
-    // Fused combine (K = 8) for one staged fp32 block of the shared expert's
+    // Fused combine (K = KC) for one staged fp32 block of the shared expert's
     // output S: 32 rows x 64 columns, pieces of 8 columns (lanes 8 r + c take
     // row r, column piece c; four rows per lane). Per piece, in the order of
-    // the separate combine: acc = 0, acc = fma(g_j, O_j, acc) for j = 0..7,
+    // the separate combine: acc = 0, acc = fma(g_j, O_j, acc) for j = 0..K-1,
     // acc = fma(lambda, S, acc), one rounding to bf16.
     auto combine_block = [&](const Tile& t, uint32_t stg, int i, int h) {
-        constexpr int KC = 8;
         const int cp = lane & 7;
         const bf16_t* const eo = static_cast<const bf16_t*>(a.eo);
         // y rows of this tile; stores of pad rows fall outside and are dropped,
@@ -1005,15 +1004,23 @@ void k_gemm_pp(const GemmArgs a) {
         // used (twenty 16-byte loads in flight per lane).
 #pragma unroll
         for (int kp = 0; kp < 4; kp += 2) {
-            float4 g[2][2];
+            float gj[2][KC];
             u32x4_t o[2][KC];
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
                 const int rr = (lane >> 3) + 8 * (kp + u);
                 const int tok = t.row0 + min(wm * WT + i * 32 + rr, t.rows - 1);
                 const int c0 = t.n0 + wn * WT + h * 64 + cp * 8;
-                g[u][0] = *reinterpret_cast<const float4*>(a.gate + (size_t)tok * KC);
-                g[u][1] = *reinterpret_cast<const float4*>(a.gate + (size_t)tok * KC + 4);
+                if constexpr (KC % 4 == 0) {
+#pragma unroll
+                    for (int j = 0; j < KC; j += 4) {
+                        const float4 g4 = *reinterpret_cast<const float4*>(a.gate + (size_t)tok * KC + j);
+                        gj[u][j] = g4.x; gj[u][j + 1] = g4.y; gj[u][j + 2] = g4.z; gj[u][j + 3] = g4.w;
+                    }
+                } else {
+#pragma unroll
+                    for (int j = 0; j < KC; ++j) gj[u][j] = a.gate[(size_t)tok * KC + j];
+                }
 #pragma unroll
                 for (int j = 0; j < KC; ++j)
                     o[u][j] = *reinterpret_cast<const u32x4_t*>(eo + ((size_t)tok * KC + j) * a.N + c0);
@@ -1023,18 +1030,17 @@ void k_gemm_pp(const GemmArgs a) {
                 const int k = kp + u;
                 const int r = wm * WT + i * 32 + (lane >> 3) + 8 * k;
                 const int c0 = t.n0 + wn * WT + h * 64 + cp * 8;
-                const float gj[KC] = {g[u][0].x, g[u][0].y, g[u][0].z, g[u][0].w,
-                                      g[u][1].x, g[u][1].y, g[u][1].z, g[u][1].w};
                 float acc8[8];
 #pragma unroll
                 for (int q = 0; q < 8; ++q) acc8[q] = 0.0f;
 #pragma unroll
-                for (int j = 0; j < KC; ++j)
+                for (int j = 0; j < KC; ++j) {
 #pragma unroll
                     for (int q = 0; q < 4; ++q) {
-                        acc8[2 * q] = fmaf(gj[j], __uint_as_float(o[u][j][q] << 16), acc8[2 * q]);
-                        acc8[2 * q + 1] = fmaf(gj[j], __uint_as_float(o[u][j][q] & 0xffff0000u), acc8[2 * q + 1]);
+                        acc8[2 * q] = fmaf(gj[u][j], __uint_as_float(o[u][j][q] << 16), acc8[2 * q]);
+                        acc8[2 * q + 1] = fmaf(gj[u][j], __uint_as_float(o[u][j][q] & 0xffff0000u), acc8[2 * q + 1]);
                     }
+                }
                 const float sv[8] = {__uint_as_float(s0[k].x), __uint_as_float(s0[k].y), __uint_as_float(s0[k].z),
                                      __uint_as_float(s0[k].w), __uint_as_float(s1[k].x), __uint_as_float(s1[k].y),
                                      __uint_as_float(s1[k].z), __uint_as_float(s1[k].w)};
@@ -1365,11 +1371,27 @@ int persistent_grid(long long tile_bound) {
     return (int)(bound < cus[dev] ? bound : cus[dev]);
 }
 
-template <int EPI, bool GROUPED>
+template <int EPI, bool GROUPED, int KC = 8>
 hipError_t launch_pp(const GemmArgs& a, hipStream_t s) {
     const int grid = persistent_grid((long long)a.max_tiles * (a.N / 256));
-    hipLaunchKernelGGL((k_gemm_pp<EPI, GROUPED>), dim3((unsigned)grid), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((k_gemm_pp<EPI, GROUPED, KC>), dim3((unsigned)grid), dim3(256), 0, s, a);
     return hipGetLastError();
+}
+
+// The fused combine is compiled for each K (its gate and expert-row loads are
+// unrolled over the K slots).
+hipError_t launch_pp_combine(const GemmArgs& a, hipStream_t s) {
+    switch (a.route_k) {
+        case 1: return launch_pp<EPI_COMBINE, false, 1>(a, s);
+        case 2: return launch_pp<EPI_COMBINE, false, 2>(a, s);
+        case 3: return launch_pp<EPI_COMBINE, false, 3>(a, s);
+        case 4: return launch_pp<EPI_COMBINE, false, 4>(a, s);
+        case 5: return launch_pp<EPI_COMBINE, false, 5>(a, s);
+        case 6: return launch_pp<EPI_COMBINE, false, 6>(a, s);
+        case 7: return launch_pp<EPI_COMBINE, false, 7>(a, s);
+        case 8: return launch_pp<EPI_COMBINE, false, 8>(a, s);
+    }
+    return hipErrorInvalidValue;
 }
 
 template <int EPI, bool GROUPED>
@@ -1449,7 +1471,7 @@ hipError_t dispatch(const moe_desc_t& d, int epilogue, int bm, const GemmArgs& a
                 break;
             case EPI_COMBINE:
                 if (!GROUPED && gemm_combine_fusable(d, bm, a.N, a.Kdim) && a.route_k == d.K)
-                    return launch_pp<EPI_COMBINE, false>(a, s);
+                    return launch_pp_combine(a, s);
                 break;
         }
     } else {
@@ -1482,8 +1504,8 @@ int gemm_dense_bm(int32_t dtype, int64_t rows, int32_t n) {
 }
 
 bool gemm_combine_fusable(const moe_desc_t& d, int bm, int n, int kdim) {
-    // The persistent 256 x 256 kernel with its K = 8 combine epilogue.
-    return d.dtype == MOE_BF16 && d.K == 8 && bm == 256 && n % 256 == 0 && kdim >= 128;
+    // The persistent 256 x 256 kernel with its combine epilogue (K <= 8).
+    return d.dtype == MOE_BF16 && d.K <= 8 && bm == 256 && n % 256 == 0 && kdim >= 128;
 }
 
 hipError_t launch_gemm(const moe_desc_t& d, int epilogue, int bm, const GemmArgs& a, hipStream_t s) {

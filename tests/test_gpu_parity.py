@@ -346,6 +346,33 @@ def test_shared_fc2_with_fused_combine_ragged_tail():
     check_close(host(y)[tok], y_ref, True, "fused-combine sampled y")
 
 
+@pytest.mark.slow
+@pytest.mark.parametrize("K", [1, 2, 3, 5, 7])
+def test_fused_combine_any_k(K):
+    """The shared expert's fc2 performs the combine for every K <= 8 once it
+    runs on 256-row tiles: 512 + 1 tiles with a partial last tile (77 rows).
+    Sampled tokens, including the tail, match the oracle; a repeat is
+    bit-identical."""
+    from workloads.configs import LayerConfig
+
+    cfg = LayerConfig(name=f"fused_k{K}", T=512 * 256 + 77, d=256, E=16, K=K, h=128, h_shared=256,
+                      dtype="bf16", bias="uniform", seed=40 + K)
+    inp = make_inputs(cfg)
+    lay = DeviceLayer(inp)
+    y, idx, gate = lay.forward()
+    y2, _, _ = lay.forward()
+    torch.cuda.synchronize()
+    assert np.array_equal(host(y).view(np.uint32), host(y2).view(np.uint32))
+    x, wr = inp.f32("x"), inp.f32("w_router")
+    rng = np.random.default_rng(K)
+    tok = np.unique(np.r_[0, rng.choice(cfg.T, 30, replace=False), np.arange(512 * 256, cfg.T, 3),
+                          cfg.T - 1]).astype(np.int32)
+    o_idx, o_gate, y_ref = oracle.layer(x, wr, inp.bias, inp.f32("w1"), inp.f32("w2"), inp.f32("w1s"),
+                                        inp.f32("w2s"), cfg.K, cfg.lam, True, tokens=tok)
+    assert np.array_equal(host(idx)[tok], o_idx) and np.array_equal(host(gate)[tok], o_gate)
+    check_close(host(y)[tok], y_ref, True, f"fused combine K={K}")
+
+
 @pytest.mark.parametrize("E", [1, 3, 8, 64, 256, 1024])
 def test_bias_update_bit_exact(E):
     """Loss-free balancing update (Eqs. (8)-(9)) through the C ABI against the
