@@ -10,8 +10,11 @@ from .oracle import (  # noqa: F401
     bias_update,
     build_oracle,
     combine,
+    expert_backward,
     expert_rows,
     gelu,
+    gelu_grad,
+    grouped_backward,
     layer,
     logits,
     num_threads,
@@ -21,5 +24,6 @@ from .oracle import (  # noqa: F401
     scores,
     sigmoid,
     silu,
+    silu_grad,
     topk_from_scores,
 )

@@ -17,6 +17,10 @@
  *   SwiGLU expert MLP    E(x) = W2 (SiLU(W1 x) * (W3 x))   App. "MoE Kernel", Algorithm 1 Phase 2
  *   bias update          b_e -= alpha sign(t_e - mu)  or  alpha (t_e - mu) / sigma
  *                                                       Sec. 3.2 "Load Balancing", Eqs. (8)-(9)
+ *   expert backward      dx, dW1, dW2 of the expert MLP given the gradient of
+ *                        its output (the grouped training GEMMs with the
+ *                        activation as a separate step, App. "MoE Kernel",
+ *                        the paragraph after Algorithm 1): the chain rule
  *
  * Precision. Everything that is a plain definition (expert MLPs, combine) is
  * evaluated in double precision. Routing decides integers (which experts a
@@ -39,6 +43,11 @@
  *   - in a bf16 layer the expert activation GELU(W1 x) is materialised in bf16
  *     (round to nearest even) before fc2, as the paper's kernel writes its
  *     activation tile to a buffer; nothing else is rounded here.
+ *   - backward: the same rounding points as the forward for the activation
+ *     (bf16 layers round act(W1 x) to bf16, which dW2 then uses), and in a
+ *     bf16 layer the gradient of the pre-activation (GELU: dH; SwiGLU: dG and
+ *     dU) is rounded to bf16, the operand of the dx and dW1 products. Weight
+ *     gradients are sums over the expert's rows; nothing else is rounded.
  *   - bias update: t_e is the number of tokens routed to expert e (the
  *     permutation's counts), mu their mean over the E experts, sigma their
  *     standard deviation over the E experts (the whole population: divided
@@ -281,6 +290,108 @@ void oracle_expert_rows(int n, int d, int h, const float *rows, const float *w1,
 void oracle_expert_rows_swiglu(int n, int d, int h, const float *rows, const float *w13,
                                const float *w2, int act_bf16, double *out) {
     expert_rows(n, d, h, 1, rows, w13, w2, act_bf16, out);
+}
+
+/* ------------------------------------------------------- expert backward */
+
+/* d/dv GELU(v) = Phi(v) + v phi(v), Phi the standard normal CDF and phi its
+ * density. */
+double oracle_gelu_grad(double v) {
+    return 0.5 * (1.0 + erf(v * 0.70710678118654752440)) + v * exp(-0.5 * v * v) * 0.39894228040143267794;
+}
+
+/* d/dv SiLU(v) = s (1 + v (1 - s)) with s = Sigmoid(v) = 1 / (1 + exp(-v)). */
+double oracle_silu_grad(double v) {
+    const double sg = 1.0 / (1.0 + exp(-v));
+    return sg * (1.0 + v * (1.0 - sg));
+}
+
+/* Backward of one expert MLP over n rows (the chain rule, term by term).
+ * Forward per row r (x = rows[r], out = W2 a):
+ *   GELU experts:   p = W1 x, a = GELU(p)
+ *   SwiGLU experts: p = W1 x (gate), q = W3 x (up), a = SiLU(p) * q
+ * Given G = go[r] = dL/d out:
+ *   da    = W2^T G
+ *   GELU:   dp = da * GELU'(p)
+ *   SwiGLU: dp = da * q * SiLU'(p),  dq = da * SiLU(p)
+ *   dx[r] = W1^T dp (+ W3^T dq)
+ *   dW2  += G a^T,  dW1 += dp x^T  (dW3 += dq x^T)
+ * act_bf16: a, dp and dq are rounded to bf16 where they are formed.
+ * Shapes: rows, go, dx [n, d]; w1 and dw1 [h, d] (SwiGLU [2h, d]: gate rows,
+ * then up rows); w2 and dw2 [d, h]. dw1 and dw2 are overwritten with the sums
+ * over the n rows, taken in ascending row order. */
+static void expert_backward(int n, int d, int h, int swiglu, const float *rows, const float *w1,
+                            const float *w2, const float *go, int act_bf16, double *dx, double *dw1,
+                            double *dw2) {
+    const int hr = swiglu ? 2 * h : h;              /* rows of w1 and dw1 */
+    double *act = (double *)malloc(sizeof(double) * (size_t)n * h);
+    double *dpre = (double *)malloc(sizeof(double) * (size_t)n * hr); /* dp rows, then dq rows */
+#pragma omp parallel
+    {
+        double *da = (double *)malloc(sizeof(double) * (size_t)h);
+#pragma omp for schedule(static)
+        for (int r = 0; r < n; ++r) {
+            const float *x = rows + (size_t)r * d;
+            const float *g = go + (size_t)r * d;
+            for (int k = 0; k < h; ++k) {
+                double acc = 0.0;
+                for (int c = 0; c < d; ++c) acc += (double)w2[(size_t)c * h + k] * (double)g[c];
+                da[k] = acc;
+            }
+            for (int k = 0; k < h; ++k) {
+                const float *wg = w1 + (size_t)k * d;
+                double p = 0.0;
+                for (int i = 0; i < d; ++i) p += (double)wg[i] * (double)x[i];
+                double a, dp, dq = 0.0;
+                if (swiglu) {
+                    const float *wu = w1 + ((size_t)h + k) * d;
+                    double q = 0.0;
+                    for (int i = 0; i < d; ++i) q += (double)wu[i] * (double)x[i];
+                    a = oracle_silu(p) * q;
+                    dp = da[k] * q * oracle_silu_grad(p);
+                    dq = da[k] * oracle_silu(p);
+                } else {
+                    a = oracle_gelu(p);
+                    dp = da[k] * oracle_gelu_grad(p);
+                }
+                act[(size_t)r * h + k] = act_bf16 ? oracle_round_bf16(a) : a;
+                dpre[(size_t)r * hr + k] = act_bf16 ? oracle_round_bf16(dp) : dp;
+                if (swiglu) dpre[(size_t)r * hr + h + k] = act_bf16 ? oracle_round_bf16(dq) : dq;
+            }
+            for (int i = 0; i < d; ++i) {
+                double acc = 0.0;
+                for (int k = 0; k < hr; ++k) acc += (double)w1[(size_t)k * d + i] * dpre[(size_t)r * hr + k];
+                dx[(size_t)r * d + i] = acc;
+            }
+        }
+        free(da);
+    }
+#pragma omp parallel for schedule(static)
+    for (int c = 0; c < d; ++c)
+        for (int k = 0; k < h; ++k) {
+            double acc = 0.0;
+            for (int r = 0; r < n; ++r) acc += (double)go[(size_t)r * d + c] * act[(size_t)r * h + k];
+            dw2[(size_t)c * h + k] = acc;
+        }
+#pragma omp parallel for schedule(static)
+    for (int k = 0; k < hr; ++k)
+        for (int i = 0; i < d; ++i) {
+            double acc = 0.0;
+            for (int r = 0; r < n; ++r) acc += dpre[(size_t)r * hr + k] * (double)rows[(size_t)r * d + i];
+            dw1[(size_t)k * d + i] = acc;
+        }
+    free(act);
+    free(dpre);
+}
+
+void oracle_expert_backward(int n, int d, int h, const float *rows, const float *w1, const float *w2,
+                            const float *go, int act_bf16, double *dx, double *dw1, double *dw2) {
+    expert_backward(n, d, h, 0, rows, w1, w2, go, act_bf16, dx, dw1, dw2);
+}
+
+void oracle_expert_backward_swiglu(int n, int d, int h, const float *rows, const float *w13, const float *w2,
+                                   const float *go, int act_bf16, double *dx, double *dw13, double *dw2) {
+    expert_backward(n, d, h, 1, rows, w13, w2, go, act_bf16, dx, dw13, dw2);
 }
 
 /* --------------------------------------------------------------- combine */

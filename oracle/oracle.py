@@ -70,6 +70,10 @@ def _load():
             "oracle_silu": ([D], D),
             "oracle_expert_rows_swiglu": ([I, I, I, P, P, P, I, P], None),
             "oracle_layer_swiglu": ([I, P, I, I, I, I, I, I, F, I, P, P, P, P, P, P, P, P, P, P], None),
+            "oracle_gelu_grad": ([D], D),
+            "oracle_silu_grad": ([D], D),
+            "oracle_expert_backward": ([I, I, I, P, P, P, P, I, P, P, P], None),
+            "oracle_expert_backward_swiglu": ([I, I, I, P, P, P, P, I, P, P, P], None),
         }
         for name, (args, res) in sigs.items():
             fn = getattr(lib, name)
@@ -181,6 +185,63 @@ def expert_rows(rows, w1, w2, act_bf16: bool, act: str = "gelu") -> np.ndarray:
     assert act in ("gelu", "swiglu")
     fn(n, d, h, _ptr(rows), _ptr(w1), _ptr(w2), int(bool(act_bf16)), _ptr(out))
     return out
+
+
+def gelu_grad(v) -> np.ndarray:
+    """d/dv GELU(v) in double precision (elementwise)."""
+    f = _load().oracle_gelu_grad
+    return np.vectorize(lambda z: f(float(z)), otypes=[np.float64])(np.asarray(v, dtype=np.float64))
+
+
+def silu_grad(v) -> np.ndarray:
+    """d/dv SiLU(v) in double precision (elementwise)."""
+    f = _load().oracle_silu_grad
+    return np.vectorize(lambda z: f(float(z)), otypes=[np.float64])(np.asarray(v, dtype=np.float64))
+
+
+def expert_backward(rows, w1, w2, grad_out, act_bf16: bool, act: str = "gelu"):
+    """Backward of one expert MLP over the rows [n, d] given grad_out [n, d]
+    (the gradient of W2 act(W1 r) for each row). Returns float64 (dx [n, d],
+    dw1 [h, d] or [2h, d] for SwiGLU, dw2 [d, h]); the weight gradients are
+    sums over the rows."""
+    assert act in ("gelu", "swiglu")
+    rows, w1, w2, grad_out = _f32(rows), _f32(w1), _f32(w2), _f32(grad_out)
+    n, d = rows.shape
+    h = w2.shape[1]
+    hr = 2 * h if act == "swiglu" else h
+    assert w1.shape == (hr, d) and w2.shape == (d, h) and grad_out.shape == (n, d)
+    dx = np.empty((n, d), dtype=np.float64)
+    dw1 = np.empty((hr, d), dtype=np.float64)
+    dw2 = np.empty((d, h), dtype=np.float64)
+    fn = _load().oracle_expert_backward_swiglu if act == "swiglu" else _load().oracle_expert_backward
+    fn(n, d, h, _ptr(rows), _ptr(w1), _ptr(w2), _ptr(grad_out), int(bool(act_bf16)), _ptr(dx), _ptr(dw1),
+       _ptr(dw2))
+    return dx, dw1, dw2
+
+
+def grouped_backward(x, topk_idx, w1, w2, grad_expert_out, act_bf16: bool, act: str = "gelu"):
+    """Backward of the routed experts of a layer: x [T, d], topk_idx [T, K],
+    w1 [E, h or 2h, d], w2 [E, d, h], grad_expert_out [T*K, d] in slot order.
+    Returns float64 (dx [T, d] summed over each token's K slots in slot
+    order, dw1 like w1, dw2 like w2)."""
+    x = _f32(x)
+    g = _f32(grad_expert_out)
+    T, K = np.asarray(topk_idx).shape
+    E = w1.shape[0]
+    _, offsets, slots = permute(topk_idx, E)
+    dxs = np.zeros((T * K, x.shape[1]), dtype=np.float64)
+    dw1 = np.zeros(w1.shape, dtype=np.float64)
+    dw2 = np.zeros(w2.shape, dtype=np.float64)
+    for e in range(E):
+        seg = slots[offsets[e]:offsets[e + 1]]
+        if seg.size == 0:
+            continue
+        dxr, dw1[e], dw2[e] = expert_backward(x[seg // K], w1[e], w2[e], g[seg], act_bf16, act)
+        dxs[seg] = dxr
+    dx = dxs.reshape(T, K, -1)[:, 0, :].copy()
+    for j in range(1, K):
+        dx += dxs.reshape(T, K, -1)[:, j, :]
+    return dx, dw1, dw2
 
 
 def combine(expert_out, gate, shared, lam: float) -> np.ndarray:

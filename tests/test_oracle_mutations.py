@@ -53,6 +53,14 @@ MUTANTS = {
     "swiglu_up_reads_gate_rows": ("const float *wu = w1 + ((size_t)h + k) * d;", "const float *wu = w1 + (size_t)k * d;"),
     "swiglu_expert_stride": ("const size_t w1_rows = swiglu ? 2 * (size_t)h : (size_t)h;",
                              "const size_t w1_rows = (size_t)h;"),
+    "gelu_grad_drops_density": ("+ v * exp(-0.5 * v * v) * 0.39894228040143267794", ""),
+    "bwd_w2_not_transposed": ("acc += (double)w2[(size_t)c * h + k] * (double)g[c];",
+                              "acc += (double)w2[(size_t)k * d + c] * (double)g[c];"),
+    "bwd_dw2_uses_preactivation": ("act[(size_t)r * h + k] = act_bf16 ? oracle_round_bf16(a) : a;",
+                                   "act[(size_t)r * h + k] = act_bf16 ? oracle_round_bf16(p) : p;"),
+    "bwd_dp_not_rounded": ("dpre[(size_t)r * hr + k] = act_bf16 ? oracle_round_bf16(dp) : dp;",
+                           "dpre[(size_t)r * hr + k] = dp;"),
+    "bwd_swiglu_dq_wrong": ("dq = da[k] * oracle_silu(p);", "dq = da[k] * p;"),
 }
 
 

@@ -524,3 +524,132 @@ def test_swiglu_layer_identical_experts_and_shared():
     w2[:] = 0
     _, _, y0 = oracle.layer(x, wr, b, w13, w2, w13s, w2s, 3, 1.0, False, act="swiglu")
     assert np.max(np.abs(y0 - oracle.expert_rows(x, w13s, w2s, False, act="swiglu"))) < 1e-12
+
+
+# ---------------------------------------------------------- expert backward
+
+
+def test_activation_gradients_against_scipy_and_differences():
+    from scipy.special import expit
+    from scipy.stats import norm
+
+    assert oracle.gelu_grad([0.0])[0] == 0.5
+    assert abs(oracle.gelu_grad([1.0])[0] - (norm.cdf(1.0) + norm.pdf(1.0))) < 1e-15
+    assert oracle.silu_grad([0.0])[0] == 0.5
+    v = np.linspace(-8, 8, 161)
+    eps = 1e-5
+    gelu = lambda z: z * norm.cdf(z)  # noqa: E731
+    silu = lambda z: z * expit(z)  # noqa: E731
+    assert np.max(np.abs(oracle.gelu_grad(v) - (gelu(v + eps) - gelu(v - eps)) / (2 * eps))) < 1e-8
+    assert np.max(np.abs(oracle.silu_grad(v) - (silu(v + eps) - silu(v - eps)) / (2 * eps))) < 1e-8
+
+
+def _dyadic(rng, shape, scale):
+    """float32 values on a 2^-8 grid: x +- 2^-14 stays exact in float32."""
+    return (np.round(rng.uniform(-scale, scale, shape) * 256) / 256).astype(np.float32)
+
+
+@pytest.mark.parametrize("act", ["gelu", "swiglu"])
+def test_expert_backward_matches_central_differences(act):
+    # L = sum_r <G_r, W2 act(W1 x_r)>; the oracle's forward (float64 from
+    # float32 inputs) is differentiated numerically in every input and weight.
+    rng = np.random.default_rng(31)
+    n, d, h = 3, 6, 5  # d != h: a transposed operand cannot pass
+    hr = 2 * h if act == "swiglu" else h
+    x = _dyadic(rng, (n, d), 1.5)
+    w1 = _dyadic(rng, (hr, d), 0.7)
+    w2 = _dyadic(rng, (d, h), 0.7)
+    g = rng.standard_normal((n, d)).astype(np.float32)
+    dx, dw1, dw2 = oracle.expert_backward(x, w1, w2, g, False, act=act)
+    step = 2.0 ** -14
+
+    def loss(xx, a1, a2):
+        return float(np.sum(oracle.expert_rows(xx, a1, a2, False, act=act) * g.astype(np.float64)))
+
+    def fd(which, arr, idx):
+        p, m = arr.copy(), arr.copy()
+        p[idx] += np.float32(step)
+        m[idx] -= np.float32(step)
+        args_p = [x, w1, w2]
+        args_m = [x, w1, w2]
+        args_p[which], args_m[which] = p, m
+        return (loss(*args_p) - loss(*args_m)) / (2 * step)
+
+    for which, arr, grad in ((0, x, dx), (1, w1, dw1), (2, w2, dw2)):
+        for idx in np.ndindex(arr.shape):
+            want = fd(which, arr, idx)
+            assert abs(grad[idx] - want) <= 1e-7 * (1 + abs(want)), (act, which, idx, grad[idx], want)
+
+
+def test_expert_backward_identity_closed_form():
+    from scipy.stats import norm
+
+    rng = np.random.default_rng(32)
+    d, c = 16, 0.375
+    x = rng.standard_normal((9, d)).astype(np.float32)
+    g = rng.standard_normal((9, d)).astype(np.float32)
+    eye = np.eye(d, dtype=np.float32)
+    dx, dw1, dw2 = oracle.expert_backward(x, eye, c * eye, g, False)
+    xd, gd = x.astype(np.float64), g.astype(np.float64)
+    gp = norm.cdf(xd) + xd * norm.pdf(xd)  # GELU'
+    assert np.max(np.abs(dx - c * gd * gp)) < 1e-13
+    assert np.max(np.abs(dw2 - gd.T @ (xd * norm.cdf(xd)))) < 1e-12
+    assert np.max(np.abs(dw1 - (c * gd * gp).T @ xd)) < 1e-12
+
+
+@pytest.mark.parametrize("act", ["gelu", "swiglu"])
+def test_expert_backward_bf16_rounding_points(act):
+    # bf16 layers: dW2 uses the rounded activation (the forward's), and the
+    # pre-activation gradient is rounded before it meets x and W1.
+    from scipy.special import expit
+    from scipy.stats import norm
+
+    rng = np.random.default_rng(33)
+    n, d, h = 11, 24, 10
+    hr = 2 * h if act == "swiglu" else h
+    x = bf16_values(rng, (n, d), 1.0)
+    w1 = bf16_values(rng, (hr, d), 0.3)
+    w2 = bf16_values(rng, (d, h), 0.3)
+    g = bf16_values(rng, (n, d), 1.0)
+    dx, dw1, dw2 = oracle.expert_backward(x, w1, w2, g, True, act=act)
+    xd, gd = x.astype(np.float64), g.astype(np.float64)
+    p = xd @ w1[:h].astype(np.float64).T
+    da = gd @ w2.astype(np.float64)
+    if act == "gelu":
+        a = p * norm.cdf(p)
+        dpre = bf16_round64(da * (norm.cdf(p) + p * norm.pdf(p)))
+    else:
+        q = xd @ w1[h:].astype(np.float64).T
+        s = expit(p)
+        a = p * s * q
+        dpre = np.concatenate([bf16_round64(da * q * s * (1 + p * (1 - s))), bf16_round64(da * p * s)], axis=1)
+    a = bf16_round64(a)
+    assert np.max(np.abs(dw2 - gd.T @ a)) < 1e-9
+    assert np.max(np.abs(dw1 - dpre.T @ xd)) < 1e-9
+    assert np.max(np.abs(dx - dpre @ w1.astype(np.float64))) < 1e-9
+
+
+def test_grouped_backward_sums_slots_and_experts():
+    # Identical experts: each token's dx is the sum over its K slots of one
+    # expert's backward, and the weight gradients summed over experts equal
+    # one expert's over all slots; linear in the output gradient.
+    rng = np.random.default_rng(34)
+    T, d, E, K, h = 30, 12, 5, 3, 7
+    x = rng.standard_normal((T, d)).astype(np.float32)
+    w1 = np.repeat(rng.standard_normal((1, h, d)).astype(np.float32) * 0.4, E, axis=0)
+    w2 = np.repeat(rng.standard_normal((1, d, h)).astype(np.float32) * 0.4, E, axis=0)
+    idx = np.stack([rng.choice(E, K, replace=False) for _ in range(T)]).astype(np.int32)
+    g1 = rng.standard_normal((T * K, d)).astype(np.float32)
+    g2 = rng.standard_normal((T * K, d)).astype(np.float32)
+    dx, dw1, dw2 = oracle.grouped_backward(x, idx, w1, w2, g1, False)
+    rows = np.repeat(x, K, axis=0)
+    dxr, dw1r, dw2r = oracle.expert_backward(rows, w1[0], w2[0], g1, False)
+    assert np.max(np.abs(dx - dxr.reshape(T, K, d).sum(1))) < 1e-12
+    assert np.max(np.abs(dw1.sum(0) - dw1r)) < 1e-11 and np.max(np.abs(dw2.sum(0) - dw2r)) < 1e-11
+    used = np.zeros(E, bool)
+    used[np.unique(idx)] = True
+    assert np.all(dw1[~used] == 0) and np.all(dw2[~used] == 0)
+    a = oracle.grouped_backward(x, idx, w1, w2, g1 + g2, False)
+    b = oracle.grouped_backward(x, idx, w1, w2, g2, False)
+    for u, v, w in zip(a, (dx, dw1, dw2), b):
+        assert np.max(np.abs(u - (v + w))) < 1e-5
