@@ -69,6 +69,8 @@ def parse():
     p.add_argument("--swiglu-configs", default="vith_swiglu_bf16,single_image_swiglu_bf16",
                    help="SwiGLU-expert layers measured beside the main workload (comma-separated, '' for none)")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-backward", action="store_true",
+                   help="skip the expert-MLP backward (training) measurement on the main workload")
     p.add_argument("--cpu-seconds", type=float, default=15.0,
                    help="target CPU time of the oracle sample")
     p.add_argument("--stage-reps", type=int, default=10)
@@ -308,6 +310,38 @@ def main():
             weight_bound = c.T * c.K / c.E < 256
             out["swiglu"][name] = hbm_line(c, L, l_ms, f1 + f2) if weight_bound else mfma_line(c, l_ms, f1, f2)
             del L
+
+    if not args.no_backward and cfg.act == "gelu" and cfg.dtype == "bf16":
+        # Expert-MLP backward on the main workload's routing: 5 products of
+        # 2 T K d h flop (fc1 again, dA, dx, dW2, dW1).
+        T, K, E, d, h = cfg.T, cfg.K, cfg.E, cfg.d, cfg.h
+        lay.forward()
+        binding.moe_permute(lay.desc, lay.idx, lay.counts, lay.offsets, lay.slots, lay.ws)
+        bws = binding.alloc_backward_workspace(lay.desc)
+        gen = torch.Generator(device="cuda").manual_seed(5)
+        gout = (torch.randn(T * K, d, device="cuda", generator=gen) * 0.5).to(torch.bfloat16)
+        dx = torch.empty(T, d, dtype=torch.bfloat16, device="cuda")
+        dw1 = torch.empty(E, h, d, dtype=torch.float32, device="cuda")
+        dw2 = torch.empty(E, d, h, dtype=torch.float32, device="cuda")
+
+        def bwd():
+            binding.moe_grouped_mlp_backward(lay.desc, lay.x, lay.slots, lay.offsets, lay.w1, lay.w2, gout, dx,
+                                             dw1, dw2, bws)
+
+        for _ in range(2):
+            bwd()
+        b_ms = time_calls(bwd, max(3, args.steps // 2))
+        fl = 5 * 2.0 * T * K * d * h
+        tf = fl / (b_ms * 1e-3) / 1e12
+        out["backward"] = {
+            "workload": cfg.name, "entry": "moe_grouped_mlp_backward", "us": round(b_ms * 1e3, 1),
+            "tokens_per_s": round(T / (b_ms * 1e-3), 1),
+            "roofline": {"kernel": "expert-MLP backward: fc1 again, dA, dx, dW2, dW1 products plus transposes",
+                         "bound": "mfma", "achieved": round(tf, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                         "frac": round(tf / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                         "algorithmic_flops_per_launch": fl, "avg_launch_us": round(b_ms * 1e3, 2)},
+        }
+        del bws, gout, dx, dw1, dw2
 
     if not args.no_cpu_baseline:
         import oracle

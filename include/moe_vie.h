@@ -176,6 +176,33 @@ moe_status_t moe_layer_forward(const moe_desc_t *desc, const void *x, const void
                                float *topk_gate_out, void *workspace, size_t workspace_bytes,
                                void *const *events, void *stream);
 
+/* Bytes of device workspace that moe_grouped_mlp_backward needs for `desc`
+ * (bf16 layers with GELU experts). Writes *bytes; validates desc. */
+moe_status_t moe_backward_workspace_size(const moe_desc_t *desc, size_t *bytes);
+
+/* Backward of stage 4 for training (the grouped GEMMs of the paper's training
+ * kernel, with the activation as its own step: App. "MoE Kernel", the
+ * paragraph after Algorithm 1). For every slot n = t*K + j routed to expert
+ * e, with G_n = grad_expert_out[n] (the gradient of expert_out[n]) and
+ * p_n = W1[e] x_t:
+ *   dx[t]  = sum over j of W1[e]^T dH_n      dH_n = (W2[e]^T G_n) * GELU'(p_n)
+ *   dw1[e] = sum over the slots of e of dH_n x_t^T
+ *   dw2[e] = sum over the slots of e of G_n GELU(p_n)^T
+ *   x [T, d], w1 [E, h, d], w2 [E, d, h], grad_expert_out [T*K, d] (slot
+ *   order): layer dtype (bf16); sorted_slots, offsets: as from moe_permute
+ *   dx  [T, d] bf16 out: the K slot gradients summed in fp32 in slot order,
+ *       rounded once
+ *   dw1 [E, h, d] and dw2 [E, d, h] fp32 out; experts with no slots get 0
+ * As in the forward, GELU(p) is rounded to bf16 (dw2 uses that value); dH is
+ * rounded to bf16, the operand of the dx and dw1 products; every product
+ * accumulates in fp32. bf16 layers with GELU experts only (other layers:
+ * MOE_ERR_UNSUPPORTED). Deterministic: no atomics. Uses its own workspace
+ * (moe_backward_workspace_size), 256-byte aligned. */
+moe_status_t moe_grouped_mlp_backward(const moe_desc_t *desc, const void *x, const int32_t *sorted_slots,
+                                      const int32_t *offsets, const void *w1, const void *w2,
+                                      const void *grad_expert_out, void *dx, float *dw1, float *dw2,
+                                      void *workspace, size_t workspace_bytes, void *stream);
+
 /* Rules of moe_bias_update. */
 typedef enum { MOE_BIAS_SIGN = 0, MOE_BIAS_ZSCORE = 1 } moe_bias_rule_t;
 

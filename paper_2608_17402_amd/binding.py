@@ -27,7 +27,8 @@ STATUS = {0: "MOE_OK", 1: "MOE_ERR_INVALID_ARG", 2: "MOE_ERR_UNSUPPORTED", 3: "M
 
 # Public entry points declared in include/moe_vie.h.
 EXPORTS = ("moe_status_string", "moe_last_error", "moe_workspace_size", "moe_route", "moe_permute",
-           "moe_grouped_mlp", "moe_combine", "moe_layer_forward", "moe_bias_update")
+           "moe_grouped_mlp", "moe_combine", "moe_layer_forward", "moe_bias_update", "moe_backward_workspace_size",
+           "moe_grouped_mlp_backward")
 MOE_BIAS_SIGN = 0
 MOE_BIAS_ZSCORE = 1
 
@@ -87,6 +88,10 @@ def load(path: Optional[str] = None):
     lib.moe_layer_forward.restype = st
     lib.moe_bias_update.argtypes = [D, P, P, ctypes.c_float, ctypes.c_int32, P]
     lib.moe_bias_update.restype = st
+    lib.moe_backward_workspace_size.argtypes = [D, ctypes.POINTER(ctypes.c_size_t)]
+    lib.moe_backward_workspace_size.restype = st
+    lib.moe_grouped_mlp_backward.argtypes = [D, P, P, P, P, P, P, P, P, P, P, S, P]
+    lib.moe_grouped_mlp_backward.restype = st
     if path is None:
         _lib = lib
     return lib
@@ -184,6 +189,29 @@ def moe_layer_forward(desc, x, w_router, bias, w1, w2, w1s, w2s, y, topk_idx_out
                                     _ptr(topk_gate_out, "topk_gate_out", torch.float32),
                                     _ptr(workspace, "workspace"), workspace.numel(), ev, _stream(stream)),
            "moe_layer_forward")
+
+
+def backward_workspace_size(desc: MoeDesc) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load().moe_backward_workspace_size(ctypes.byref(desc), ctypes.byref(n)), "moe_backward_workspace_size")
+    return n.value
+
+
+def alloc_backward_workspace(desc: MoeDesc, device="cuda") -> torch.Tensor:
+    return torch.empty(max(backward_workspace_size(desc), 256), dtype=torch.uint8, device=device)
+
+
+def moe_grouped_mlp_backward(desc, x, sorted_slots, offsets, w1, w2, grad_expert_out, dx, dw1, dw2, workspace,
+                             stream=None):
+    """dx [T, d], dw1 [E, h, d] and dw2 [E, d, h] (fp32) of the routed experts
+    from the gradient of their slot-order outputs."""
+    dt = torch_dtype(desc)
+    _check(load().moe_grouped_mlp_backward(
+        ctypes.byref(desc), _ptr(x, "x", dt), _ptr(sorted_slots, "sorted_slots", torch.int32),
+        _ptr(offsets, "offsets", torch.int32), _ptr(w1, "w1", dt), _ptr(w2, "w2", dt),
+        _ptr(grad_expert_out, "grad_expert_out", dt), _ptr(dx, "dx", dt), _ptr(dw1, "dw1", torch.float32),
+        _ptr(dw2, "dw2", torch.float32), _ptr(workspace, "workspace"), workspace.numel() * workspace.element_size(),
+        _stream(stream)), "moe_grouped_mlp_backward")
 
 
 def moe_bias_update(desc, counts, bias, alpha: float, rule: int, stream=None):

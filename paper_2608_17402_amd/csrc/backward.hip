@@ -1,0 +1,174 @@
+// Data-movement kernels of the expert-MLP backward: weight transposes, the
+// per-expert K windows of the weight-gradient products, the transposing gather
+// into those windows, and the per-token sum of the slot gradients. The
+// products themselves run on the MFMA kernels of gemm.hip.
+#include "moe_internal.h"
+
+namespace moe {
+namespace {
+
+constexpr int TT = 64;  // transpose tile (rows x columns)
+
+// out[g][c][r] = in[g][r][c] for a [G][R][C] bf16 tensor (R, C multiples of
+// 64). One 64 x 64 tile per workgroup through LDS: 16-byte row pieces in,
+// 16-byte pieces of the transposed rows out.
+__global__ __launch_bounds__(256) void k_transpose_w(const bf16_t* __restrict__ in, int R, int C,
+                                                    bf16_t* __restrict__ out) {
+    __shared__ bf16_t tile[TT][TT + 2];
+    const int r0 = blockIdx.x * TT, c0 = blockIdx.y * TT;
+    const size_t g = blockIdx.z;
+    const bf16_t* src = in + g * (size_t)R * C;
+    bf16_t* dst = out + g * (size_t)R * C;
+    const int tid = threadIdx.x;
+    for (int q = tid; q < TT * TT / 8; q += 256) {
+        const int r = q / (TT / 8), c = (q % (TT / 8)) * 8;
+        const uint4 v = *reinterpret_cast<const uint4*>(src + (size_t)(r0 + r) * C + c0 + c);
+        const bf16_t* e = reinterpret_cast<const bf16_t*>(&v);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) tile[r][c + k] = e[k];
+    }
+    __syncthreads();
+    for (int q = tid; q < TT * TT / 8; q += 256) {
+        const int c = q / (TT / 8), r = (q % (TT / 8)) * 8;
+        uint4 v;
+        bf16_t* e = reinterpret_cast<bf16_t*>(&v);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) e[k] = tile[r + k][c];
+        *reinterpret_cast<uint4*>(dst + (size_t)(c0 + c) * R + r0 + r) = v;
+    }
+}
+
+// K windows of the weight-gradient products: expert e owns columns
+// koff[e] .. koff[e+1] of the transposed operands, its row count rounded up
+// to a multiple of 64 (the product's K slab). One workgroup; the counts come
+// from the permutation's offsets.
+__global__ __launch_bounds__(1024) void k_window_offsets(const int32_t* __restrict__ offsets, int E,
+                                                        int32_t* __restrict__ koff) {
+    __shared__ int32_t len[kMaxE];
+    for (int e = threadIdx.x; e < E; e += blockDim.x) len[e] = (offsets[e + 1] - offsets[e] + 63) / 64 * 64;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int32_t acc = 0;
+        for (int e = 0; e < E; ++e) {
+            koff[e] = acc;
+            acc += len[e];
+        }
+        koff[E] = acc;
+    }
+}
+
+// Transposing gather into the K windows: out[c][q] for window position q of
+// expert e (q = koff[e] + i) is in[src(offsets[e] + i)][c] when i < count_e,
+// and 0 in the padding up to the window's end. src(p) is p (rows already in
+// sorted order), row_map[p] (slot rows) or row_map[p] / K (token rows).
+// in: [rows, C] bf16, out: [C, ld] bf16, C a multiple of 64. Positions past
+// koff[E] are left alone.
+__global__ __launch_bounds__(256) void k_transpose_window(const bf16_t* __restrict__ in, int C, int mode,
+                                                         const int32_t* __restrict__ row_map, int K,
+                                                         const int32_t* __restrict__ offsets,
+                                                         const int32_t* __restrict__ koff, int E,
+                                                         bf16_t* __restrict__ out, int ld) {
+    __shared__ bf16_t tile[TT][TT + 2];
+    __shared__ int32_t srow[TT];
+    const int q0 = blockIdx.x * TT, c0 = blockIdx.y * TT;
+    const int total = koff[E];
+    if (q0 >= total) return;  // uniform per workgroup
+    const int tid = threadIdx.x;
+    if (tid < TT) {
+        const int q = q0 + tid;
+        int v = -1;
+        if (q < total) {
+            int lo = 0, hi = E - 1;  // last expert with koff[e] <= q
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) / 2;
+                if (koff[mid] <= q) lo = mid;
+                else hi = mid - 1;
+            }
+            const int i = q - koff[lo];
+            if (i < offsets[lo + 1] - offsets[lo]) {
+                const int p = offsets[lo] + i;
+                v = mode == SRC_SORTED ? p : (mode == SRC_SLOT ? row_map[p] : row_map[p] / K);
+            }
+        }
+        srow[tid] = v;
+    }
+    __syncthreads();
+    for (int t = tid; t < TT * TT / 8; t += 256) {
+        const int r = t / (TT / 8), c = (t % (TT / 8)) * 8;
+        uint4 v = make_uint4(0u, 0u, 0u, 0u);
+        if (srow[r] >= 0) v = *reinterpret_cast<const uint4*>(in + (size_t)srow[r] * C + c0 + c);
+        const bf16_t* e = reinterpret_cast<const bf16_t*>(&v);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) tile[r][c + k] = e[k];
+    }
+    __syncthreads();
+    for (int t = tid; t < TT * TT / 8; t += 256) {
+        const int c = t / (TT / 8), r = (t % (TT / 8)) * 8;
+        if (q0 + r >= total) continue;  // total is a multiple of 64: whole pieces
+        uint4 v;
+        bf16_t* e = reinterpret_cast<bf16_t*>(&v);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) e[k] = tile[r + k][c];
+        *reinterpret_cast<uint4*>(out + (size_t)(c0 + c) * ld + q0 + r) = v;
+    }
+}
+
+__device__ __forceinline__ uint32_t pack2_bf16_rne(float lo, float hi) {
+    uint32_t a = __float_as_uint(lo), b = __float_as_uint(hi);
+    a += 0x7fffu + ((a >> 16) & 1u);
+    b += 0x7fffu + ((b >> 16) & 1u);
+    return (a >> 16) | (b & 0xffff0000u);
+}
+
+// dx[t, :] = bf16(sum_j dxs[t K + j, :]) in slot order (fp32 sums), 4 columns
+// per thread.
+__global__ __launch_bounds__(256) void k_slot_sum(const float* __restrict__ dxs, int T, int K, int d,
+                                                 bf16_t* __restrict__ dx) {
+    const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int q = d / 4;
+    if (i >= (size_t)T * q) return;
+    const size_t t = i / q;
+    const int c = (int)(i % q) * 4;
+    float4 acc = *reinterpret_cast<const float4*>(dxs + (t * K) * d + c);
+    for (int j = 1; j < K; ++j) {
+        const float4 v = *reinterpret_cast<const float4*>(dxs + (t * K + j) * d + c);
+        acc.x += v.x;
+        acc.y += v.y;
+        acc.z += v.z;
+        acc.w += v.w;
+    }
+    uint2 o;
+    o.x = pack2_bf16_rne(acc.x, acc.y);
+    o.y = pack2_bf16_rne(acc.z, acc.w);
+    *reinterpret_cast<uint2*>(dx + t * d + c) = o;
+}
+
+}  // namespace
+
+hipError_t launch_transpose_w(const void* in, int G, int R, int C, void* out, hipStream_t s) {
+    hipLaunchKernelGGL(k_transpose_w, dim3(R / TT, C / TT, G), dim3(256), 0, s, static_cast<const bf16_t*>(in), R,
+                       C, static_cast<bf16_t*>(out));
+    return hipGetLastError();
+}
+
+hipError_t launch_window_offsets(const int32_t* offsets, int E, int32_t* koff, hipStream_t s) {
+    hipLaunchKernelGGL(k_window_offsets, dim3(1), dim3(1024), 0, s, offsets, E, koff);
+    return hipGetLastError();
+}
+
+hipError_t launch_transpose_window(const void* in, int C, int mode, const int32_t* row_map, int K,
+                                   const int32_t* offsets, const int32_t* koff, int E, void* out, int ld,
+                                   hipStream_t s) {
+    hipLaunchKernelGGL(k_transpose_window, dim3(ld / TT, C / TT), dim3(256), 0, s, static_cast<const bf16_t*>(in),
+                       C, mode, row_map, K, offsets, koff, E, static_cast<bf16_t*>(out), ld);
+    return hipGetLastError();
+}
+
+hipError_t launch_slot_sum(const float* dxs, int T, int K, int d, void* dx, hipStream_t s) {
+    const size_t n = (size_t)T * (d / 4);
+    hipLaunchKernelGGL(k_slot_sum, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, dxs, T, K, d,
+                       static_cast<bf16_t*>(dx));
+    return hipGetLastError();
+}
+
+}  // namespace moe

@@ -109,12 +109,53 @@ __device__ __forceinline__ float swiglu_col(float g, float u, bool valid) {
     return valid ? silu_as(g) * u : 0.0f;
 }
 
+// Tile of workgroup `b` in the weight-gradient product: groups x (M / bm)
+// row tiles x (N / bn) column tiles, dense (every tile exists), in the same
+// XCD-aware order as locate_tile. M = a.dense_rows.
+__device__ __forceinline__ TileCoord locate_wgrad_tile(const GemmArgs& a, int bm, int bn) {
+    TileCoord tc;
+    tc.valid = false;
+    const int n_n = a.N / bn;
+    const int m_per = a.dense_rows / bm;
+    const int total = a.groups * m_per * n_n;
+    const int per = (total + kNumXcd - 1) / kNumXcd;
+    const int b = blockIdx.x;
+    const int j = b / kNumXcd;
+    if (j >= per) return tc;
+    const int lid = (b % kNumXcd) * per + j;
+    if (lid >= total) return tc;
+    const int mt = lid / n_n;
+    tc.n0 = (lid - mt * n_n) * bn;
+    tc.e = mt / m_per;
+    tc.row0 = (mt - tc.e * m_per) * bm;
+    tc.rows = bm;
+    tc.valid = true;
+    return tc;
+}
+
 // Weight rows a tile may read: the group's rows (B rows past b_rows, when
 // set, read as zeros through the buffer-resource bound).
 __device__ __forceinline__ int weight_rows(const GemmArgs& a) { return a.b_rows > 0 ? a.b_rows : a.N; }
 
 // Epilogues of a first expert layer: their token rows are gathered from x.
 __host__ __device__ constexpr bool fc1_epi(int epi) { return epi == EPI_GELU_STORE || epi == EPI_SWIGLU_STORE; }
+
+// d/dx GELU(x) = Phi(x) + x phi(x) from the same approximation: Q =
+// erfc(|x| / sqrt 2) / 2 as in gelu_as, Phi(x) = 1 - Q for x >= 0 and Q
+// otherwise; phi(x) = exp(-x^2 / 2) / sqrt(2 pi).
+__device__ __forceinline__ float gelu_grad_as(float x) {
+    const float ax = fabsf(x);
+    const float t = __builtin_amdgcn_rcpf(fmaf(0.23164189f, ax, 1.0f));
+    float q = fmaf(0.5307027f, t, -0.72657603f);
+    q = fmaf(q, t, 0.7107069f);
+    q = fmaf(q, t, -0.14224836f);
+    q = fmaf(q, t, 0.1274148f);
+    q *= t;
+    const float e = __builtin_amdgcn_exp2f((x * -0.7213475f) * x);
+    const float qe = q * e;
+    const float phi_cdf = x >= 0.0f ? 1.0f - qe : qe;
+    return fmaf(x * 0.39894228f, e, phi_cdf);
+}
 
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
@@ -223,20 +264,26 @@ void k_gemm_bf16(const GemmArgs a) {
     static_assert(STAGES >= 2 && STAGES <= 5, "2 to 5 stages");
     __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES * STAGE];
     __shared__ int32_t srow[BM];
-    const TileCoord tc = locate_tile<GROUPED>(a, BM, BN);
+    constexpr bool WGRAD = EPI == EPI_WGRAD_F32;
+    // A rows gathered through the row map (first layers, the backward's dA).
+    constexpr bool A_GATHER = fc1_epi(EPI) || EPI == EPI_GELU_BWD || EPI == EPI_DGELU;
+    // Output rows scattered to slot order (second layer, the backward's dx).
+    constexpr bool O_SCATTER = EPI == EPI_SCATTER_SLOT || EPI == EPI_SCATTER_SLOT_F32;
+    const TileCoord tc = WGRAD ? locate_wgrad_tile(a, BM, BN) : locate_tile<GROUPED>(a, BM, BN);
     if (!tc.valid) return;
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
     const int wave = tid / kWave;
     const int wm = wave / WAVES_N, wn = wave % WAVES_N;
 
-    // Row ids: gathered token rows (fc1 of routed experts) or output slots (fc2).
+    // Row ids: gathered operand rows, or output slots.
     for (int r = tid; r < BM; r += NT) {
         const int rr = r < tc.rows ? r : tc.rows - 1;  // pad rows repeat the last valid row
         const int p = tc.row0 + rr;
         int v = p;
-        if (fc1_epi(EPI) && a.row_mode == ROWS_GATHER_TOKENS) v = a.row_map[p] / a.route_k;
-        if (EPI == EPI_SCATTER_SLOT) v = a.row_map[p];
+        if (A_GATHER && a.row_mode == ROWS_GATHER_TOKENS) v = a.row_map[p] / a.route_k;
+        if (A_GATHER && a.row_mode == ROWS_GATHER_SLOTS) v = a.row_map[p];
+        if (O_SCATTER) v = a.row_map[p];
         srow[r] = v;
     }
     __syncthreads();
@@ -261,7 +308,7 @@ void k_gemm_bf16(const GemmArgs a) {
         const int r = sl / CPR, pch = sl % CPR;
         const int c = pch ^ ((r >> SWZ_SHIFT) & SWZ_MASK);
         int xrow;
-        if (fc1_epi(EPI)) xrow = srow[r];
+        if (A_GATHER) xrow = srow[r];
         else xrow = tc.row0 + (r < tc.rows ? r : tc.rows - 1);
         xv[i] = (uint32_t)xrow * (uint32_t)(Kd * 2) + c * 16;
     }
@@ -305,11 +352,18 @@ void k_gemm_bf16(const GemmArgs a) {
         xoff[ks] = base + (wm * WTM) * ROWB + k;
         woff[ks] = base + BM * ROWB + (wn * WTN) * ROWB + k;
     }
-    const int nk = Kd / BK;
+    // K range: the whole row, or (weight gradients) the group's window.
+    int nk = Kd / BK;
+    uint32_t kbase = 0;
+    if (WGRAD) {
+        const int k0 = a.koff[tc.e], k1 = a.koff[tc.e + 1];
+        nk = (k1 - k0) / BK;
+        kbase = (uint32_t)k0 * 2;
+    }
 
     auto issue = [&](int stage, int kslab) {
         uint8_t* buf = smem + stage * STAGE;
-        const uint32_t soff = (uint32_t)kslab * BK * 2;
+        const uint32_t soff = kbase + (uint32_t)kslab * BK * 2;
 #pragma unroll
         for (int i = 0; i < AP; ++i) copy16_to_lds(xres, xv[i], soff, buf + (wave + NW * i) * 1024);
 #pragma unroll
@@ -378,7 +432,7 @@ void k_gemm_bf16(const GemmArgs a) {
     // written to the wave's own LDS area row by row (rows padded by 16 bytes
     // so the 32 rows of one write spread over the banks), then read back as
     // 16-byte row pieces so that consecutive lanes store whole 128-byte lines.
-    constexpr bool OUT_F32 = EPI == EPI_STORE_F32;
+    constexpr bool OUT_F32 = EPI == EPI_STORE_F32 || EPI == EPI_SCATTER_SLOT_F32 || WGRAD;
     constexpr int OES = OUT_F32 ? 4 : 2;           // output element size
     constexpr int SEG = (SWIGLU ? HW : WTN) * OES; // bytes of one wave-tile row
     constexpr int RSTR = SEG + 16;                 // padded LDS row stride
@@ -418,8 +472,15 @@ void k_gemm_bf16(const GemmArgs a) {
                     if (OUT_F32) {
                         *reinterpret_cast<float4*>(dst) = make_float4(v0, v1, v2, v3);
                     } else {
-                        if (EPI == EPI_GELU_STORE) {
+                        if (EPI == EPI_GELU_STORE || EPI == EPI_GELU_BWD) {
                             v0 = gelu_as(v0); v1 = gelu_as(v1); v2 = gelu_as(v2); v3 = gelu_as(v3);
+                        }
+                        if (EPI == EPI_DGELU) {  // times the stored GELU' of the same element
+                            const int r = wm * WTM + i * 32 + fr;
+                            const size_t p = (size_t)(tc.row0 + (r < tc.rows ? r : tc.rows - 1));
+                            const float4 f = *reinterpret_cast<const float4*>(
+                                static_cast<const float*>(a.aux) + p * a.N + ocol0 + j * 32 + 8 * g + 4 * fk);
+                            v0 *= f.x; v1 *= f.y; v2 *= f.z; v3 *= f.w;
                         }
                         *reinterpret_cast<uint2*>(dst) = pack4_bf16(v0, v1, v2, v3);
                     }
@@ -434,12 +495,43 @@ void k_gemm_bf16(const GemmArgs a) {
             const int r = wm * WTM + i * 32 + rr;
             const uint4 v = *reinterpret_cast<const uint4*>(stg + rr * RSTR + pc * 16);
             if (r < tc.rows && (!SWIGLU || ocol0 < a.act_ld)) {
-                const size_t orow = EPI == EPI_SCATTER_SLOT ? (size_t)srow[r] : (size_t)(tc.row0 + r);
+                size_t orow = O_SCATTER ? (size_t)srow[r] : (size_t)(tc.row0 + r);
+                if (WGRAD) orow += (size_t)tc.e * a.dense_rows;
                 uint8_t* out = static_cast<uint8_t*>(a.C) + (orow * ostride + ocol0) * OES + pc * 16;
                 *reinterpret_cast<uint4*>(out) = v;
             }
         }
         wave_sync_lds();
+    }
+    if constexpr (EPI == EPI_GELU_BWD) {
+        // Second output: GELU'(acc) in fp32 (rows of N), the same staging.
+        constexpr int SEG2 = WTN * 4, RSTR2 = SEG2 + 16, CPRO2 = SEG2 / 16, PIECES2 = 32 * CPRO2 / kWave;
+        static_assert(NW * 32 * RSTR2 <= STAGES * STAGE, "epilogue staging must fit in the stage buffers");
+        __syncthreads();  // the wider rows overlap other waves' first-pass areas
+        uint8_t* stg2 = smem + wave * 32 * RSTR2;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int g = 0; g < 4; ++g)
+                    *reinterpret_cast<float4*>(stg2 + fr * RSTR2 + (j * 32 + 8 * g + 4 * fk) * 4) =
+                        make_float4(gelu_grad_as(acc[j][i][4 * g + 0]), gelu_grad_as(acc[j][i][4 * g + 1]),
+                                    gelu_grad_as(acc[j][i][4 * g + 2]), gelu_grad_as(acc[j][i][4 * g + 3]));
+            wave_sync_lds();
+#pragma unroll
+            for (int k = 0; k < PIECES2; ++k) {
+                const int q = lane + kWave * k;
+                const int rr = q / CPRO2, pc = q % CPRO2;
+                const int r = wm * WTM + i * 32 + rr;
+                const uint4 v = *reinterpret_cast<const uint4*>(stg2 + rr * RSTR2 + pc * 16);
+                if (r < tc.rows) {
+                    uint8_t* out = static_cast<uint8_t*>(a.C2) + ((size_t)(tc.row0 + r) * a.N + ocol0) * 4 + pc * 16;
+                    *reinterpret_cast<uint4*>(out) = v;
+                }
+            }
+            wave_sync_lds();
+        }
     }
 }
 
@@ -1440,6 +1532,20 @@ hipError_t dispatch_bf16(int bm, const GemmArgs& a, hipStream_t s) {
     return hipErrorInvalidValue;
 }
 
+// Backward products: always the tiled kernel (256- or 64-row tiles).
+template <int EPI, bool GROUPED>
+hipError_t dispatch_tiled(int bm, const GemmArgs& a, hipStream_t s) {
+    if (bm == 256) {
+        if (a.N % 128 == 0) return launch_bf16<256, 128, 2, 2, 64, 2, 1, EPI, GROUPED>(a, s);
+        return launch_bf16<256, 64, 4, 1, 64, 2, 1, EPI, GROUPED>(a, s);
+    }
+    if (bm == 64) {
+        if (a.N % 128 == 0) return launch_bf16<64, 128, 1, 4, 64, 3, 2, EPI, GROUPED>(a, s);
+        return launch_bf16<64, 64, 2, 2, 64, 3, 2, EPI, GROUPED>(a, s);
+    }
+    return hipErrorInvalidValue;
+}
+
 // SwiGLU first layer: the virtual column count N follows from the tile shape
 // (each tile of BN columns computes BN / 2 activation columns).
 template <bool GROUPED>
@@ -1463,6 +1569,19 @@ hipError_t dispatch(const moe_desc_t& d, int epilogue, int bm, const GemmArgs& a
         switch (epilogue) {
             case EPI_GELU_STORE: return dispatch_bf16<EPI_GELU_STORE, GROUPED>(bm, a, s);
             case EPI_SWIGLU_STORE: return dispatch_swiglu<GROUPED>(bm, a, s);
+            case EPI_GELU_BWD:
+                if (GROUPED) return dispatch_tiled<EPI_GELU_BWD, true>(bm, a, s);
+                break;
+            case EPI_DGELU:
+                if (GROUPED) return dispatch_tiled<EPI_DGELU, true>(bm, a, s);
+                break;
+            case EPI_SCATTER_SLOT_F32:
+                if (GROUPED) return dispatch_tiled<EPI_SCATTER_SLOT_F32, true>(bm, a, s);
+                break;
+            case EPI_WGRAD_F32:
+                if (!GROUPED && a.koff && a.groups > 0 && a.dense_rows % bm == 0)
+                    return dispatch_tiled<EPI_WGRAD_F32, false>(bm, a, s);
+                break;
             case EPI_SCATTER_SLOT:
                 if (GROUPED) return dispatch_bf16<EPI_SCATTER_SLOT, true>(bm, a, s);
                 break;

@@ -69,6 +69,20 @@ moe_status_t check_desc(const moe_desc_t* d) {
     return MOE_OK;
 }
 
+// The backward supports bf16 layers with GELU experts; its transposed
+// operands and slot gradients are addressed through 32-bit buffer offsets.
+moe_status_t check_backward_desc(const moe_desc_t* d) {
+    const moe_status_t st = check_desc(d);
+    if (st != MOE_OK) return st;
+    if (d->dtype != MOE_BF16) return fail(MOE_ERR_UNSUPPORTED, "the backward needs a bf16 layer");
+    if (d->flags & MOE_FLAG_SWIGLU) return fail(MOE_ERR_UNSUPPORTED, "the backward supports GELU experts only");
+    const uint64_t lim = (uint64_t)1 << 32, TK = (uint64_t)d->T * d->K;
+    const uint64_t ld = TK + 64 * (uint64_t)d->E + 64;
+    if (TK * d->d * 2 >= lim || (uint64_t)(d->d > d->h ? d->d : d->h) * ld * 2 >= lim)
+        return fail(MOE_ERR_UNSUPPORTED, "the backward's slot or transposed operands exceed 4 GiB");
+    return MOE_OK;
+}
+
 moe_status_t check_ptr(const void* p, const char* name, bool nullable = false) {
     if (!p) {
         if (nullable) return MOE_OK;
@@ -151,6 +165,31 @@ WorkspacePlan plan_workspace(const moe_desc_t& d) {
     p.sout = take(d.h_shared ? (size_t)d.T * d.d * 4 : 0);
     p.total = off;
     return p;
+}
+
+BackwardPlan plan_backward(const moe_desc_t& d) {
+    BackwardPlan b;
+    b.fwd = plan_workspace(d);
+    const size_t TK = (size_t)d.T * d.K;
+    b.ld = (int32_t)((TK + 64 * (size_t)d.E + 63) / 64 * 64);
+    size_t off = b.fwd.total;
+    auto take = [&](size_t bytes) {
+        const size_t o = off;
+        off = align_up(off + bytes);
+        return o;
+    };
+    b.dgelu = take(TK * d.h * 4);
+    b.w1t = take((size_t)d.E * d.h * d.d * 2);
+    b.w2t = take((size_t)d.E * d.h * d.d * 2);
+    b.dh = take(TK * d.h * 2);
+    b.dxs = take(TK * d.d * 4);
+    b.koff = take(((size_t)d.E + 1) * 4);
+    b.gt = take((size_t)d.d * b.ld * 2);
+    b.at = take((size_t)d.h * b.ld * 2);
+    b.dht = take((size_t)d.h * b.ld * 2);
+    b.xt = take((size_t)d.d * b.ld * 2);
+    b.total = off;
+    return b;
 }
 
 static bool fast_router(const moe_desc_t& d) { return d.dtype == MOE_BF16 && !(d.flags & MOE_FLAG_EXACT_ROUTER); }
@@ -281,6 +320,105 @@ static moe_status_t enqueue_shared_mlp(const moe_desc_t& d, const WorkspacePlan&
         return MOE_OK;
     }
     HIP_CHECK(launch_gemm(d, EPI_STORE_F32, bm, g2, s), "shared fc2 gemm");
+    return MOE_OK;
+}
+
+// Backward of the routed experts (GELU, bf16): recompute fc1 keeping GELU',
+// dH = (G W2) * GELU' with G the output gradients gathered by slot, the slot
+// gradients of x dH W1 (fp32, slot order) summed per token, and the weight
+// gradients as K-windowed products of transposed operands.
+static moe_status_t enqueue_backward(const moe_desc_t& d, const BackwardPlan& b, void* ws, const void* x,
+                                     const int32_t* sorted_slots, const int32_t* offsets, const void* w1,
+                                     const void* w2, const void* gout, void* dx, float* dw1, float* dw2,
+                                     hipStream_t s) {
+    const WorkspacePlan& p = b.fwd;
+    const size_t TK = (size_t)d.T * d.K;
+    TileDesc* tiles = region<TileDesc>(ws, p.tiles);
+    int32_t* ntiles = region<int32_t>(ws, p.ntiles);
+    void* act = region<void>(ws, p.act);
+    float* dgelu = region<float>(ws, b.dgelu);
+    void* w1t = region<void>(ws, b.w1t);
+    void* w2t = region<void>(ws, b.w2t);
+    void* dh = region<void>(ws, b.dh);
+    float* dxs = region<float>(ws, b.dxs);
+    int32_t* koff = region<int32_t>(ws, b.koff);
+    HIP_CHECK(launch_build_tiles(d.E, p.tile_bm, p.max_tiles, offsets, tiles, ntiles, s), "build_tiles");
+    HIP_CHECK(launch_transpose_w(w1, d.E, d.h, d.d, w1t, s), "transpose w1");
+    HIP_CHECK(launch_transpose_w(w2, d.E, d.d, d.h, w2t, s), "transpose w2");
+
+    GemmArgs g{};  // fc1 again: the activation (bf16) and GELU' (fp32)
+    g.A = x;
+    g.B = w1;
+    g.C = act;
+    g.C2 = dgelu;
+    g.row_map = sorted_slots;
+    g.tiles = tiles;
+    g.n_tiles = ntiles;
+    g.N = d.h;
+    g.Kdim = d.d;
+    g.route_k = d.K;
+    g.row_mode = ROWS_GATHER_TOKENS;
+    g.max_tiles = p.max_tiles;
+    g.b_group_stride = (int64_t)d.h * d.d;
+    g.a_bytes = (uint32_t)((size_t)d.T * d.d * 2);
+    HIP_CHECK(launch_gemm(d, EPI_GELU_BWD, p.tile_bm, g, s), "backward fc1");
+
+    GemmArgs ga = g;  // dH = (G W2) * GELU'
+    ga.A = gout;
+    ga.B = w2t;
+    ga.C = dh;
+    ga.C2 = nullptr;
+    ga.aux = dgelu;
+    ga.row_mode = ROWS_GATHER_SLOTS;
+    ga.a_bytes = (uint32_t)(TK * d.d * 2);
+    HIP_CHECK(launch_gemm(d, EPI_DGELU, p.tile_bm, ga, s), "backward dA");
+
+    GemmArgs gx = g;  // slot gradients of x: dH W1, fp32 to slot order
+    gx.A = dh;
+    gx.B = w1t;
+    gx.C = dxs;
+    gx.C2 = nullptr;
+    gx.N = d.d;
+    gx.Kdim = d.h;
+    gx.row_mode = ROWS_IDENTITY;
+    gx.a_bytes = (uint32_t)(TK * d.h * 2);
+    HIP_CHECK(launch_gemm(d, EPI_SCATTER_SLOT_F32, p.tile_bm, gx, s), "backward dx");
+    HIP_CHECK(launch_slot_sum(dxs, d.T, d.K, d.d, dx, s), "slot sum");
+
+    // Weight gradients: transposed operands in per-expert K windows.
+    void* gt = region<void>(ws, b.gt);
+    void* at = region<void>(ws, b.at);
+    void* dht = region<void>(ws, b.dht);
+    void* xt = region<void>(ws, b.xt);
+    HIP_CHECK(launch_window_offsets(offsets, d.E, koff, s), "window offsets");
+    HIP_CHECK(launch_transpose_window(gout, d.d, SRC_SLOT, sorted_slots, d.K, offsets, koff, d.E, gt, b.ld, s),
+              "transpose G");
+    HIP_CHECK(launch_transpose_window(act, d.h, SRC_SORTED, sorted_slots, d.K, offsets, koff, d.E, at, b.ld, s),
+              "transpose A");
+    HIP_CHECK(launch_transpose_window(dh, d.h, SRC_SORTED, sorted_slots, d.K, offsets, koff, d.E, dht, b.ld, s),
+              "transpose dH");
+    HIP_CHECK(launch_transpose_window(x, d.d, SRC_TOKEN, sorted_slots, d.K, offsets, koff, d.E, xt, b.ld, s),
+              "transpose x");
+    auto wgrad = [&](const void* pa, int m, const void* pb, int n, float* out, const char* what) -> moe_status_t {
+        GemmArgs w{};
+        w.A = pa;
+        w.B = pb;
+        w.C = out;
+        w.dense_rows = m;
+        w.N = n;
+        w.Kdim = b.ld;
+        w.route_k = 1;
+        w.row_mode = ROWS_IDENTITY;
+        w.koff = koff;
+        w.groups = d.E;
+        const int bm = m % 256 == 0 ? 256 : 64;
+        w.max_tiles = d.E * (m / bm);
+        w.a_bytes = (uint32_t)((size_t)m * b.ld * 2);
+        HIP_CHECK(launch_gemm(d, EPI_WGRAD_F32, bm, w, s), what);
+        return MOE_OK;
+    };
+    CHECK(wgrad(gt, d.d, at, d.h, dw2, "dW2"));
+    CHECK(wgrad(dht, d.h, xt, d.d, dw1, "dW1"));
     return MOE_OK;
 }
 
@@ -419,6 +557,39 @@ MOE_API moe_status_t moe_layer_forward(const moe_desc_t* desc, const void* x, co
         CHECK(enqueue_shared_mlp(d, p, workspace, x, w1s, w2s, sout, s, &c, &fused));
     }
     if (!fused) HIP_CHECK(launch_combine(d, eout, gate, sout, 1, y, s), "combine");
+    return ok();
+}
+
+MOE_API moe_status_t moe_backward_workspace_size(const moe_desc_t* desc, size_t* bytes) {
+    CHECK(check_backward_desc(desc));
+    if (!bytes) return fail(MOE_ERR_INVALID_ARG, "bytes is NULL");
+    *bytes = plan_backward(*desc).total;
+    return ok();
+}
+
+MOE_API moe_status_t moe_grouped_mlp_backward(const moe_desc_t* desc, const void* x, const int32_t* sorted_slots,
+                                              const int32_t* offsets, const void* w1, const void* w2,
+                                              const void* grad_expert_out, void* dx, float* dw1, float* dw2,
+                                              void* workspace, size_t workspace_bytes, void* stream) {
+    CHECK(check_backward_desc(desc));
+    CHECK(check_ptr(x, "x"));
+    CHECK(check_ptr(sorted_slots, "sorted_slots"));
+    CHECK(check_ptr(offsets, "offsets"));
+    CHECK(check_ptr(w1, "w1"));
+    CHECK(check_ptr(w2, "w2"));
+    CHECK(check_ptr(grad_expert_out, "grad_expert_out"));
+    CHECK(check_ptr(dx, "dx"));
+    CHECK(check_ptr(dw1, "dw1"));
+    CHECK(check_ptr(dw2, "dw2"));
+    const BackwardPlan b = plan_backward(*desc);
+    if (!workspace) return fail(MOE_ERR_WORKSPACE, "workspace is NULL (need %zu bytes)", b.total);
+    if (reinterpret_cast<uintptr_t>(workspace) & 255u)
+        return fail(MOE_ERR_INVALID_ARG, "workspace is not 256-byte aligned");
+    if (workspace_bytes < b.total)
+        return fail(MOE_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, b.total);
+    (void)hipGetLastError();
+    CHECK(enqueue_backward(*desc, b, workspace, x, sorted_slots, offsets, w1, w2, grad_expert_out, dx, dw1, dw2,
+                           static_cast<hipStream_t>(stream)));
     return ok();
 }
 

@@ -32,6 +32,7 @@ struct TileDesc {
 enum GemmRowMode : int {
     ROWS_GATHER_TOKENS = 0,  // A row of sorted position p is x[sorted_slots[p] / K]
     ROWS_IDENTITY = 1,       // A row of position p is row p
+    ROWS_GATHER_SLOTS = 2,   // A row of sorted position p is row sorted_slots[p] (slot order)
 };
 
 enum GemmEpilogue : int {
@@ -44,6 +45,13 @@ enum GemmEpilogue : int {
                             // act_ld (C's row stride): B holds per group the act_n gate rows, then
                             // the act_n up rows. The launcher sets N: a tile of BN columns computes
                             // BN / 2 activation columns from the matching gate and up rows
+    // Backward of GELU experts (tiled kernel only):
+    EPI_GELU_BWD = 5,       // C[p, :] = bf16(GELU(acc)) and C2[p, :] = GELU'(acc) (fp32), sorted order
+    EPI_DGELU = 6,          // C[p, :] = bf16(acc * aux[p, :]) (aux fp32 [rows, N]), sorted order
+    EPI_SCATTER_SLOT_F32 = 7,  // C[sorted_slots[p], :] = acc as fp32
+    EPI_WGRAD_F32 = 8,      // C[e][m, :] = sum over expert e's window of the K axis (fp32): the weight
+                            // gradients. A [dense_rows, Kdim] and B [N, Kdim] are shared by all groups;
+                            // group e reads columns koff[e] .. koff[e+1] (multiples of 64)
 };
 
 struct GemmArgs {
@@ -62,6 +70,10 @@ struct GemmArgs {
     int64_t b_group_stride;    // elements between consecutive experts' weights
     int32_t b_rows;            // dense bf16 only: rows of B that exist (0 = N); rows past them read as zeros
     uint32_t a_bytes;          // bytes of the A operand buffer (bounds of its buffer resource)
+    void* C2;                  // EPI_GELU_BWD: second output (fp32)
+    const void* aux;           // EPI_DGELU: per-element factor (fp32, rows of N)
+    const int32_t* koff;       // EPI_WGRAD_F32: [groups + 1] K-window starts
+    int32_t groups;            // EPI_WGRAD_F32: number of groups (experts)
     int32_t act_n;             // EPI_SWIGLU_STORE: activation width h (valid columns)
     int32_t act_ld;            // EPI_SWIGLU_STORE: activation row stride (h rounded up to 128)
     const float* gate;         // EPI_COMBINE: gates [rows, route_k]
@@ -82,6 +94,21 @@ struct WorkspacePlan {
 
 size_t elem_size(int32_t dtype);
 WorkspacePlan plan_workspace(const moe_desc_t& d);
+
+// Workspace of the expert-MLP backward: the forward plan (tile table,
+// activation), then the backward's own regions.
+struct BackwardPlan {
+    WorkspacePlan fwd;
+    size_t dgelu;            // GELU'(W1 x) [T*K, h] fp32, sorted order
+    size_t w1t, w2t;         // transposed weights [E, d, h] and [E, h, d]
+    size_t dh;               // pre-activation gradient [T*K, h] bf16, sorted order
+    size_t dxs;              // slot gradients of x [T*K, d] fp32, slot order
+    size_t koff;             // [E + 1] K-window starts
+    size_t gt, at, dht, xt;  // transposed operands [d | h, ld] bf16
+    int32_t ld;              // their row length: T*K + 64 E, rounded up to 64
+    size_t total;
+};
+BackwardPlan plan_backward(const moe_desc_t& d);
 // M-tile height of the grouped GEMM for groups of `avg_rows` rows on average.
 int gemm_tile_bm(int32_t dtype, int64_t avg_rows);
 // Row stride of an expert activation of hidden width h: h itself for GELU
@@ -116,6 +143,15 @@ hipError_t launch_build_tiles(int32_t E, int32_t bm, int32_t max_tiles, const in
 hipError_t launch_gemm(const moe_desc_t& d, int epilogue, int bm, const GemmArgs& a, hipStream_t s);
 // Whether launch_gemm(EPI_COMBINE) supports this dense GEMM (M-tile bm, N columns, K = kdim).
 bool gemm_combine_fusable(const moe_desc_t& d, int bm, int n, int kdim);
+// Backward data movement (backward.hip). Row sources of the transposing
+// gather: rows already in sorted order, slot rows, token rows.
+enum TransposeSource : int { SRC_SORTED = 0, SRC_SLOT = 1, SRC_TOKEN = 2 };
+hipError_t launch_transpose_w(const void* in, int G, int R, int C, void* out, hipStream_t s);
+hipError_t launch_window_offsets(const int32_t* offsets, int E, int32_t* koff, hipStream_t s);
+hipError_t launch_transpose_window(const void* in, int C, int mode, const int32_t* row_map, int K,
+                                   const int32_t* offsets, const int32_t* koff, int E, void* out, int ld,
+                                   hipStream_t s);
+hipError_t launch_slot_sum(const float* dxs, int T, int K, int d, void* dx, hipStream_t s);
 hipError_t launch_bias_update(int32_t E, const int32_t* counts, float* bias, float alpha, int32_t rule,
                               hipStream_t s);
 hipError_t launch_combine(const moe_desc_t& d, const void* expert_out, const float* gate,

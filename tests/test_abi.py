@@ -146,3 +146,26 @@ def test_bias_update_rejects_bad_arguments(lib):
     assert b"rule" in lib.moe_last_error()
     bad = binding.make_desc(100, 64, 8, 0, 64)
     assert lib.moe_bias_update(ctypes.byref(bad), fake, fake, ctypes.c_float(0.1), 0, None) == 1
+
+
+def test_backward_validation(lib):
+    n = ctypes.c_size_t(0)
+    ok = binding.make_desc(1000, 256, 8, 2, 192, 0, 1.0, "bf16")
+    assert lib.moe_backward_workspace_size(ctypes.byref(ok), ctypes.byref(n)) == 0
+    # at least the transposed operands: (2 d + 2 h) x (T*K + 64 E) bf16
+    assert n.value >= (2 * 256 + 2 * 192) * (2000 + 64 * 8) * 2
+    f32 = binding.make_desc(1000, 256, 8, 2, 192, 0, 1.0, "f32")
+    sw = binding.make_desc(1000, 256, 8, 2, 192, 0, 1.0, "bf16", flags=binding.MOE_FLAG_SWIGLU)
+    for desc in (f32, sw):
+        assert lib.moe_backward_workspace_size(ctypes.byref(desc), ctypes.byref(n)) == 2
+        assert lib.moe_last_error() != b""
+    P, S = ctypes.c_void_p, ctypes.c_size_t
+    fake = P(1 << 20)
+    d = ctypes.byref(ok)
+    assert lib.moe_grouped_mlp_backward(d, fake, fake, fake, fake, fake, None, fake, fake, fake, fake, S(1 << 40),
+                                        None) == 1
+    assert b"grad_expert_out is NULL" in lib.moe_last_error()
+    assert lib.moe_grouped_mlp_backward(d, fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, S(256),
+                                        None) == 3
+    assert lib.moe_grouped_mlp_backward(d, fake, fake, fake, fake, fake, fake, fake, fake, P((1 << 20) + 8),
+                                        fake, S(1 << 40), None) == 1
