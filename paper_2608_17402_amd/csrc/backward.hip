@@ -1,6 +1,7 @@
 // Data-movement kernels of the expert-MLP backward: weight transposes, the
-// per-expert K windows of the weight-gradient products, the transposing gather
-// into those windows, and the per-token sum of the slot gradients. The
+// plan of the weight-gradient products (per-expert K windows cut into work
+// items) and the sum of their partial blocks, the transposing gather into the
+// windows, and the per-token sum of the slot gradients. The
 // products themselves run on the MFMA kernels of gemm.hip.
 #include "moe_internal.h"
 
@@ -38,31 +39,88 @@ __global__ __launch_bounds__(256) void k_transpose_w(const bf16_t* __restrict__ 
     }
 }
 
-// K windows of the weight-gradient products: expert e owns columns
-// koff[e] .. koff[e+1] of the transposed operands, its row count rounded up
-// to a multiple of 64 (the product's K slab). One workgroup; the counts come
-// from the permutation's offsets.
-__global__ __launch_bounds__(1024) void k_window_offsets(const int32_t* __restrict__ offsets, int E,
-                                                        int32_t* __restrict__ koff) {
-    __shared__ int32_t len[kMaxE];
-    for (int e = threadIdx.x; e < E; e += blockDim.x) len[e] = (offsets[e + 1] - offsets[e] + 63) / 64 * 64;
+// Plan of the weight-gradient products, one workgroup:
+//  - K windows: expert e owns columns koff[e] .. koff[e+1] of the transposed
+//    operands, its row count rounded up to a multiple of 64 (the K slab);
+//  - work items: each window cut into pieces of at most kWgradSlabs slabs, so
+//    that no tile runs much longer than the others under a skewed load. An
+//    expert with one piece (or none: an empty expert gets one item of length
+//    0, which writes zeros) writes its gradient directly (dest = -1); the
+//    pieces of a longer window write partial blocks dest = first .. first +
+//    n - 1, summed afterwards in that order;
+//  - rlist: the split experts {e, first partial block, pieces}.
+// wcount[0] = items, wcount[1] = split experts.
+__global__ __launch_bounds__(1024) void k_wgrad_plan(const int32_t* __restrict__ offsets, int E,
+                                                    int32_t* __restrict__ koff, TileDesc* __restrict__ items,
+                                                    TileDesc* __restrict__ rlist, int32_t* __restrict__ wcount) {
+    __shared__ int32_t len[kMaxE], pieces[kMaxE], ifirst[kMaxE], pfirst[kMaxE], rslot[kMaxE];
+    constexpr int CHUNK = kWgradSlabs * 64;
+    for (int e = threadIdx.x; e < E; e += blockDim.x) {
+        len[e] = (offsets[e + 1] - offsets[e] + 63) / 64 * 64;
+        pieces[e] = len[e] > CHUNK ? (len[e] + CHUNK - 1) / CHUNK : 1;
+    }
     __syncthreads();
     if (threadIdx.x == 0) {
-        int32_t acc = 0;
+        int32_t k = 0, it = 0, pt = 0, rs = 0;
         for (int e = 0; e < E; ++e) {
-            koff[e] = acc;
-            acc += len[e];
+            koff[e] = k;
+            ifirst[e] = it;
+            pfirst[e] = pieces[e] > 1 ? pt : -1;
+            rslot[e] = pieces[e] > 1 ? rs : -1;
+            k += len[e];
+            it += pieces[e];
+            if (pieces[e] > 1) {
+                pt += pieces[e];
+                ++rs;
+            }
         }
-        koff[E] = acc;
+        koff[E] = k;
+        wcount[0] = it;
+        wcount[1] = rs;
     }
+    __syncthreads();
+    for (int e = threadIdx.x; e < E; e += blockDim.x) {
+        for (int c = 0; c < pieces[e]; ++c) {
+            TileDesc t;
+            t.e = e;
+            t.row0 = koff[e] + c * CHUNK;
+            t.rows = min(CHUNK, len[e] - c * CHUNK);
+            t.pad = pfirst[e] < 0 ? -1 : pfirst[e] + c;
+            items[ifirst[e] + c] = t;
+        }
+        if (rslot[e] >= 0) rlist[rslot[e]] = TileDesc{e, pfirst[e], pieces[e], 0};
+    }
+}
+
+// Gradients of the split experts: out[e] = sum of its partial blocks in
+// order (fp32), four elements per thread. blockIdx.y = split expert.
+__global__ __launch_bounds__(256) void k_wgrad_reduce(const float* __restrict__ partials,
+                                                     const TileDesc* __restrict__ rlist,
+                                                     const int32_t* __restrict__ wcount, size_t mn,
+                                                     float* __restrict__ out) {
+    if ((int)blockIdx.y >= wcount[1]) return;
+    const TileDesc r = rlist[blockIdx.y];
+    const size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+    if (i >= mn) return;
+    float4 acc = *reinterpret_cast<const float4*>(partials + (size_t)r.row0 * mn + i);
+    for (int c = 1; c < r.rows; ++c) {
+        const float4 v = *reinterpret_cast<const float4*>(partials + ((size_t)r.row0 + c) * mn + i);
+        acc.x += v.x;
+        acc.y += v.y;
+        acc.z += v.z;
+        acc.w += v.w;
+    }
+    *reinterpret_cast<float4*>(out + (size_t)r.e * mn + i) = acc;
 }
 
 // Transposing gather into the K windows: out[c][q] for window position q of
 // expert e (q = koff[e] + i) is in[src(offsets[e] + i)][c] when i < count_e,
 // and 0 in the padding up to the window's end. src(p) is p (rows already in
 // sorted order), row_map[p] (slot rows) or row_map[p] / K (token rows).
-// in: [rows, C] bf16, out: [C, ld] bf16, C a multiple of 64. Positions past
-// koff[E] are left alone.
+// in: [rows, C] bf16; out: [C, ld] bf16 stored slab-major, [ld / 64][C][64]
+// (element (c, q) at ((q / 64) C + c) 64 + q % 64), so that one 64-column K
+// slab of a product's operand tile is contiguous. C a multiple of 64.
+// Positions past koff[E] are left alone.
 __global__ __launch_bounds__(256) void k_transpose_window(const bf16_t* __restrict__ in, int C, int mode,
                                                          const int32_t* __restrict__ row_map, int K,
                                                          const int32_t* __restrict__ offsets,
@@ -109,7 +167,7 @@ __global__ __launch_bounds__(256) void k_transpose_window(const bf16_t* __restri
         bf16_t* e = reinterpret_cast<bf16_t*>(&v);
 #pragma unroll
         for (int k = 0; k < 8; ++k) e[k] = tile[r + k][c];
-        *reinterpret_cast<uint4*>(out + (size_t)(c0 + c) * ld + q0 + r) = v;
+        *reinterpret_cast<uint4*>(out + ((size_t)(q0 / TT) * C + c0 + c) * TT + r) = v;
     }
 }
 
@@ -151,8 +209,17 @@ hipError_t launch_transpose_w(const void* in, int G, int R, int C, void* out, hi
     return hipGetLastError();
 }
 
-hipError_t launch_window_offsets(const int32_t* offsets, int E, int32_t* koff, hipStream_t s) {
-    hipLaunchKernelGGL(k_window_offsets, dim3(1), dim3(1024), 0, s, offsets, E, koff);
+hipError_t launch_wgrad_plan(const int32_t* offsets, int E, int32_t* koff, TileDesc* items, TileDesc* rlist,
+                             int32_t* wcount, hipStream_t s) {
+    hipLaunchKernelGGL(k_wgrad_plan, dim3(1), dim3(1024), 0, s, offsets, E, koff, items, rlist, wcount);
+    return hipGetLastError();
+}
+
+hipError_t launch_wgrad_reduce(const float* partials, const TileDesc* rlist, const int32_t* wcount, int E,
+                               size_t mn, float* out, hipStream_t s) {
+    const size_t blocks = (mn / 4 + 255) / 256;
+    hipLaunchKernelGGL(k_wgrad_reduce, dim3((unsigned)blocks, (unsigned)E), dim3(256), 0, s, partials, rlist, wcount,
+                       mn, out);
     return hipGetLastError();
 }
 

@@ -109,15 +109,16 @@ __device__ __forceinline__ float swiglu_col(float g, float u, bool valid) {
     return valid ? silu_as(g) * u : 0.0f;
 }
 
-// Tile of workgroup `b` in the weight-gradient product: groups x (M / bm)
-// row tiles x (N / bn) column tiles, dense (every tile exists), in the same
-// XCD-aware order as locate_tile. M = a.dense_rows.
+// Tile of workgroup `b` in the weight-gradient product: work items x (M / bm)
+// row tiles x (N / bn) column tiles, in the same XCD-aware order as
+// locate_tile (the tiles of one item are adjacent). M = a.dense_rows. tc.e is
+// the work item here.
 __device__ __forceinline__ TileCoord locate_wgrad_tile(const GemmArgs& a, int bm, int bn) {
     TileCoord tc;
     tc.valid = false;
     const int n_n = a.N / bn;
     const int m_per = a.dense_rows / bm;
-    const int total = a.groups * m_per * n_n;
+    const int total = *a.n_tiles * m_per * n_n;
     const int per = (total + kNumXcd - 1) / kNumXcd;
     const int b = blockIdx.x;
     const int j = b / kNumXcd;
@@ -295,11 +296,16 @@ void k_gemm_bf16(const GemmArgs a) {
     const __amdgpu_buffer_rsrc_t xres = make_rsrc(a.A, a.a_bytes);
     // SwiGLU: the group's 2 act_n weight rows; reads past them return zeros.
     const __amdgpu_buffer_rsrc_t wres =
-        make_rsrc(static_cast<const bf16_t*>(a.B) + (size_t)tc.e * a.b_group_stride,
+        make_rsrc(static_cast<const bf16_t*>(a.B) + (WGRAD ? 0 : (size_t)tc.e * a.b_group_stride),
                   (uint32_t)(SWIGLU ? 2 * a.act_n : weight_rows(a)) * Kd * 2);
 
     constexpr int SWZ_SHIFT = CPR == 8 ? 1 : 2;
     constexpr int SWZ_MASK = CPR - 1;
+    // Operand row stride. The weight-gradient operands are slab-major
+    // ([K / 64][rows][64]): a row's 64-column piece is 128 bytes after the
+    // previous row's, and a K slab is rows * 128 bytes.
+    static_assert(!WGRAD || BK == 64, "slab-major operands have 64-column slabs");
+    const uint32_t rstride = WGRAD ? 128u : (uint32_t)(Kd * 2);
 
     uint32_t xv[AP];
 #pragma unroll
@@ -310,7 +316,7 @@ void k_gemm_bf16(const GemmArgs a) {
         int xrow;
         if (A_GATHER) xrow = srow[r];
         else xrow = tc.row0 + (r < tc.rows ? r : tc.rows - 1);
-        xv[i] = (uint32_t)xrow * (uint32_t)(Kd * 2) + c * 16;
+        xv[i] = (uint32_t)xrow * rstride + c * 16;
     }
     uint32_t wv[BP];
 #pragma unroll
@@ -327,7 +333,7 @@ void k_gemm_bf16(const GemmArgs a) {
             const int w = r % WTN;
             wrow = tc.n0 / 2 + (r / WTN) * HW + w % HW + (w >= HW ? a.act_n : 0);
         }
-        wv[i] = (uint32_t)wrow * (uint32_t)(Kd * 2) + c * 16;
+        wv[i] = (uint32_t)wrow * rstride + c * 16;
     }
 
     f32x16_t acc[FN][FM];
@@ -355,19 +361,25 @@ void k_gemm_bf16(const GemmArgs a) {
     // K range: the whole row, or (weight gradients) the group's window.
     int nk = Kd / BK;
     uint32_t kbase = 0;
+    TileDesc item{};
     if (WGRAD) {
-        const int k0 = a.koff[tc.e], k1 = a.koff[tc.e + 1];
-        nk = (k1 - k0) / BK;
-        kbase = (uint32_t)k0 * 2;
+        item = a.tiles[tc.e];
+        nk = item.rows / BK;
+        kbase = (uint32_t)item.row0 * 2;
     }
 
     auto issue = [&](int stage, int kslab) {
         uint8_t* buf = smem + stage * STAGE;
-        const uint32_t soff = kbase + (uint32_t)kslab * BK * 2;
+        uint32_t soff_a = kbase + (uint32_t)kslab * BK * 2, soff_b = soff_a;
+        if (WGRAD) {
+            const uint32_t slab = (uint32_t)(item.row0 / 64 + kslab);
+            soff_a = slab * (uint32_t)a.dense_rows * 128u;
+            soff_b = slab * (uint32_t)a.N * 128u;
+        }
 #pragma unroll
-        for (int i = 0; i < AP; ++i) copy16_to_lds(xres, xv[i], soff, buf + (wave + NW * i) * 1024);
+        for (int i = 0; i < AP; ++i) copy16_to_lds(xres, xv[i], soff_a, buf + (wave + NW * i) * 1024);
 #pragma unroll
-        for (int i = 0; i < BP; ++i) copy16_to_lds(wres, wv[i], soff, buf + BM * ROWB + (wave + NW * i) * 1024);
+        for (int i = 0; i < BP; ++i) copy16_to_lds(wres, wv[i], soff_b, buf + BM * ROWB + (wave + NW * i) * 1024);
     };
     auto read_frags = [&](uint32_t sbase, int ks, bf16x8_t* xf, bf16x8_t* wf) {
         const uint32_t xa = xoff[ks] + sbase, wa = woff[ks] + sbase;
@@ -475,12 +487,13 @@ void k_gemm_bf16(const GemmArgs a) {
                         if (EPI == EPI_GELU_STORE || EPI == EPI_GELU_BWD) {
                             v0 = gelu_as(v0); v1 = gelu_as(v1); v2 = gelu_as(v2); v3 = gelu_as(v3);
                         }
-                        if (EPI == EPI_DGELU) {  // times the stored GELU' of the same element
+                        if (EPI == EPI_DGELU) {  // times GELU' of the stored pre-activation
                             const int r = wm * WTM + i * 32 + fr;
                             const size_t p = (size_t)(tc.row0 + (r < tc.rows ? r : tc.rows - 1));
                             const float4 f = *reinterpret_cast<const float4*>(
                                 static_cast<const float*>(a.aux) + p * a.N + ocol0 + j * 32 + 8 * g + 4 * fk);
-                            v0 *= f.x; v1 *= f.y; v2 *= f.z; v3 *= f.w;
+                            v0 *= gelu_grad_as(f.x); v1 *= gelu_grad_as(f.y);
+                            v2 *= gelu_grad_as(f.z); v3 *= gelu_grad_as(f.w);
                         }
                         *reinterpret_cast<uint2*>(dst) = pack4_bf16(v0, v1, v2, v3);
                     }
@@ -496,15 +509,19 @@ void k_gemm_bf16(const GemmArgs a) {
             const uint4 v = *reinterpret_cast<const uint4*>(stg + rr * RSTR + pc * 16);
             if (r < tc.rows && (!SWIGLU || ocol0 < a.act_ld)) {
                 size_t orow = O_SCATTER ? (size_t)srow[r] : (size_t)(tc.row0 + r);
-                if (WGRAD) orow += (size_t)tc.e * a.dense_rows;
-                uint8_t* out = static_cast<uint8_t*>(a.C) + (orow * ostride + ocol0) * OES + pc * 16;
+                void* obase = a.C;
+                if (WGRAD) {  // the expert's gradient, or the item's partial block
+                    orow += (size_t)(item.pad < 0 ? item.e : item.pad) * a.dense_rows;
+                    if (item.pad >= 0) obase = a.C2;
+                }
+                uint8_t* out = static_cast<uint8_t*>(obase) + (orow * ostride + ocol0) * OES + pc * 16;
                 *reinterpret_cast<uint4*>(out) = v;
             }
         }
         wave_sync_lds();
     }
     if constexpr (EPI == EPI_GELU_BWD) {
-        // Second output: GELU'(acc) in fp32 (rows of N), the same staging.
+        // Second output: the pre-activation (acc) in fp32 (rows of N), the same staging.
         constexpr int SEG2 = WTN * 4, RSTR2 = SEG2 + 16, CPRO2 = SEG2 / 16, PIECES2 = 32 * CPRO2 / kWave;
         static_assert(NW * 32 * RSTR2 <= STAGES * STAGE, "epilogue staging must fit in the stage buffers");
         __syncthreads();  // the wider rows overlap other waves' first-pass areas
@@ -516,8 +533,8 @@ void k_gemm_bf16(const GemmArgs a) {
 #pragma unroll
                 for (int g = 0; g < 4; ++g)
                     *reinterpret_cast<float4*>(stg2 + fr * RSTR2 + (j * 32 + 8 * g + 4 * fk) * 4) =
-                        make_float4(gelu_grad_as(acc[j][i][4 * g + 0]), gelu_grad_as(acc[j][i][4 * g + 1]),
-                                    gelu_grad_as(acc[j][i][4 * g + 2]), gelu_grad_as(acc[j][i][4 * g + 3]));
+                        make_float4(acc[j][i][4 * g + 0], acc[j][i][4 * g + 1], acc[j][i][4 * g + 2],
+                                    acc[j][i][4 * g + 3]);
             wave_sync_lds();
 #pragma unroll
             for (int k = 0; k < PIECES2; ++k) {
@@ -853,10 +870,12 @@ void k_gemm_pp(const GemmArgs a) {
     constexpr int AP = BM * CPR / kWave / NW;  // 8 token copy pieces per wave and slab
     constexpr int BP = BN * CPR / kWave / NW;  // 8 weight copy pieces
     static_assert(AP == 8 && BP == 8, "copy schedule is written for 8 + 8 pieces");
-    constexpr bool GATHER = GROUPED && fc1_epi(EPI);
+    constexpr bool BWD1 = EPI == EPI_GELU_BWD;  // bf16 GELU, then the fp32 pre-activation into C2
+    constexpr bool DG = EPI == EPI_DGELU;       // bf16 of acc times GELU'(aux)
+    constexpr bool GATHER = GROUPED && (fc1_epi(EPI) || BWD1 || DG);
     constexpr bool SWIGLU = EPI == EPI_SWIGLU_STORE;
-    constexpr bool SCATTER = EPI == EPI_SCATTER_SLOT;
-    constexpr bool OUT_F32 = EPI == EPI_STORE_F32;
+    constexpr bool SCATTER = EPI == EPI_SCATTER_SLOT || EPI == EPI_SCATTER_SLOT_F32;
+    constexpr bool OUT_F32 = EPI == EPI_STORE_F32 || EPI == EPI_SCATTER_SLOT_F32;
     constexpr bool COMBINE = EPI == EPI_COMBINE;
     constexpr bool STAGE_F32 = OUT_F32 || COMBINE;  // accumulators staged as fp32
     constexpr int OES = OUT_F32 ? 4 : 2;
@@ -967,12 +986,15 @@ void k_gemm_pp(const GemmArgs a) {
             tok[i] = a.row_map[t.row0 + min(r, t.rows - 1)];
         }
     };
+    // Row map entries are slots; the operand row is the slot's token (slot /
+    // K) or, gathering slot rows, the slot itself.
+    const int rdiv = a.row_mode == ROWS_GATHER_SLOTS ? 1 : a.route_k;
     auto token_offsets = [&](const int32_t (&tok)[AP], uint32_t (&xv)[AP]) {
 #pragma unroll
         for (int i = 0; i < AP; ++i) {
             int r, c;
             piece_rc(i, r, c);
-            xv[i] = (uint32_t)(tok[i] / a.route_k) * rowbytes + c * 16;
+            xv[i] = (uint32_t)(tok[i] / rdiv) * rowbytes + c * 16;
         }
     };
     // Output slot of staged piece k of 32-row block i (fc2 scatter).
@@ -1198,14 +1220,30 @@ void k_gemm_pp(const GemmArgs a) {
                                            (u32x2_t){pk.x, pk.y});
                         }
                 } else {
+                    // dH: GELU' of the stored pre-activation of this lane's row and columns.
+                    float4 fac[FB][4];
+                    if constexpr (DG) {
+                        const int r = wm * WT + i * 32 + fr;
+                        const float* arow = static_cast<const float*>(a.aux) +
+                                            (size_t)(t.row0 + min(r, t.rows - 1)) * a.N + t.n0 + wn * WT + 4 * fk;
+#pragma unroll
+                        for (int j = 0; j < FB; ++j)
+#pragma unroll
+                            for (int g = 0; g < 4; ++g)
+                                fac[j][g] = *reinterpret_cast<const float4*>(arow + j * 32 + 8 * g);
+                    }
 #pragma unroll
                     for (int j = 0; j < FB; ++j)
 #pragma unroll
                         for (int g = 0; g < 4; ++g) {
                             float v0 = acc_read(acc[j][i][4 * g + 0]), v1 = acc_read(acc[j][i][4 * g + 1]);
                             float v2 = acc_read(acc[j][i][4 * g + 2]), v3 = acc_read(acc[j][i][4 * g + 3]);
-                            if (EPI == EPI_GELU_STORE) {
+                            if (EPI == EPI_GELU_STORE || BWD1) {
                                 v0 = gelu_as(v0); v1 = gelu_as(v1); v2 = gelu_as(v2); v3 = gelu_as(v3);
+                            }
+                            if constexpr (DG) {
+                                v0 *= gelu_grad_as(fac[j][g].x); v1 *= gelu_grad_as(fac[j][g].y);
+                                v2 *= gelu_grad_as(fac[j][g].z); v3 *= gelu_grad_as(fac[j][g].w);
                             }
                             const int chunk = 4 * j + g;
                             const uint2 pk = pack4_bf16(v0, v1, v2, v3);
@@ -1255,6 +1293,43 @@ void k_gemm_pp(const GemmArgs a) {
                         const size_t orw = SCATTER ? (size_t)orow[i][k] : (size_t)(t.row0 + r);
                         uint8_t* out = cbase + (orw * a.N + t.n0 + wn * WT + h * 64) * OES + (lane & 15) * 16;
                         store16_asm(out, v[k]);
+                    }
+                }
+            }
+            if constexpr (BWD1) {
+                // Second output: the pre-activation (acc) as fp32 rows of C2,
+                // two 64-column halves through the same staging rows.
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                    for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+                        for (int g = 0; g < 4; ++g) {
+                            const int j = 2 * h + jj;
+                            const u32x4_t v = {__float_as_uint(acc_read(acc[j][i][4 * g + 0])),
+                                               __float_as_uint(acc_read(acc[j][i][4 * g + 1])),
+                                               __float_as_uint(acc_read(acc[j][i][4 * g + 2])),
+                                               __float_as_uint(acc_read(acc[j][i][4 * g + 3]))};
+                            const int chunk = 8 * jj + 2 * g + fk;
+                            lds_write16_asm(wrow + ((uint32_t)(chunk ^ sw) << 4), v);
+                        }
+                    u32x4_t v[8];
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) {
+                        const int rr = (lane >> 4) + 4 * k;
+                        v[k] = lds_read16u_asm(stg + (uint32_t)rr * 256u + ((uint32_t)((lane & 15) ^ (rr & 15)) << 4));
+                    }
+                    wait_lgkmcnt0();
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) tie(v[k]);
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) {
+                        const int r = wm * WT + i * 32 + (lane >> 4) + 4 * k;
+                        if (r < t.rows)
+                            store16_asm(static_cast<uint8_t*>(a.C2) +
+                                            ((size_t)(t.row0 + r) * a.N + t.n0 + wn * WT + h * 64) * 4 + (lane & 15) * 16,
+                                        v[k]);
                     }
                 }
             }
@@ -1535,6 +1610,9 @@ hipError_t dispatch_bf16(int bm, const GemmArgs& a, hipStream_t s) {
 // Backward products: always the tiled kernel (256- or 64-row tiles).
 template <int EPI, bool GROUPED>
 hipError_t dispatch_tiled(int bm, const GemmArgs& a, hipStream_t s) {
+    constexpr bool ROW_PRODUCT = EPI == EPI_GELU_BWD || EPI == EPI_DGELU || EPI == EPI_SCATTER_SLOT_F32;
+    if constexpr (ROW_PRODUCT)
+        if (bm == 256 && a.N % 256 == 0 && a.Kdim >= 128) return launch_pp<EPI, GROUPED>(a, s);
     if (bm == 256) {
         if (a.N % 128 == 0) return launch_bf16<256, 128, 2, 2, 64, 2, 1, EPI, GROUPED>(a, s);
         return launch_bf16<256, 64, 4, 1, 64, 2, 1, EPI, GROUPED>(a, s);
@@ -1579,8 +1657,7 @@ hipError_t dispatch(const moe_desc_t& d, int epilogue, int bm, const GemmArgs& a
                 if (GROUPED) return dispatch_tiled<EPI_SCATTER_SLOT_F32, true>(bm, a, s);
                 break;
             case EPI_WGRAD_F32:
-                if (!GROUPED && a.koff && a.groups > 0 && a.dense_rows % bm == 0)
-                    return dispatch_tiled<EPI_WGRAD_F32, false>(bm, a, s);
+                if (GROUPED && a.dense_rows % bm == 0) return dispatch_tiled<EPI_WGRAD_F32, true>(bm, a, s);
                 break;
             case EPI_SCATTER_SLOT:
                 if (GROUPED) return dispatch_bf16<EPI_SCATTER_SLOT, true>(bm, a, s);

@@ -188,6 +188,11 @@ BackwardPlan plan_backward(const moe_desc_t& d) {
     b.at = take((size_t)d.h * b.ld * 2);
     b.dht = take((size_t)d.h * b.ld * 2);
     b.xt = take((size_t)d.d * b.ld * 2);
+    b.items_max = d.E + (int32_t)(((size_t)b.ld / 64 + kWgradSlabs - 1) / kWgradSlabs);
+    b.items = take((size_t)b.items_max * sizeof(TileDesc));
+    b.rlist = take((size_t)d.E * sizeof(TileDesc));
+    b.wcount = take(16);
+    b.partials = take((size_t)b.items_max * d.d * d.h * 4);
     b.total = off;
     return b;
 }
@@ -323,8 +328,9 @@ static moe_status_t enqueue_shared_mlp(const moe_desc_t& d, const WorkspacePlan&
     return MOE_OK;
 }
 
-// Backward of the routed experts (GELU, bf16): recompute fc1 keeping GELU',
-// dH = (G W2) * GELU' with G the output gradients gathered by slot, the slot
+// Backward of the routed experts (GELU, bf16): recompute fc1 keeping the fp32
+// pre-activation P, dH = (G W2) * GELU'(P) with G the output gradients
+// gathered by slot (GELU' formed in that product's epilogue), the slot
 // gradients of x dH W1 (fp32, slot order) summed per token, and the weight
 // gradients as K-windowed products of transposed operands.
 static moe_status_t enqueue_backward(const moe_desc_t& d, const BackwardPlan& b, void* ws, const void* x,
@@ -346,7 +352,7 @@ static moe_status_t enqueue_backward(const moe_desc_t& d, const BackwardPlan& b,
     HIP_CHECK(launch_transpose_w(w1, d.E, d.h, d.d, w1t, s), "transpose w1");
     HIP_CHECK(launch_transpose_w(w2, d.E, d.d, d.h, w2t, s), "transpose w2");
 
-    GemmArgs g{};  // fc1 again: the activation (bf16) and GELU' (fp32)
+    GemmArgs g{};  // fc1 again: the activation (bf16) and the pre-activation (fp32)
     g.A = x;
     g.B = w1;
     g.C = act;
@@ -363,7 +369,7 @@ static moe_status_t enqueue_backward(const moe_desc_t& d, const BackwardPlan& b,
     g.a_bytes = (uint32_t)((size_t)d.T * d.d * 2);
     HIP_CHECK(launch_gemm(d, EPI_GELU_BWD, p.tile_bm, g, s), "backward fc1");
 
-    GemmArgs ga = g;  // dH = (G W2) * GELU'
+    GemmArgs ga = g;  // dH = (G W2) * GELU'(P)
     ga.A = gout;
     ga.B = w2t;
     ga.C = dh;
@@ -390,7 +396,11 @@ static moe_status_t enqueue_backward(const moe_desc_t& d, const BackwardPlan& b,
     void* at = region<void>(ws, b.at);
     void* dht = region<void>(ws, b.dht);
     void* xt = region<void>(ws, b.xt);
-    HIP_CHECK(launch_window_offsets(offsets, d.E, koff, s), "window offsets");
+    TileDesc* items = region<TileDesc>(ws, b.items);
+    TileDesc* rlist = region<TileDesc>(ws, b.rlist);
+    int32_t* wcount = region<int32_t>(ws, b.wcount);
+    float* partials = region<float>(ws, b.partials);
+    HIP_CHECK(launch_wgrad_plan(offsets, d.E, koff, items, rlist, wcount, s), "weight-gradient plan");
     HIP_CHECK(launch_transpose_window(gout, d.d, SRC_SLOT, sorted_slots, d.K, offsets, koff, d.E, gt, b.ld, s),
               "transpose G");
     HIP_CHECK(launch_transpose_window(act, d.h, SRC_SORTED, sorted_slots, d.K, offsets, koff, d.E, at, b.ld, s),
@@ -409,12 +419,14 @@ static moe_status_t enqueue_backward(const moe_desc_t& d, const BackwardPlan& b,
         w.Kdim = b.ld;
         w.route_k = 1;
         w.row_mode = ROWS_IDENTITY;
-        w.koff = koff;
-        w.groups = d.E;
+        w.tiles = items;
+        w.n_tiles = wcount;
+        w.C2 = partials;
         const int bm = m % 256 == 0 ? 256 : 64;
-        w.max_tiles = d.E * (m / bm);
+        w.max_tiles = b.items_max * (m / bm);
         w.a_bytes = (uint32_t)((size_t)m * b.ld * 2);
         HIP_CHECK(launch_gemm(d, EPI_WGRAD_F32, bm, w, s), what);
+        HIP_CHECK(launch_wgrad_reduce(partials, rlist, wcount, d.E, (size_t)m * n, out, s), what);
         return MOE_OK;
     };
     CHECK(wgrad(gt, d.d, at, d.h, dw2, "dW2"));

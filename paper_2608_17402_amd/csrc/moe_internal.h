@@ -46,12 +46,14 @@ enum GemmEpilogue : int {
                             // the act_n up rows. The launcher sets N: a tile of BN columns computes
                             // BN / 2 activation columns from the matching gate and up rows
     // Backward of GELU experts (tiled kernel only):
-    EPI_GELU_BWD = 5,       // C[p, :] = bf16(GELU(acc)) and C2[p, :] = GELU'(acc) (fp32), sorted order
-    EPI_DGELU = 6,          // C[p, :] = bf16(acc * aux[p, :]) (aux fp32 [rows, N]), sorted order
+    EPI_GELU_BWD = 5,       // C[p, :] = bf16(GELU(acc)) and C2[p, :] = acc (fp32), sorted order
+    EPI_DGELU = 6,          // C[p, :] = bf16(acc * GELU'(aux[p, :])) (aux fp32 [rows, N]), sorted order
     EPI_SCATTER_SLOT_F32 = 7,  // C[sorted_slots[p], :] = acc as fp32
-    EPI_WGRAD_F32 = 8,      // C[e][m, :] = sum over expert e's window of the K axis (fp32): the weight
-                            // gradients. A [dense_rows, Kdim] and B [N, Kdim] are shared by all groups;
-                            // group e reads columns koff[e] .. koff[e+1] (multiples of 64)
+    EPI_WGRAD_F32 = 8,      // weight gradients (fp32): A [dense_rows, Kdim] and B [N, Kdim], stored
+                            // slab-major ([Kdim / 64][rows][64]), are shared by all experts; work item
+                            // i = tiles[i] = {e, k0, klen, dest} sums K columns
+                            // k0 .. k0 + klen (multiples of 64) of rows m into C[e][m, :] (dest < 0) or into
+                            // the partial block C2[dest] [dense_rows, N]; *n_tiles items
 };
 
 struct GemmArgs {
@@ -70,10 +72,8 @@ struct GemmArgs {
     int64_t b_group_stride;    // elements between consecutive experts' weights
     int32_t b_rows;            // dense bf16 only: rows of B that exist (0 = N); rows past them read as zeros
     uint32_t a_bytes;          // bytes of the A operand buffer (bounds of its buffer resource)
-    void* C2;                  // EPI_GELU_BWD: second output (fp32)
-    const void* aux;           // EPI_DGELU: per-element factor (fp32, rows of N)
-    const int32_t* koff;       // EPI_WGRAD_F32: [groups + 1] K-window starts
-    int32_t groups;            // EPI_WGRAD_F32: number of groups (experts)
+    void* C2;                  // EPI_GELU_BWD: second output (fp32); EPI_WGRAD_F32: partial blocks
+    const void* aux;           // EPI_DGELU: the pre-activation (fp32, rows of N)
     int32_t act_n;             // EPI_SWIGLU_STORE: activation width h (valid columns)
     int32_t act_ld;            // EPI_SWIGLU_STORE: activation row stride (h rounded up to 128)
     const float* gate;         // EPI_COMBINE: gates [rows, route_k]
@@ -99,13 +99,17 @@ WorkspacePlan plan_workspace(const moe_desc_t& d);
 // activation), then the backward's own regions.
 struct BackwardPlan {
     WorkspacePlan fwd;
-    size_t dgelu;            // GELU'(W1 x) [T*K, h] fp32, sorted order
+    size_t dgelu;            // pre-activation W1 x [T*K, h] fp32, sorted order
     size_t w1t, w2t;         // transposed weights [E, d, h] and [E, h, d]
     size_t dh;               // pre-activation gradient [T*K, h] bf16, sorted order
     size_t dxs;              // slot gradients of x [T*K, d] fp32, slot order
     size_t koff;             // [E + 1] K-window starts
     size_t gt, at, dht, xt;  // transposed operands [d | h, ld] bf16
-    int32_t ld;              // their row length: T*K + 64 E, rounded up to 64
+    size_t items, rlist;     // weight-gradient work items and split experts (TileDesc each)
+    size_t wcount;           // [4] int32: item count, split-expert count
+    size_t partials;         // [parts_max, d, h] fp32 partial sums of split experts
+    int32_t ld;              // row length of the transposed operands: T*K + 64 E, rounded up to 64
+    int32_t items_max;       // bound on the work items (and on the partial blocks)
     size_t total;
 };
 BackwardPlan plan_backward(const moe_desc_t& d);
@@ -147,7 +151,12 @@ bool gemm_combine_fusable(const moe_desc_t& d, int bm, int n, int kdim);
 // gather: rows already in sorted order, slot rows, token rows.
 enum TransposeSource : int { SRC_SORTED = 0, SRC_SLOT = 1, SRC_TOKEN = 2 };
 hipError_t launch_transpose_w(const void* in, int G, int R, int C, void* out, hipStream_t s);
-hipError_t launch_window_offsets(const int32_t* offsets, int E, int32_t* koff, hipStream_t s);
+// Longest K window of one weight-gradient work item, in 64-column slabs.
+constexpr int kWgradSlabs = 64;
+hipError_t launch_wgrad_plan(const int32_t* offsets, int E, int32_t* koff, TileDesc* items, TileDesc* rlist,
+                             int32_t* wcount, hipStream_t s);
+hipError_t launch_wgrad_reduce(const float* partials, const TileDesc* rlist, const int32_t* wcount, int E,
+                               size_t mn, float* out, hipStream_t s);
 hipError_t launch_transpose_window(const void* in, int C, int mode, const int32_t* row_map, int K,
                                    const int32_t* offsets, const int32_t* koff, int E, void* out, int ld,
                                    hipStream_t s);
