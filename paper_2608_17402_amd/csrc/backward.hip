@@ -41,13 +41,15 @@ __global__ __launch_bounds__(256) void k_transpose_w(const bf16_t* __restrict__ 
 
 // Plan of the weight-gradient products, one workgroup:
 //  - K windows: expert e owns columns koff[e] .. koff[e+1] of the transposed
-//    operands, its row count rounded up to a multiple of 64 (the K slab);
-//  - work items: each window cut into pieces of at most kWgradSlabs slabs, so
-//    that no tile runs much longer than the others under a skewed load. An
-//    expert with one piece (or none: an empty expert gets one item of length
-//    0, which writes zeros) writes its gradient directly (dest = -1); the
-//    pieces of a longer window write partial blocks dest = first .. first +
-//    n - 1, summed afterwards in that order;
+//    operands, its row count rounded up to a multiple of 64 (the K slab) and
+//    to at least two slabs (the persistent kernel's pipeline holds two; an
+//    empty expert's window is all zeros, so its gradient comes out 0);
+//  - work items: each window cut into pieces of at most kWgradSlabs slabs, of
+//    even size (so every piece keeps two slabs or more), so that no tile runs
+//    much longer than the others under a skewed load. An expert with one
+//    piece writes its gradient directly (dest = -1); the pieces of a longer
+//    window write partial blocks dest = first .. first + n - 1, summed
+//    afterwards in that order;
 //  - rlist: the split experts {e, first partial block, pieces}.
 // wcount[0] = items, wcount[1] = split experts.
 __global__ __launch_bounds__(1024) void k_wgrad_plan(const int32_t* __restrict__ offsets, int E,
@@ -56,8 +58,8 @@ __global__ __launch_bounds__(1024) void k_wgrad_plan(const int32_t* __restrict__
     __shared__ int32_t len[kMaxE], pieces[kMaxE], ifirst[kMaxE], pfirst[kMaxE], rslot[kMaxE];
     constexpr int CHUNK = kWgradSlabs * 64;
     for (int e = threadIdx.x; e < E; e += blockDim.x) {
-        len[e] = (offsets[e + 1] - offsets[e] + 63) / 64 * 64;
-        pieces[e] = len[e] > CHUNK ? (len[e] + CHUNK - 1) / CHUNK : 1;
+        len[e] = max(128, (offsets[e + 1] - offsets[e] + 63) / 64 * 64);
+        pieces[e] = (len[e] + CHUNK - 1) / CHUNK;
     }
     __syncthreads();
     if (threadIdx.x == 0) {
@@ -80,13 +82,18 @@ __global__ __launch_bounds__(1024) void k_wgrad_plan(const int32_t* __restrict__
     }
     __syncthreads();
     for (int e = threadIdx.x; e < E; e += blockDim.x) {
-        for (int c = 0; c < pieces[e]; ++c) {
+        const int slabs = len[e] / 64, n = pieces[e];
+        const int base = slabs / n, extra = slabs % n;  // the first `extra` pieces take one more slab
+        int s0 = 0;
+        for (int c = 0; c < n; ++c) {
+            const int sz = base + (c < extra ? 1 : 0);
             TileDesc t;
             t.e = e;
-            t.row0 = koff[e] + c * CHUNK;
-            t.rows = min(CHUNK, len[e] - c * CHUNK);
+            t.row0 = koff[e] + s0 * 64;
+            t.rows = sz * 64;
             t.pad = pfirst[e] < 0 ? -1 : pfirst[e] + c;
             items[ifirst[e] + c] = t;
+            s0 += sz;
         }
         if (rslot[e] >= 0) rlist[rslot[e]] = TileDesc{e, pfirst[e], pieces[e], 0};
     }

@@ -875,7 +875,11 @@ void k_gemm_pp(const GemmArgs a) {
     constexpr bool GATHER = GROUPED && (fc1_epi(EPI) || BWD1 || DG);
     constexpr bool SWIGLU = EPI == EPI_SWIGLU_STORE;
     constexpr bool SCATTER = EPI == EPI_SCATTER_SLOT || EPI == EPI_SCATTER_SLOT_F32;
-    constexpr bool OUT_F32 = EPI == EPI_STORE_F32 || EPI == EPI_SCATTER_SLOT_F32;
+    // Weight gradients: slab-major operands, a K window per work item, fp32
+    // output to the expert's gradient or a partial block.
+    constexpr bool WG = EPI == EPI_WGRAD_F32;
+    static_assert(!WG || GROUPED, "weight-gradient tiles come from the work-item table");
+    constexpr bool OUT_F32 = EPI == EPI_STORE_F32 || EPI == EPI_SCATTER_SLOT_F32 || WG;
     constexpr bool COMBINE = EPI == EPI_COMBINE;
     constexpr bool STAGE_F32 = OUT_F32 || COMBINE;  // accumulators staged as fp32
     constexpr int OES = OUT_F32 ? 4 : 2;
@@ -886,8 +890,9 @@ void k_gemm_pp(const GemmArgs a) {
     __shared__ __attribute__((aligned(1024))) uint8_t smem[AST * SLAB + WST * SLAB];
 
     const int n_n = a.N / BN;
+    const int m_per = WG ? a.dense_rows / BM : 1;  // row tiles per work item
     const int total =
-        (GROUPED ? __builtin_amdgcn_readfirstlane(*a.n_tiles) : (a.dense_rows + BM - 1) / BM) * n_n;
+        (GROUPED ? __builtin_amdgcn_readfirstlane(*a.n_tiles) * m_per : (a.dense_rows + BM - 1) / BM) * n_n;
     const int per = (total + kNumXcd - 1) / kNumXcd;
     const int xcd = blockIdx.x % kNumXcd;
     const int wpx = gridDim.x / kNumXcd;  // workgroups per XCD: the tile stride
@@ -901,17 +906,20 @@ void k_gemm_pp(const GemmArgs a) {
     const int wm = wave >> 1, wn = wave & 1;
     const int Kd = a.Kdim;
     const int nk = Kd / BK;
-    const uint32_t rowbytes = (uint32_t)Kd * 2;
+    // Slab-major operands (weight gradients): a row's piece of one K slab is
+    // 128 bytes after the previous row's.
+    const uint32_t rowbytes = WG ? 128u : (uint32_t)Kd * 2;
 
     struct Tile {
         int e, row0, rows, n0;
+        int slab0, nk, dest;  // weight gradients: first K slab, K slabs, partial block or -1
     };
     // Tile-table entry of tile l (grouped): read through the vector path (the
     // kernel's own stores keep the compiler from proving the table constant).
     // Indices past this workgroup's share read its last tile instead.
     auto tile_entry = [&](int l) {
         TileDesc d{};
-        if (GROUPED) d = a.tiles[min(l, lid_end - 1) / n_n];
+        if (GROUPED) d = a.tiles[min(l, lid_end - 1) / n_n / m_per];
         return d;
     };
     // Tile l from its table entry; the entry is the same for every lane, so it
@@ -920,7 +928,17 @@ void k_gemm_pp(const GemmArgs a) {
         Tile t;
         const int mt = l / n_n;
         t.n0 = (l - mt * n_n) * BN;
-        if (GROUPED) {
+        t.slab0 = 0;
+        t.nk = nk;
+        t.dest = -1;
+        if (WG) {
+            t.e = __builtin_amdgcn_readfirstlane(d.e);
+            t.row0 = (mt - (mt / m_per) * m_per) * BM;
+            t.rows = BM;
+            t.slab0 = __builtin_amdgcn_readfirstlane(d.row0) / BK;
+            t.nk = __builtin_amdgcn_readfirstlane(d.rows) / BK;
+            t.dest = __builtin_amdgcn_readfirstlane(d.pad);
+        } else if (GROUPED) {
             t.e = __builtin_amdgcn_readfirstlane(d.e);
             t.row0 = __builtin_amdgcn_readfirstlane(d.row0);
             t.rows = __builtin_amdgcn_readfirstlane(d.rows);
@@ -944,12 +962,23 @@ void k_gemm_pp(const GemmArgs a) {
         if (SWIGLU)
             return make_rsrc(Bw + (size_t)t.e * a.b_group_stride + (size_t)(t.n0 / 2) * Kd,
                              (uint32_t)__builtin_amdgcn_readfirstlane(2 * a.act_n - t.n0 / 2) * rowbytes);
+        // Weight gradients: every K slab of rows n0 .. (slab-major operand).
+        if (WG) return make_rsrc(Bw + (size_t)t.n0 * 64, (uint32_t)a.N * (uint32_t)Kd * 2u - (uint32_t)t.n0 * 128u);
         const int rows = __builtin_amdgcn_readfirstlane(max(0, min(BN, weight_rows(a) - t.n0)));
         return make_rsrc(Bw + (size_t)t.e * a.b_group_stride + (size_t)t.n0 * Kd, (uint32_t)rows * rowbytes);
     };
     auto xres_of = [&](const Tile& t) {
         if (GATHER) return make_rsrc(Ax, a.a_bytes);
+        if (WG) return make_rsrc(Ax + (size_t)t.row0 * 64, a.a_bytes - (uint32_t)t.row0 * 128u);
         return make_rsrc(Ax + (size_t)t.row0 * Kd, (uint32_t)t.rows * rowbytes);
+    };
+    // Source offset of K slab s of tile t: s slabs along the rows, or
+    // (slab-major) slab t.slab0 + s of rows x 128 bytes.
+    auto soff_a = [&](const Tile& t, int s) -> uint32_t {
+        return WG ? (uint32_t)(t.slab0 + s) * (uint32_t)a.dense_rows * 128u : (uint32_t)s * (BK * 2);
+    };
+    auto soff_b = [&](const Tile& t, int s) -> uint32_t {
+        return WG ? (uint32_t)(t.slab0 + s) * (uint32_t)a.N * 128u : (uint32_t)s * (BK * 2);
     };
     const __amdgpu_buffer_rsrc_t xnull = make_rsrc(Ax, 0);
     const __amdgpu_buffer_rsrc_t wnull = make_rsrc(Bw, 0);
@@ -1290,8 +1319,13 @@ void k_gemm_pp(const GemmArgs a) {
                     const int rr = (lane >> 4) + 4 * k;
                     const int r = wm * WT + i * 32 + rr;
                     if (r < t.rows) {
-                        const size_t orw = SCATTER ? (size_t)orow[i][k] : (size_t)(t.row0 + r);
-                        uint8_t* out = cbase + (orw * a.N + t.n0 + wn * WT + h * 64) * OES + (lane & 15) * 16;
+                        size_t orw = SCATTER ? (size_t)orow[i][k] : (size_t)(t.row0 + r);
+                        uint8_t* ob = cbase;
+                        if (WG) {  // the expert's gradient, or the work item's partial block
+                            orw += (size_t)(t.dest < 0 ? t.e : t.dest) * a.dense_rows;
+                            if (t.dest >= 0) ob = static_cast<uint8_t*>(a.C2);
+                        }
+                        uint8_t* out = ob + (orw * a.N + t.n0 + wn * WT + h * 64) * OES + (lane & 15) * 16;
                         store16_asm(out, v[k]);
                     }
                 }
@@ -1338,10 +1372,10 @@ void k_gemm_pp(const GemmArgs a) {
 
     // Prologue: token slab 0, weight slab 0, token slab 1, the first half of
     // weight slab 1; wait for slab 0 of both operands; read its first fragments.
-    static_for<AP>([&](auto LC) { copy_a(LC, 0, 0u, xres_c, GATHER ? xv_c : tv); });
-    static_for<BP>([&](auto LC) { copy_w(LC, 0, 0u, wres_c); });
-    static_for<AP>([&](auto LC) { copy_a(LC, 1, (uint32_t)BK * 2, xres_c, GATHER ? xv_c : tv); });
-    static_for<BP / 2>([&](auto LC) { copy_w(LC, 1, (uint32_t)BK * 2, wres_c); });
+    static_for<AP>([&](auto LC) { copy_a(LC, 0, soff_a(tc, 0), xres_c, GATHER ? xv_c : tv); });
+    static_for<BP>([&](auto LC) { copy_w(LC, 0, soff_b(tc, 0), wres_c); });
+    static_for<AP>([&](auto LC) { copy_a(LC, 1, soff_a(tc, 1), xres_c, GATHER ? xv_c : tv); });
+    static_for<BP / 2>([&](auto LC) { copy_w(LC, 1, soff_b(tc, 1), wres_c); });
     wait_vmcnt<AP + BP / 2>();
     barrier_no_fence();
     static_for<2 * FB>([&](auto QC) { read_frag(std::integral_constant<int, 0>{}, QC, 0u, 0u, 0); });
@@ -1354,9 +1388,11 @@ void k_gemm_pp(const GemmArgs a) {
             const int as1 = as == AST - 1 ? 0 : as + 1, as2 = as1 == AST - 1 ? 0 : as1 + 1;
             const int ws1 = ws ^ 1;
             // Slabs kt + 1 and kt + 2 may belong to the next tile.
-            const bool n1 = kt + 1 >= nk, n2 = kt + 2 >= nk;
-            const uint32_t so1 = (uint32_t)(n1 ? kt + 1 - nk : kt + 1) * (BK * 2);
-            const uint32_t so2 = (uint32_t)(n2 ? kt + 2 - nk : kt + 2) * (BK * 2);
+            const int nkc = tc.nk;
+            const bool n1 = kt + 1 >= nkc, n2 = kt + 2 >= nkc;
+            const uint32_t so1 = soff_b(n1 ? tn : tc, n1 ? kt + 1 - nkc : kt + 1);
+            const uint32_t so2 = soff_a(n2 ? tn : tc, n2 ? kt + 2 - nkc : kt + 2);
+            const uint32_t so2w = soff_b(n2 ? tn : tc, n2 ? kt + 2 - nkc : kt + 2);
             const __amdgpu_buffer_rsrc_t wr1 = n1 ? wres_n : wres_c;
             const __amdgpu_buffer_rsrc_t xr2 = n2 ? xres_n : xres_c;
             const __amdgpu_buffer_rsrc_t wr2 = n2 ? wres_n : wres_c;
@@ -1386,11 +1422,11 @@ void k_gemm_pp(const GemmArgs a) {
             // K step 3: first fragments of slab kt + 1; first half of weight
             // slab kt + 2 into the weight slot of slab kt.
             kstep(std::integral_constant<int, 1>{}, (uint32_t)as1 * SLAB, (uint32_t)ws1 * SLAB, 0, [&](auto CC) {
-                copy_w(std::integral_constant<int, decltype(CC)::value>{}, ws, so2, wr2);
+                copy_w(std::integral_constant<int, decltype(CC)::value>{}, ws, so2w, wr2);
             });
             as = as1;
             ws = ws1;
-        } while (++kt < nk);
+        } while (++kt < tc.nk);
 
         // The last K step also read the next tile's first fragments; let them
         // land (their registers are reused by the epilogue) and read them again
@@ -1613,6 +1649,9 @@ hipError_t dispatch_tiled(int bm, const GemmArgs& a, hipStream_t s) {
     constexpr bool ROW_PRODUCT = EPI == EPI_GELU_BWD || EPI == EPI_DGELU || EPI == EPI_SCATTER_SLOT_F32;
     if constexpr (ROW_PRODUCT)
         if (bm == 256 && a.N % 256 == 0 && a.Kdim >= 128) return launch_pp<EPI, GROUPED>(a, s);
+    // Weight gradients: every work item spans at least two K slabs.
+    if constexpr (EPI == EPI_WGRAD_F32)
+        if (bm == 256 && a.N % 256 == 0 && a.dense_rows % 256 == 0) return launch_pp<EPI, GROUPED>(a, s);
     if (bm == 256) {
         if (a.N % 128 == 0) return launch_bf16<256, 128, 2, 2, 64, 2, 1, EPI, GROUPED>(a, s);
         return launch_bf16<256, 64, 4, 1, 64, 2, 1, EPI, GROUPED>(a, s);

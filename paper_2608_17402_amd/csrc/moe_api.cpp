@@ -77,7 +77,7 @@ moe_status_t check_backward_desc(const moe_desc_t* d) {
     if (d->dtype != MOE_BF16) return fail(MOE_ERR_UNSUPPORTED, "the backward needs a bf16 layer");
     if (d->flags & MOE_FLAG_SWIGLU) return fail(MOE_ERR_UNSUPPORTED, "the backward supports GELU experts only");
     const uint64_t lim = (uint64_t)1 << 32, TK = (uint64_t)d->T * d->K;
-    const uint64_t ld = TK + 64 * (uint64_t)d->E + 64;
+    const uint64_t ld = TK + 128 * (uint64_t)d->E + 64;
     if (TK * d->d * 2 >= lim || (uint64_t)(d->d > d->h ? d->d : d->h) * ld * 2 >= lim)
         return fail(MOE_ERR_UNSUPPORTED, "the backward's slot or transposed operands exceed 4 GiB");
     return MOE_OK;
@@ -171,7 +171,7 @@ BackwardPlan plan_backward(const moe_desc_t& d) {
     BackwardPlan b;
     b.fwd = plan_workspace(d);
     const size_t TK = (size_t)d.T * d.K;
-    b.ld = (int32_t)((TK + 64 * (size_t)d.E + 63) / 64 * 64);
+    b.ld = (int32_t)((TK + 128 * (size_t)d.E + 63) / 64 * 64);  // windows: >= 2 slabs, rounded up to one
     size_t off = b.fwd.total;
     auto take = [&](size_t bytes) {
         const size_t o = off;

@@ -108,7 +108,7 @@ struct BackwardPlan {
     size_t items, rlist;     // weight-gradient work items and split experts (TileDesc each)
     size_t wcount;           // [4] int32: item count, split-expert count
     size_t partials;         // [parts_max, d, h] fp32 partial sums of split experts
-    int32_t ld;              // row length of the transposed operands: T*K + 64 E, rounded up to 64
+    int32_t ld;              // row length of the transposed operands: T*K + 128 E, rounded up to 64
     int32_t items_max;       // bound on the work items (and on the partial blocks)
     size_t total;
 };
