@@ -263,6 +263,38 @@ def main():
         ev.close()
         return L, l_ms, f1, f2
 
+    def backward_line(c, L):
+        """Expert-MLP backward on layer L's own routing: five products of
+        2 T K d h (SwiGLU: the gate/up products count twice) flop."""
+        T, K, E, d, h = c.T, c.K, c.E, c.d, c.h
+        sw = c.act == "swiglu"
+        L.forward()
+        binding.moe_permute(L.desc, L.idx, L.counts, L.offsets, L.slots, L.ws)
+        bws = binding.alloc_backward_workspace(L.desc)
+        gen = torch.Generator(device="cuda").manual_seed(5)
+        gout = (torch.randn(T * K, d, device="cuda", generator=gen) * 0.5).to(torch.bfloat16)
+        dx = torch.empty(T, d, dtype=torch.bfloat16, device="cuda")
+        dw1 = torch.empty(E, L.w1.shape[1], d, dtype=torch.float32, device="cuda")
+        dw2 = torch.empty(E, d, L.w2.shape[2], dtype=torch.float32, device="cuda")
+
+        def bwd():
+            binding.moe_grouped_mlp_backward(L.desc, L.x, L.slots, L.offsets, L.w1, L.w2, gout, dx, dw1, dw2, bws)
+
+        for _ in range(2):
+            bwd()
+        b_ms = time_calls(bwd, max(3, args.steps // 2))
+        # fc1 again (SwiGLU: two), dA, dx (SwiGLU: K = 2h), dW2, dW1 (SwiGLU: two)
+        fl = (8.0 if sw else 5.0) * 2.0 * T * K * d * h
+        tf = fl / (b_ms * 1e-3) / 1e12
+        return {
+            "workload": c.name, "act": c.act, "entry": "moe_grouped_mlp_backward", "us": round(b_ms * 1e3, 1),
+            "tokens_per_s": round(T / (b_ms * 1e-3), 1),
+            "roofline": {"kernel": "expert-MLP backward: fc1 again, dA, dx, dW2, dW1 products plus transposes",
+                         "bound": "mfma", "achieved": round(tf, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                         "frac": round(tf / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                         "algorithmic_flops_per_launch": fl, "avg_launch_us": round(b_ms * 1e3, 2)},
+        }
+
     def hbm_line(c, L, l_ms, g_ms):
         w_bytes = c.routed_weight_bytes()
         gbs = w_bytes / (g_ms * 1e-3) / 1e9
@@ -300,6 +332,9 @@ def main():
         out["single_image"]["stages_us"] = {k: round(v * 1e3, 1) for k, v in si_stages.items()}
         del si
 
+    if not args.no_backward and cfg.dtype == "bf16":
+        out["backward"] = backward_line(cfg, lay)
+
     sw_names = [n for n in args.swiglu_configs.split(",") if n]
     if sw_names:
         out["swiglu"] = {}
@@ -309,39 +344,9 @@ def main():
             # ~32 rows per expert is weight-read bound; large batches are MFMA bound.
             weight_bound = c.T * c.K / c.E < 256
             out["swiglu"][name] = hbm_line(c, L, l_ms, f1 + f2) if weight_bound else mfma_line(c, l_ms, f1, f2)
+            if not weight_bound and not args.no_backward:
+                out["swiglu"][name]["backward"] = backward_line(c, L)
             del L
-
-    if not args.no_backward and cfg.act == "gelu" and cfg.dtype == "bf16":
-        # Expert-MLP backward on the main workload's routing: 5 products of
-        # 2 T K d h flop (fc1 again, dA, dx, dW2, dW1).
-        T, K, E, d, h = cfg.T, cfg.K, cfg.E, cfg.d, cfg.h
-        lay.forward()
-        binding.moe_permute(lay.desc, lay.idx, lay.counts, lay.offsets, lay.slots, lay.ws)
-        bws = binding.alloc_backward_workspace(lay.desc)
-        gen = torch.Generator(device="cuda").manual_seed(5)
-        gout = (torch.randn(T * K, d, device="cuda", generator=gen) * 0.5).to(torch.bfloat16)
-        dx = torch.empty(T, d, dtype=torch.bfloat16, device="cuda")
-        dw1 = torch.empty(E, h, d, dtype=torch.float32, device="cuda")
-        dw2 = torch.empty(E, d, h, dtype=torch.float32, device="cuda")
-
-        def bwd():
-            binding.moe_grouped_mlp_backward(lay.desc, lay.x, lay.slots, lay.offsets, lay.w1, lay.w2, gout, dx,
-                                             dw1, dw2, bws)
-
-        for _ in range(2):
-            bwd()
-        b_ms = time_calls(bwd, max(3, args.steps // 2))
-        fl = 5 * 2.0 * T * K * d * h
-        tf = fl / (b_ms * 1e-3) / 1e12
-        out["backward"] = {
-            "workload": cfg.name, "entry": "moe_grouped_mlp_backward", "us": round(b_ms * 1e3, 1),
-            "tokens_per_s": round(T / (b_ms * 1e-3), 1),
-            "roofline": {"kernel": "expert-MLP backward: fc1 again, dA, dx, dW2, dW1 products plus transposes",
-                         "bound": "mfma", "achieved": round(tf, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                         "frac": round(tf / PEAK_BF16_TFLOPS, 4), "traffic": None,
-                         "algorithmic_flops_per_launch": fl, "avg_launch_us": round(b_ms * 1e3, 2)},
-        }
-        del bws, gout, dx, dw1, dw2
 
     if not args.no_cpu_baseline:
         import oracle

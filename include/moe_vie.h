@@ -177,7 +177,7 @@ moe_status_t moe_layer_forward(const moe_desc_t *desc, const void *x, const void
                                void *const *events, void *stream);
 
 /* Bytes of device workspace that moe_grouped_mlp_backward needs for `desc`
- * (bf16 layers with GELU experts). Writes *bytes; validates desc. */
+ * (bf16 layers). Writes *bytes; validates desc. */
 moe_status_t moe_backward_workspace_size(const moe_desc_t *desc, size_t *bytes);
 
 /* Backward of stage 4 for training (the grouped GEMMs of the paper's training
@@ -193,11 +193,19 @@ moe_status_t moe_backward_workspace_size(const moe_desc_t *desc, size_t *bytes);
  *   dx  [T, d] bf16 out: the K slot gradients summed in fp32 in slot order,
  *       rounded once
  *   dw1 [E, h, d] and dw2 [E, d, h] fp32 out; experts with no slots get 0
- * As in the forward, GELU(p) is rounded to bf16 (dw2 uses that value); dH is
- * rounded to bf16, the operand of the dx and dw1 products; every product
- * accumulates in fp32. bf16 layers with GELU experts only (other layers:
- * MOE_ERR_UNSUPPORTED). Deterministic: no atomics. Uses its own workspace
- * (moe_backward_workspace_size), 256-byte aligned. */
+ * SwiGLU experts (MOE_FLAG_SWIGLU; w1 = w13 [E, 2h, d], w2 [E, d, ldh]): with
+ * g_n = W1[e] x_t, u_n = W3[e] x_t and dA_n = W2[e]^T G_n,
+ *   dG_n = dA_n * u_n * SiLU'(g_n),  dU_n = dA_n * SiLU(g_n)
+ *   dx[t]   = sum over j of W1[e]^T dG_n + W3[e]^T dU_n
+ *   dw1[e]  = [E, 2h, d] fp32: rows 0..h-1 sum dG_n x_t^T, rows h..2h-1 dU_n x_t^T
+ *   dw2[e]  = [E, d, ldh] fp32, the layout of w2: columns < h sum G_n a_n^T
+ *             (a_n = SiLU(g_n) * u_n), padding columns 0
+ * As in the forward, the activation is rounded to bf16 (dw2 uses that
+ * value); the pre-activation gradient (dH, or dG and dU) is rounded to bf16,
+ * the operand of the dx and dw1 products; every product accumulates in fp32.
+ * bf16 layers only (fp32 layers: MOE_ERR_UNSUPPORTED). Deterministic: no
+ * atomics. Uses its own workspace (moe_backward_workspace_size), 256-byte
+ * aligned. */
 moe_status_t moe_grouped_mlp_backward(const moe_desc_t *desc, const void *x, const int32_t *sorted_slots,
                                       const int32_t *offsets, const void *w1, const void *w2,
                                       const void *grad_expert_out, void *dx, float *dw1, float *dw2,

@@ -10,20 +10,30 @@ namespace {
 
 constexpr int TT = 64;  // transpose tile (rows x columns)
 
-// out[g][c][r] = in[g][r][c] for a [G][R][C] bf16 tensor (R, C multiples of
-// 64). One 64 x 64 tile per workgroup through LDS: 16-byte row pieces in,
-// 16-byte pieces of the transposed rows out.
-__global__ __launch_bounds__(256) void k_transpose_w(const bf16_t* __restrict__ in, int R, int C,
-                                                    bf16_t* __restrict__ out) {
+// out[g][c][r] = in[g][src(r)][c]: the transpose of a [G][Rs][C] bf16 tensor
+// viewed as R rows (R, C multiples of 64). Without padding (ld = 0) src(r) =
+// r and R = Rs. With padding (stacked gate and up rows of h each, ld = h
+// rounded up to 64, R = 2 ld): rows r < ld are gate row r, rows ld + i are up
+// row h + i, and rows past h in either half are zero. One 64 x 64 tile per
+// workgroup through LDS: 16-byte row pieces in, 16-byte pieces of the
+// transposed rows out.
+__global__ __launch_bounds__(256) void k_transpose_w(const bf16_t* __restrict__ in, int Rs, int R, int C, int h,
+                                                    int ld, bf16_t* __restrict__ out) {
     __shared__ bf16_t tile[TT][TT + 2];
     const int r0 = blockIdx.x * TT, c0 = blockIdx.y * TT;
     const size_t g = blockIdx.z;
-    const bf16_t* src = in + g * (size_t)R * C;
+    const bf16_t* src = in + g * (size_t)Rs * C;
     bf16_t* dst = out + g * (size_t)R * C;
     const int tid = threadIdx.x;
     for (int q = tid; q < TT * TT / 8; q += 256) {
         const int r = q / (TT / 8), c = (q % (TT / 8)) * 8;
-        const uint4 v = *reinterpret_cast<const uint4*>(src + (size_t)(r0 + r) * C + c0 + c);
+        int sr = r0 + r;
+        if (ld > 0) {
+            const int up = sr >= ld, i = sr - (up ? ld : 0);
+            sr = i < h ? i + (up ? h : 0) : -1;
+        }
+        uint4 v = make_uint4(0u, 0u, 0u, 0u);
+        if (sr >= 0) v = *reinterpret_cast<const uint4*>(src + (size_t)sr * C + c0 + c);
         const bf16_t* e = reinterpret_cast<const bf16_t*>(&v);
 #pragma unroll
         for (int k = 0; k < 8; ++k) tile[r][c + k] = e[k];
@@ -178,6 +188,21 @@ __global__ __launch_bounds__(256) void k_transpose_window(const bf16_t* __restri
     }
 }
 
+// out[g][r][:] = in[g][src(r)][:] for the 2h stacked rows of a [G][2 ld][C]
+// fp32 tensor (src(r) = r for r < h, ld + r - h after): the padded weight
+// gradient of stacked gate and up rows back to the unpadded layout.
+__global__ __launch_bounds__(256) void k_compact_rows(const float* __restrict__ in, int G, int h, int ld, int C,
+                                                     float* __restrict__ out) {
+    const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const size_t q = C / 4;
+    if (i >= (size_t)G * 2 * h * q) return;
+    const size_t row = i / q, g = row / (2 * h);
+    const int r = (int)(row - g * 2 * h), c = (int)(i % q) * 4;
+    const int sr = r < h ? r : ld + r - h;
+    *reinterpret_cast<float4*>(out + row * C + c) =
+        *reinterpret_cast<const float4*>(in + (g * 2 * ld + sr) * (size_t)C + c);
+}
+
 __device__ __forceinline__ uint32_t pack2_bf16_rne(float lo, float hi) {
     uint32_t a = __float_as_uint(lo), b = __float_as_uint(hi);
     a += 0x7fffu + ((a >> 16) & 1u);
@@ -211,8 +236,20 @@ __global__ __launch_bounds__(256) void k_slot_sum(const float* __restrict__ dxs,
 }  // namespace
 
 hipError_t launch_transpose_w(const void* in, int G, int R, int C, void* out, hipStream_t s) {
-    hipLaunchKernelGGL(k_transpose_w, dim3(R / TT, C / TT, G), dim3(256), 0, s, static_cast<const bf16_t*>(in), R,
-                       C, static_cast<bf16_t*>(out));
+    hipLaunchKernelGGL(k_transpose_w, dim3(R / TT, C / TT, G), dim3(256), 0, s, static_cast<const bf16_t*>(in), R, R,
+                       C, 0, 0, static_cast<bf16_t*>(out));
+    return hipGetLastError();
+}
+
+hipError_t launch_transpose_w13(const void* in, int G, int h, int ld, int C, void* out, hipStream_t s) {
+    hipLaunchKernelGGL(k_transpose_w, dim3(2 * ld / TT, C / TT, G), dim3(256), 0, s, static_cast<const bf16_t*>(in),
+                       2 * h, 2 * ld, C, h, ld, static_cast<bf16_t*>(out));
+    return hipGetLastError();
+}
+
+hipError_t launch_compact_rows(const float* in, int G, int h, int ld, int C, float* out, hipStream_t s) {
+    const size_t n = (size_t)G * 2 * h * (C / 4);
+    hipLaunchKernelGGL(k_compact_rows, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, in, G, h, ld, C, out);
     return hipGetLastError();
 }
 

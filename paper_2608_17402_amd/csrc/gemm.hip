@@ -104,6 +104,14 @@ __device__ __forceinline__ float silu_as(float v) {
     return v * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(v * -1.44269504f));
 }
 
+// Gradients of SiLU(g) * u from the gradient da of the product: (dg, du) =
+// (da u SiLU'(g), da SiLU(g)), SiLU'(g) = s (1 + g (1 - s)), s = Sigmoid(g).
+__device__ __forceinline__ void swiglu_grad(float g, float u, float da, float& dg, float& du) {
+    const float sg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(g * -1.44269504f));
+    dg = da * u * (sg * fmaf(g, 1.0f - sg, 1.0f));
+    du = da * (g * sg);
+}
+
 // SwiGLU activation of one column: SiLU(gate) * up, or 0 past the valid width.
 __device__ __forceinline__ float swiglu_col(float g, float u, bool valid) {
     return valid ? silu_as(g) * u : 0.0f;
@@ -139,7 +147,9 @@ __device__ __forceinline__ TileCoord locate_wgrad_tile(const GemmArgs& a, int bm
 __device__ __forceinline__ int weight_rows(const GemmArgs& a) { return a.b_rows > 0 ? a.b_rows : a.N; }
 
 // Epilogues of a first expert layer: their token rows are gathered from x.
-__host__ __device__ constexpr bool fc1_epi(int epi) { return epi == EPI_GELU_STORE || epi == EPI_SWIGLU_STORE; }
+__host__ __device__ constexpr bool fc1_epi(int epi) {
+    return epi == EPI_GELU_STORE || epi == EPI_SWIGLU_STORE || epi == EPI_SWIGLU_BWD;
+}
 
 // d/dx GELU(x) = Phi(x) + x phi(x) from the same approximation: Q =
 // erfc(|x| / sqrt 2) / 2 as in gelu_as, Phi(x) = 1 - Q for x >= 0 and Q
@@ -267,7 +277,7 @@ void k_gemm_bf16(const GemmArgs a) {
     __shared__ int32_t srow[BM];
     constexpr bool WGRAD = EPI == EPI_WGRAD_F32;
     // A rows gathered through the row map (first layers, the backward's dA).
-    constexpr bool A_GATHER = fc1_epi(EPI) || EPI == EPI_GELU_BWD || EPI == EPI_DGELU;
+    constexpr bool A_GATHER = fc1_epi(EPI) || EPI == EPI_GELU_BWD || EPI == EPI_DGELU || EPI == EPI_DSWIGLU;
     // Output rows scattered to slot order (second layer, the backward's dx).
     constexpr bool O_SCATTER = EPI == EPI_SCATTER_SLOT || EPI == EPI_SCATTER_SLOT_F32;
     const TileCoord tc = WGRAD ? locate_wgrad_tile(a, BM, BN) : locate_tile<GROUPED>(a, BM, BN);
@@ -289,7 +299,8 @@ void k_gemm_bf16(const GemmArgs a) {
     }
     __syncthreads();
 
-    constexpr bool SWIGLU = EPI == EPI_SWIGLU_STORE;
+    constexpr bool SWIGLU = EPI == EPI_SWIGLU_STORE || EPI == EPI_SWIGLU_BWD;
+    constexpr bool DSW = EPI == EPI_DSWIGLU;  // two bf16 outputs per element (dG, dU)
     constexpr int HW = WTN / 2;  // SwiGLU: activation columns per wave
     static_assert(!SWIGLU || FN % 2 == 0, "SwiGLU waves hold gate and up blocks in pairs");
     const int Kd = a.Kdim;
@@ -446,7 +457,7 @@ void k_gemm_bf16(const GemmArgs a) {
     // 16-byte row pieces so that consecutive lanes store whole 128-byte lines.
     constexpr bool OUT_F32 = EPI == EPI_STORE_F32 || EPI == EPI_SCATTER_SLOT_F32 || WGRAD;
     constexpr int OES = OUT_F32 ? 4 : 2;           // output element size
-    constexpr int SEG = (SWIGLU ? HW : WTN) * OES; // bytes of one wave-tile row
+    constexpr int SEG = (SWIGLU ? HW : WTN) * OES * (DSW ? 2 : 1);  // bytes of one wave-tile row
     constexpr int RSTR = SEG + 16;                 // padded LDS row stride
     constexpr int CPRO = SEG / 16;                 // 16-byte pieces per row
     constexpr int PIECES = 32 * CPRO / kWave;      // pieces per lane per block
@@ -457,10 +468,33 @@ void k_gemm_bf16(const GemmArgs a) {
     // First output column of this wave's rows (SwiGLU: activation column,
     // rows act_ld apart).
     const int ocol0 = SWIGLU ? tc.n0 / 2 + wn * HW : tc.n0 + wn * WTN;
-    const size_t ostride = SWIGLU ? (size_t)a.act_ld : (size_t)a.N;
+    const size_t ostride = SWIGLU ? (size_t)a.act_ld : (DSW ? 2 * (size_t)a.act_ld : (size_t)a.N);
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
-        if constexpr (SWIGLU) {
+        if constexpr (DSW) {
+            // dG in the first half of the staging row, dU in the second.
+            const int r = wm * WTM + i * 32 + fr;
+            const float* grow = static_cast<const float*>(a.aux) +
+                                (size_t)(tc.row0 + (r < tc.rows ? r : tc.rows - 1)) * 2 * a.act_ld + ocol0;
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int c = j * 32 + 8 * g + 4 * fk;
+                    const float4 gv = *reinterpret_cast<const float4*>(grow + c);
+                    const float4 uv = *reinterpret_cast<const float4*>(grow + a.act_ld + c);
+                    const float gg[4] = {gv.x, gv.y, gv.z, gv.w}, uu[4] = {uv.x, uv.y, uv.z, uv.w};
+                    float dg[4], du[4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        swiglu_grad(gg[q], uu[q], acc[j][i][4 * g + q], dg[q], du[q]);
+                        if (ocol0 + c + q >= a.act_n) dg[q] = du[q] = 0.0f;
+                    }
+                    *reinterpret_cast<uint2*>(stg + fr * RSTR + c * 2) = pack4_bf16(dg[0], dg[1], dg[2], dg[3]);
+                    *reinterpret_cast<uint2*>(stg + fr * RSTR + (WTN + c) * 2) =
+                        pack4_bf16(du[0], du[1], du[2], du[3]);
+                }
+        } else if constexpr (SWIGLU) {
 #pragma unroll
             for (int j = 0; j < FN / 2; ++j)
 #pragma unroll
@@ -514,11 +548,57 @@ void k_gemm_bf16(const GemmArgs a) {
                     orow += (size_t)(item.pad < 0 ? item.e : item.pad) * a.dense_rows;
                     if (item.pad >= 0) obase = a.C2;
                 }
-                uint8_t* out = static_cast<uint8_t*>(obase) + (orow * ostride + ocol0) * OES + pc * 16;
+                size_t ocol = (size_t)ocol0;
+                int pcc = pc;
+                if (DSW && pc >= CPRO / 2) {  // the dU half goes act_ld columns further on
+                    ocol += a.act_ld;
+                    pcc -= CPRO / 2;
+                }
+                uint8_t* out = static_cast<uint8_t*>(obase) + (orow * ostride + ocol) * OES + pcc * 16;
                 *reinterpret_cast<uint4*>(out) = v;
             }
         }
         wave_sync_lds();
+    }
+    if constexpr (EPI == EPI_SWIGLU_BWD) {
+        // Second output: the fp32 gate and up pre-activations, G at column c and
+        // U at act_ld + c of C2's rows (2 act_ld), staged as [G | U] per row.
+        constexpr int SEG2 = 2 * HW * 4, RSTR2 = SEG2 + 16, CPRO2 = SEG2 / 16, PIECES2 = 32 * CPRO2 / kWave;
+        static_assert(NW * 32 * RSTR2 <= STAGES * STAGE, "epilogue staging must fit in the stage buffers");
+        __syncthreads();  // the wider rows overlap other waves' first-pass areas
+        uint8_t* stg2 = smem + wave * 32 * RSTR2;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+#pragma unroll
+            for (int j = 0; j < FN / 2; ++j)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int c = j * 32 + 8 * g + 4 * fk;
+                    *reinterpret_cast<float4*>(stg2 + fr * RSTR2 + c * 4) =
+                        make_float4(acc[j][i][4 * g + 0], acc[j][i][4 * g + 1], acc[j][i][4 * g + 2],
+                                    acc[j][i][4 * g + 3]);
+                    const int ju = j + FN / 2;
+                    *reinterpret_cast<float4*>(stg2 + fr * RSTR2 + (HW + c) * 4) =
+                        make_float4(acc[ju][i][4 * g + 0], acc[ju][i][4 * g + 1], acc[ju][i][4 * g + 2],
+                                    acc[ju][i][4 * g + 3]);
+                }
+            wave_sync_lds();
+#pragma unroll
+            for (int k = 0; k < PIECES2; ++k) {
+                const int q = lane + kWave * k;
+                const int rr = q / CPRO2, pc = q % CPRO2;
+                const int r = wm * WTM + i * 32 + rr;
+                const uint4 v = *reinterpret_cast<const uint4*>(stg2 + rr * RSTR2 + pc * 16);
+                if (r < tc.rows && ocol0 < a.act_ld) {
+                    const bool up = pc >= CPRO2 / 2;
+                    const size_t col = (size_t)ocol0 + (up ? a.act_ld : 0);
+                    uint8_t* out = static_cast<uint8_t*>(a.C2) +
+                                   ((size_t)(tc.row0 + r) * 2 * a.act_ld + col) * 4 + (pc - (up ? CPRO2 / 2 : 0)) * 16;
+                    *reinterpret_cast<uint4*>(out) = v;
+                }
+            }
+            wave_sync_lds();
+        }
     }
     if constexpr (EPI == EPI_GELU_BWD) {
         // Second output: the pre-activation (acc) in fp32 (rows of N), the same staging.
@@ -1680,6 +1760,16 @@ hipError_t dispatch_swiglu(int bm, GemmArgs a, hipStream_t s) {
     return hipErrorInvalidValue;
 }
 
+// Backward's first-layer recompute for SwiGLU experts: the tiled kernel with
+// 2 x 2 waves (each wave 32 gate + 32 up columns), N = 2 act_ld.
+hipError_t dispatch_swiglu_bwd(int bm, GemmArgs a, hipStream_t s) {
+    if (a.act_n < 1 || a.act_ld < a.act_n || a.act_ld % 64) return hipErrorInvalidValue;
+    a.N = 2 * a.act_ld;
+    if (bm == 256) return launch_bf16<256, 128, 2, 2, 64, 2, 1, EPI_SWIGLU_BWD, true>(a, s);
+    if (bm == 64) return launch_bf16<64, 128, 2, 2, 64, 3, 2, EPI_SWIGLU_BWD, true>(a, s);
+    return hipErrorInvalidValue;
+}
+
 template <bool GROUPED>
 hipError_t dispatch(const moe_desc_t& d, int epilogue, int bm, const GemmArgs& a, hipStream_t s) {
     if (d.dtype == MOE_BF16) {
@@ -1697,6 +1787,12 @@ hipError_t dispatch(const moe_desc_t& d, int epilogue, int bm, const GemmArgs& a
                 break;
             case EPI_WGRAD_F32:
                 if (GROUPED && a.dense_rows % bm == 0) return dispatch_tiled<EPI_WGRAD_F32, true>(bm, a, s);
+                break;
+            case EPI_SWIGLU_BWD:
+                if (GROUPED) return dispatch_swiglu_bwd(bm, a, s);
+                break;
+            case EPI_DSWIGLU:
+                if (GROUPED) return dispatch_tiled<EPI_DSWIGLU, true>(bm, a, s);
                 break;
             case EPI_SCATTER_SLOT:
                 if (GROUPED) return dispatch_bf16<EPI_SCATTER_SLOT, true>(bm, a, s);

@@ -69,16 +69,16 @@ moe_status_t check_desc(const moe_desc_t* d) {
     return MOE_OK;
 }
 
-// The backward supports bf16 layers with GELU experts; its transposed
+// The backward supports bf16 layers (GELU or SwiGLU experts); its transposed
 // operands and slot gradients are addressed through 32-bit buffer offsets.
 moe_status_t check_backward_desc(const moe_desc_t* d) {
     const moe_status_t st = check_desc(d);
     if (st != MOE_OK) return st;
     if (d->dtype != MOE_BF16) return fail(MOE_ERR_UNSUPPORTED, "the backward needs a bf16 layer");
-    if (d->flags & MOE_FLAG_SWIGLU) return fail(MOE_ERR_UNSUPPORTED, "the backward supports GELU experts only");
     const uint64_t lim = (uint64_t)1 << 32, TK = (uint64_t)d->T * d->K;
     const uint64_t ld = TK + 128 * (uint64_t)d->E + 64;
-    if (TK * d->d * 2 >= lim || (uint64_t)(d->d > d->h ? d->d : d->h) * ld * 2 >= lim)
+    const uint64_t hw = (uint64_t)act_stride(*d, d->h) * ((d->flags & MOE_FLAG_SWIGLU) ? 2 : 1);
+    if (TK * d->d * 2 >= lim || TK * hw * 2 >= lim || (uint64_t)(d->d > hw ? d->d : hw) * ld * 2 >= lim)
         return fail(MOE_ERR_UNSUPPORTED, "the backward's slot or transposed operands exceed 4 GiB");
     return MOE_OK;
 }
@@ -178,21 +178,26 @@ BackwardPlan plan_backward(const moe_desc_t& d) {
         off = align_up(off + bytes);
         return o;
     };
-    b.dgelu = take(TK * d.h * 4);
-    b.w1t = take((size_t)d.E * d.h * d.d * 2);
-    b.w2t = take((size_t)d.E * d.h * d.d * 2);
-    b.dh = take(TK * d.h * 2);
+    const bool sw = d.flags & MOE_FLAG_SWIGLU;
+    b.hh = act_stride(d, d.h);
+    b.hw = sw ? 2 * b.hh : b.hh;
+    const size_t hh = b.hh, hw = b.hw;
+    b.pre = take(TK * hw * 4);
+    b.w1t = take((size_t)d.E * d.d * hw * 2);
+    b.w2t = take((size_t)d.E * hh * d.d * 2);
+    b.dh = take(TK * hw * 2);
     b.dxs = take(TK * d.d * 4);
     b.koff = take(((size_t)d.E + 1) * 4);
     b.gt = take((size_t)d.d * b.ld * 2);
-    b.at = take((size_t)d.h * b.ld * 2);
-    b.dht = take((size_t)d.h * b.ld * 2);
+    b.at = take(hh * b.ld * 2);
+    b.dht = take(hw * b.ld * 2);
     b.xt = take((size_t)d.d * b.ld * 2);
     b.items_max = d.E + (int32_t)(((size_t)b.ld / 64 + kWgradSlabs - 1) / kWgradSlabs);
     b.items = take((size_t)b.items_max * sizeof(TileDesc));
     b.rlist = take((size_t)d.E * sizeof(TileDesc));
     b.wcount = take(16);
-    b.partials = take((size_t)b.items_max * d.d * d.h * 4);
+    b.partials = take((size_t)b.items_max * d.d * hw * 4);
+    b.dw1p = (sw && b.hh != d.h) ? take((size_t)d.E * hw * d.d * 4) : 0;
     b.total = off;
     return b;
 }
@@ -328,35 +333,39 @@ static moe_status_t enqueue_shared_mlp(const moe_desc_t& d, const WorkspacePlan&
     return MOE_OK;
 }
 
-// Backward of the routed experts (GELU, bf16): recompute fc1 keeping the fp32
-// pre-activation P, dH = (G W2) * GELU'(P) with G the output gradients
-// gathered by slot (GELU' formed in that product's epilogue), the slot
-// gradients of x dH W1 (fp32, slot order) summed per token, and the weight
-// gradients as K-windowed products of transposed operands.
+// Backward of the routed experts (bf16). fc1 again keeps the fp32
+// pre-activations P (SwiGLU: gate G and up U, stacked); dH is (Gout W2) times
+// GELU'(P) (SwiGLU: dG and dU from G and U), formed in that product's epilogue
+// with Gout the output gradients gathered by slot; the slot gradients of x are
+// dH W1 (fp32, slot order) summed per token; the weight gradients are
+// K-windowed products of slab-major transposed operands.
 static moe_status_t enqueue_backward(const moe_desc_t& d, const BackwardPlan& b, void* ws, const void* x,
                                      const int32_t* sorted_slots, const int32_t* offsets, const void* w1,
                                      const void* w2, const void* gout, void* dx, float* dw1, float* dw2,
                                      hipStream_t s) {
     const WorkspacePlan& p = b.fwd;
+    const bool sw = d.flags & MOE_FLAG_SWIGLU;
     const size_t TK = (size_t)d.T * d.K;
+    const int hh = b.hh, hw = b.hw;
     TileDesc* tiles = region<TileDesc>(ws, p.tiles);
     int32_t* ntiles = region<int32_t>(ws, p.ntiles);
     void* act = region<void>(ws, p.act);
-    float* dgelu = region<float>(ws, b.dgelu);
+    float* pre = region<float>(ws, b.pre);
     void* w1t = region<void>(ws, b.w1t);
     void* w2t = region<void>(ws, b.w2t);
     void* dh = region<void>(ws, b.dh);
     float* dxs = region<float>(ws, b.dxs);
     int32_t* koff = region<int32_t>(ws, b.koff);
     HIP_CHECK(launch_build_tiles(d.E, p.tile_bm, p.max_tiles, offsets, tiles, ntiles, s), "build_tiles");
-    HIP_CHECK(launch_transpose_w(w1, d.E, d.h, d.d, w1t, s), "transpose w1");
-    HIP_CHECK(launch_transpose_w(w2, d.E, d.d, d.h, w2t, s), "transpose w2");
+    if (sw) HIP_CHECK(launch_transpose_w13(w1, d.E, d.h, hh, d.d, w1t, s), "transpose w13");
+    else HIP_CHECK(launch_transpose_w(w1, d.E, d.h, d.d, w1t, s), "transpose w1");
+    HIP_CHECK(launch_transpose_w(w2, d.E, d.d, hh, w2t, s), "transpose w2");
 
-    GemmArgs g{};  // fc1 again: the activation (bf16) and the pre-activation (fp32)
+    GemmArgs g{};  // fc1 again: the activation (bf16) and the pre-activations (fp32)
     g.A = x;
     g.B = w1;
     g.C = act;
-    g.C2 = dgelu;
+    g.C2 = pre;
     g.row_map = sorted_slots;
     g.tiles = tiles;
     g.n_tiles = ntiles;
@@ -365,19 +374,23 @@ static moe_status_t enqueue_backward(const moe_desc_t& d, const BackwardPlan& b,
     g.route_k = d.K;
     g.row_mode = ROWS_GATHER_TOKENS;
     g.max_tiles = p.max_tiles;
-    g.b_group_stride = (int64_t)d.h * d.d;
+    g.b_group_stride = (int64_t)(sw ? 2 : 1) * d.h * d.d;
     g.a_bytes = (uint32_t)((size_t)d.T * d.d * 2);
-    HIP_CHECK(launch_gemm(d, EPI_GELU_BWD, p.tile_bm, g, s), "backward fc1");
+    g.act_n = d.h;
+    g.act_ld = hh;
+    HIP_CHECK(launch_gemm(d, sw ? EPI_SWIGLU_BWD : EPI_GELU_BWD, p.tile_bm, g, s), "backward fc1");
 
-    GemmArgs ga = g;  // dH = (G W2) * GELU'(P)
+    GemmArgs ga = g;  // dH from Gout W2 and the pre-activations
     ga.A = gout;
     ga.B = w2t;
     ga.C = dh;
     ga.C2 = nullptr;
-    ga.aux = dgelu;
+    ga.aux = pre;
+    ga.N = hh;
+    ga.b_group_stride = (int64_t)hh * d.d;
     ga.row_mode = ROWS_GATHER_SLOTS;
     ga.a_bytes = (uint32_t)(TK * d.d * 2);
-    HIP_CHECK(launch_gemm(d, EPI_DGELU, p.tile_bm, ga, s), "backward dA");
+    HIP_CHECK(launch_gemm(d, sw ? EPI_DSWIGLU : EPI_DGELU, p.tile_bm, ga, s), "backward dA");
 
     GemmArgs gx = g;  // slot gradients of x: dH W1, fp32 to slot order
     gx.A = dh;
@@ -385,9 +398,10 @@ static moe_status_t enqueue_backward(const moe_desc_t& d, const BackwardPlan& b,
     gx.C = dxs;
     gx.C2 = nullptr;
     gx.N = d.d;
-    gx.Kdim = d.h;
+    gx.Kdim = hw;
+    gx.b_group_stride = (int64_t)d.d * hw;
     gx.row_mode = ROWS_IDENTITY;
-    gx.a_bytes = (uint32_t)(TK * d.h * 2);
+    gx.a_bytes = (uint32_t)(TK * hw * 2);
     HIP_CHECK(launch_gemm(d, EPI_SCATTER_SLOT_F32, p.tile_bm, gx, s), "backward dx");
     HIP_CHECK(launch_slot_sum(dxs, d.T, d.K, d.d, dx, s), "slot sum");
 
@@ -403,9 +417,9 @@ static moe_status_t enqueue_backward(const moe_desc_t& d, const BackwardPlan& b,
     HIP_CHECK(launch_wgrad_plan(offsets, d.E, koff, items, rlist, wcount, s), "weight-gradient plan");
     HIP_CHECK(launch_transpose_window(gout, d.d, SRC_SLOT, sorted_slots, d.K, offsets, koff, d.E, gt, b.ld, s),
               "transpose G");
-    HIP_CHECK(launch_transpose_window(act, d.h, SRC_SORTED, sorted_slots, d.K, offsets, koff, d.E, at, b.ld, s),
+    HIP_CHECK(launch_transpose_window(act, hh, SRC_SORTED, sorted_slots, d.K, offsets, koff, d.E, at, b.ld, s),
               "transpose A");
-    HIP_CHECK(launch_transpose_window(dh, d.h, SRC_SORTED, sorted_slots, d.K, offsets, koff, d.E, dht, b.ld, s),
+    HIP_CHECK(launch_transpose_window(dh, hw, SRC_SORTED, sorted_slots, d.K, offsets, koff, d.E, dht, b.ld, s),
               "transpose dH");
     HIP_CHECK(launch_transpose_window(x, d.d, SRC_TOKEN, sorted_slots, d.K, offsets, koff, d.E, xt, b.ld, s),
               "transpose x");
@@ -429,8 +443,14 @@ static moe_status_t enqueue_backward(const moe_desc_t& d, const BackwardPlan& b,
         HIP_CHECK(launch_wgrad_reduce(partials, rlist, wcount, d.E, (size_t)m * n, out, s), what);
         return MOE_OK;
     };
-    CHECK(wgrad(gt, d.d, at, d.h, dw2, "dW2"));
-    CHECK(wgrad(dht, d.h, xt, d.d, dw1, "dW1"));
+    CHECK(wgrad(gt, d.d, at, hh, dw2, "dW2"));
+    if (b.dw1p) {  // SwiGLU with padded halves: compute padded, then drop the padding rows
+        float* dw1p = region<float>(ws, b.dw1p);
+        CHECK(wgrad(dht, hw, xt, d.d, dw1p, "dW13"));
+        HIP_CHECK(launch_compact_rows(dw1p, d.E, d.h, hh, d.d, dw1, s), "dW13 rows");
+    } else {
+        CHECK(wgrad(dht, hw, xt, d.d, dw1, "dW1"));
+    }
     return MOE_OK;
 }
 

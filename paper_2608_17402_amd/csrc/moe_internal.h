@@ -54,6 +54,12 @@ enum GemmEpilogue : int {
                             // i = tiles[i] = {e, k0, klen, dest} sums K columns
                             // k0 .. k0 + klen (multiples of 64) of rows m into C[e][m, :] (dest < 0) or into
                             // the partial block C2[dest] [dense_rows, N]; *n_tiles items
+    // Backward of SwiGLU experts (tiled kernel only):
+    EPI_SWIGLU_BWD = 9,     // EPI_SWIGLU_STORE, and the fp32 gate and up pre-activations into C2
+                            // [rows, 2 act_ld]: G at column c, U at column act_ld + c
+    EPI_DSWIGLU = 10,       // dA = acc (N = act_ld columns); with G, U from aux [rows, 2 act_ld] (fp32):
+                            // C[p, c] = bf16(dA U SiLU'(G)), C[p, act_ld + c] = bf16(dA SiLU(G)) for
+                            // c < act_n, 0 for act_n <= c < act_ld
 };
 
 struct GemmArgs {
@@ -73,7 +79,7 @@ struct GemmArgs {
     int32_t b_rows;            // dense bf16 only: rows of B that exist (0 = N); rows past them read as zeros
     uint32_t a_bytes;          // bytes of the A operand buffer (bounds of its buffer resource)
     void* C2;                  // EPI_GELU_BWD: second output (fp32); EPI_WGRAD_F32: partial blocks
-    const void* aux;           // EPI_DGELU: the pre-activation (fp32, rows of N)
+    const void* aux;           // EPI_DGELU: the pre-activation (fp32, rows of N); EPI_DSWIGLU: G, U
     int32_t act_n;             // EPI_SWIGLU_STORE: activation width h (valid columns)
     int32_t act_ld;            // EPI_SWIGLU_STORE: activation row stride (h rounded up to 128)
     const float* gate;         // EPI_COMBINE: gates [rows, route_k]
@@ -99,15 +105,19 @@ WorkspacePlan plan_workspace(const moe_desc_t& d);
 // activation), then the backward's own regions.
 struct BackwardPlan {
     WorkspacePlan fwd;
-    size_t dgelu;            // pre-activation W1 x [T*K, h] fp32, sorted order
-    size_t w1t, w2t;         // transposed weights [E, d, h] and [E, h, d]
-    size_t dh;               // pre-activation gradient [T*K, h] bf16, sorted order
+    // hh = activation row stride (h, or ldh for SwiGLU); hw = pre-activation
+    // width (hh, or 2 ldh for SwiGLU: gate columns then up columns).
+    size_t pre;              // pre-activations [T*K, hw] fp32, sorted order
+    size_t w1t, w2t;         // transposed weights [E, d, hw] and [E, hh, d]
+    size_t dh;               // pre-activation gradient [T*K, hw] bf16, sorted order
     size_t dxs;              // slot gradients of x [T*K, d] fp32, slot order
     size_t koff;             // [E + 1] K-window starts
-    size_t gt, at, dht, xt;  // transposed operands [d | h, ld] bf16
+    size_t gt, at, dht, xt;  // transposed operands [d | hh | hw, ld] bf16
     size_t items, rlist;     // weight-gradient work items and split experts (TileDesc each)
     size_t wcount;           // [4] int32: item count, split-expert count
-    size_t partials;         // [parts_max, d, h] fp32 partial sums of split experts
+    size_t partials;         // [items_max, d, hw] fp32 partial sums of split experts
+    size_t dw1p;             // SwiGLU with h < ldh: padded [E, hw, d] fp32 first-layer gradient, else 0
+    int32_t hh, hw;
     int32_t ld;              // row length of the transposed operands: T*K + 128 E, rounded up to 64
     int32_t items_max;       // bound on the work items (and on the partial blocks)
     size_t total;
@@ -151,6 +161,10 @@ bool gemm_combine_fusable(const moe_desc_t& d, int bm, int n, int kdim);
 // gather: rows already in sorted order, slot rows, token rows.
 enum TransposeSource : int { SRC_SORTED = 0, SRC_SLOT = 1, SRC_TOKEN = 2 };
 hipError_t launch_transpose_w(const void* in, int G, int R, int C, void* out, hipStream_t s);
+// Stacked gate/up weights [G][2h][C] -> [G][C][2 ld], rows padded to ld each.
+hipError_t launch_transpose_w13(const void* in, int G, int h, int ld, int C, void* out, hipStream_t s);
+// [G][2 ld][C] fp32 with padded gate/up halves -> [G][2h][C].
+hipError_t launch_compact_rows(const float* in, int G, int h, int ld, int C, float* out, hipStream_t s);
 // Longest K window of one weight-gradient work item, in 64-column slabs.
 constexpr int kWgradSlabs = 64;
 hipError_t launch_wgrad_plan(const int32_t* offsets, int E, int32_t* koff, TileDesc* items, TileDesc* rlist,

@@ -155,10 +155,12 @@ def test_backward_validation(lib):
     # at least the transposed operands: (2 d + 2 h) x (T*K + 64 E) bf16
     assert n.value >= (2 * 256 + 2 * 192) * (2000 + 64 * 8) * 2
     f32 = binding.make_desc(1000, 256, 8, 2, 192, 0, 1.0, "f32")
-    sw = binding.make_desc(1000, 256, 8, 2, 192, 0, 1.0, "bf16", flags=binding.MOE_FLAG_SWIGLU)
-    for desc in (f32, sw):
-        assert lib.moe_backward_workspace_size(ctypes.byref(desc), ctypes.byref(n)) == 2
-        assert lib.moe_last_error() != b""
+    assert lib.moe_backward_workspace_size(ctypes.byref(f32), ctypes.byref(n)) == 2
+    assert lib.moe_last_error() != b""
+    sw = binding.make_desc(1000, 256, 8, 2, 300, 0, 1.0, "bf16", flags=binding.MOE_FLAG_SWIGLU)
+    assert lib.moe_backward_workspace_size(ctypes.byref(sw), ctypes.byref(n)) == 0
+    # SwiGLU: the stacked pre-activation gradients are 2 * 320 wide
+    assert n.value >= (2 * 256 + 320 + 2 * 320) * (2000 + 128 * 8) * 2
     P, S = ctypes.c_void_p, ctypes.c_size_t
     fake = P(1 << 20)
     d = ctypes.byref(ok)

@@ -37,9 +37,11 @@ def _bf16(rng, shape, std):
     return f32_to_bf16_bits((rng.standard_normal(shape) * std).astype(np.float32))
 
 
-def run_backward(T, d, E, K, h, idx, x, w1, w2, g):
-    """Permute idx on the GPU, then the backward; returns host arrays."""
-    desc = binding.make_desc(T, d, E, K, h, 0, 1.0, "bf16")
+def run_backward(T, d, E, K, h, idx, x, w1, w2, g, swiglu=False):
+    """Permute idx on the GPU, then the backward; returns host arrays. SwiGLU:
+    w1 [E, 2h, d], w2 [E, d, ldh] (padded), dw1 [E, 2h, d], dw2 [E, d, ldh]."""
+    flags = binding.MOE_FLAG_SWIGLU if swiglu else 0
+    desc = binding.make_desc(T, d, E, K, h, 0, 1.0, "bf16", flags=flags)
     ws = binding.alloc_workspace(desc)
     counts = torch.empty(E, dtype=torch.int32, device="cuda")
     offsets = torch.empty(E + 1, dtype=torch.int32, device="cuda")
@@ -47,8 +49,8 @@ def run_backward(T, d, E, K, h, idx, x, w1, w2, g):
     binding.moe_permute(desc, dev(idx), counts, offsets, slots, ws)
     bws = binding.alloc_backward_workspace(desc)
     dx = torch.empty(T, d, dtype=torch.bfloat16, device="cuda")
-    dw1 = torch.empty(E, h, d, dtype=torch.float32, device="cuda")
-    dw2 = torch.empty(E, d, h, dtype=torch.float32, device="cuda")
+    dw1 = torch.empty(E, w1.shape[1], d, dtype=torch.float32, device="cuda")
+    dw2 = torch.empty(E, d, w2.shape[2], dtype=torch.float32, device="cuda")
     xd, w1d, w2d, gd = dev(x), dev(w1), dev(w2), dev(g)
     binding.moe_grouped_mlp_backward(desc, xd, slots, offsets, w1d, w2d, gd, dx, dw1, dw2, bws)
     torch.cuda.synchronize()
@@ -172,3 +174,39 @@ def test_backward_full_vitg_sampled():
             rdx, _, _ = oracle.expert_backward(x32[t:t + 1], w1f[e], w2f[e], g32[t * K + j:t * K + j + 1], True)
             ref[n_t] += rdx[0]
     check_grad(dx[tok], ref, "sampled dx")
+
+
+SW_CASES = {
+    # h = 300 (ldh 320): padded halves, compaction of dW13; 256-row tiles
+    "sw_h300": dict(T=3000, d=256, E=4, K=2, h=300),
+    # the paper's H layer widths (h = 854, ldh = 896) at 2400 tokens
+    "sw_vith_T2400": dict(T=2400, d=1280, E=31, K=7, h=854),
+    # d = 64: 64-row tiles; h = 40
+    "sw_h40_d64": dict(T=700, d=64, E=6, K=3, h=40),
+    # h a multiple of 64: no padding, dW13 written in place
+    "sw_h128": dict(T=900, d=128, E=5, K=2, h=128),
+}
+
+
+@pytest.mark.parametrize("name", sorted(SW_CASES))
+def test_swiglu_backward_matches_oracle(name):
+    from workloads import pad_last_dim
+
+    c = SW_CASES[name]
+    T, d, E, K, h = c["T"], c["d"], c["E"], c["K"], c["h"]
+    rng = np.random.default_rng(100 + len(name))
+    x = _bf16(rng, (T, d), 1.0)
+    w13 = _bf16(rng, (E, 2 * h, d), 0.05)
+    w2 = _bf16(rng, (E, d, h), 0.05)
+    g = _bf16(rng, (T * K, d), 0.5)
+    idx = _idx(rng, T, E, K)
+    w2p = pad_last_dim(w2, 64, fill=0x3F80)  # padding columns 1.0: they must not leak into anything
+    dx, dw13, dw2 = run_backward(T, d, E, K, h, idx, x, w13, w2p, g, swiglu=True)
+    ldh = w2p.shape[2]
+    assert dw13.shape == (E, 2 * h, d) and dw2.shape == (E, d, ldh)
+    assert np.all(dw2[:, :, h:] == 0)
+    rdx, rdw13, rdw2 = oracle.grouped_backward(bf16_bits_to_f32(x), idx, bf16_bits_to_f32(w13),
+                                               bf16_bits_to_f32(w2), bf16_bits_to_f32(g), True, act="swiglu")
+    check_grad(dx, rdx, f"{name} dx")
+    check_grad(dw13, rdw13, f"{name} dw13")
+    check_grad(dw2[:, :, :h], rdw2, f"{name} dw2")
