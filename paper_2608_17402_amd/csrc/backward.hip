@@ -137,15 +137,17 @@ __global__ __launch_bounds__(256) void k_wgrad_reduce(const float* __restrict__ 
 // in: [rows, C] bf16; out: [C, ld] bf16 stored slab-major, [ld / 64][C][64]
 // (element (c, q) at ((q / 64) C + c) 64 + q % 64), so that one 64-column K
 // slab of a product's operand tile is contiguous. C a multiple of 64.
-// Positions past koff[E] are left alone.
+// Positions past koff[E] are left alone. A workgroup moves 64 positions x CW
+// columns: gathered rows are read in CW * 2-byte runs.
+template <int CW>
 __global__ __launch_bounds__(256) void k_transpose_window(const bf16_t* __restrict__ in, int C, int mode,
                                                          const int32_t* __restrict__ row_map, int K,
                                                          const int32_t* __restrict__ offsets,
                                                          const int32_t* __restrict__ koff, int E,
-                                                         bf16_t* __restrict__ out, int ld) {
-    __shared__ bf16_t tile[TT][TT + 2];
+                                                         bf16_t* __restrict__ out) {
+    __shared__ bf16_t tile[TT][CW + 2];
     __shared__ int32_t srow[TT];
-    const int q0 = blockIdx.x * TT, c0 = blockIdx.y * TT;
+    const int q0 = blockIdx.x * TT, c0 = blockIdx.y * CW;
     const int total = koff[E];
     if (q0 >= total) return;  // uniform per workgroup
     const int tid = threadIdx.x;
@@ -168,8 +170,8 @@ __global__ __launch_bounds__(256) void k_transpose_window(const bf16_t* __restri
         srow[tid] = v;
     }
     __syncthreads();
-    for (int t = tid; t < TT * TT / 8; t += 256) {
-        const int r = t / (TT / 8), c = (t % (TT / 8)) * 8;
+    for (int t = tid; t < TT * CW / 8; t += 256) {
+        const int r = t / (CW / 8), c = (t % (CW / 8)) * 8;
         uint4 v = make_uint4(0u, 0u, 0u, 0u);
         if (srow[r] >= 0) v = *reinterpret_cast<const uint4*>(in + (size_t)srow[r] * C + c0 + c);
         const bf16_t* e = reinterpret_cast<const bf16_t*>(&v);
@@ -177,9 +179,9 @@ __global__ __launch_bounds__(256) void k_transpose_window(const bf16_t* __restri
         for (int k = 0; k < 8; ++k) tile[r][c + k] = e[k];
     }
     __syncthreads();
-    for (int t = tid; t < TT * TT / 8; t += 256) {
+    // total is a multiple of 64 and q0 < total: the whole tile is inside.
+    for (int t = tid; t < TT * CW / 8; t += 256) {
         const int c = t / (TT / 8), r = (t % (TT / 8)) * 8;
-        if (q0 + r >= total) continue;  // total is a multiple of 64: whole pieces
         uint4 v;
         bf16_t* e = reinterpret_cast<bf16_t*>(&v);
 #pragma unroll
@@ -270,8 +272,14 @@ hipError_t launch_wgrad_reduce(const float* partials, const TileDesc* rlist, con
 hipError_t launch_transpose_window(const void* in, int C, int mode, const int32_t* row_map, int K,
                                    const int32_t* offsets, const int32_t* koff, int E, void* out, int ld,
                                    hipStream_t s) {
-    hipLaunchKernelGGL(k_transpose_window, dim3(ld / TT, C / TT), dim3(256), 0, s, static_cast<const bf16_t*>(in),
-                       C, mode, row_map, K, offsets, koff, E, static_cast<bf16_t*>(out), ld);
+    if (C % 256 == 0)
+        hipLaunchKernelGGL(k_transpose_window<256>, dim3(ld / TT, C / 256), dim3(256), 0, s,
+                           static_cast<const bf16_t*>(in), C, mode, row_map, K, offsets, koff, E,
+                           static_cast<bf16_t*>(out));
+    else
+        hipLaunchKernelGGL(k_transpose_window<TT>, dim3(ld / TT, C / TT), dim3(256), 0, s,
+                           static_cast<const bf16_t*>(in), C, mode, row_map, K, offsets, koff, E,
+                           static_cast<bf16_t*>(out));
     return hipGetLastError();
 }
 
