@@ -953,7 +953,8 @@ void k_gemm_pp(const GemmArgs a) {
     constexpr bool BWD1 = EPI == EPI_GELU_BWD;  // bf16 GELU, then the fp32 pre-activation into C2
     constexpr bool DG = EPI == EPI_DGELU;       // bf16 of acc times GELU'(aux)
     constexpr bool GATHER = GROUPED && (fc1_epi(EPI) || BWD1 || DG);
-    constexpr bool SWIGLU = EPI == EPI_SWIGLU_STORE;
+    constexpr bool SWIGLU = EPI == EPI_SWIGLU_STORE || EPI == EPI_SWIGLU_BWD;
+    constexpr bool SWBWD = EPI == EPI_SWIGLU_BWD;  // and the fp32 gate / up pre-activations into C2
     constexpr bool SCATTER = EPI == EPI_SCATTER_SLOT || EPI == EPI_SCATTER_SLOT_F32;
     // Weight gradients: slab-major operands, a K window per work item, fp32
     // output to the expert's gradient or a partial block.
@@ -1410,6 +1411,46 @@ void k_gemm_pp(const GemmArgs a) {
                     }
                 }
             }
+            if constexpr (SWBWD) {
+                // Second output: the gate (q = 0) and up (q = 1) pre-activations
+                // of this wave's 64 activation columns as fp32 rows of C2
+                // [rows, 2 act_ld]: G at column c, U at act_ld + c.
+                const int ocol = t.n0 / 2 + wn * (WT / 2);
+#pragma unroll
+                for (int q = 0; q < 2; ++q) {
+                    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                    for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+                        for (int g = 0; g < 4; ++g) {
+                            const int j = 2 * q + jj;
+                            const u32x4_t v = {__float_as_uint(acc_read(acc[j][i][4 * g + 0])),
+                                               __float_as_uint(acc_read(acc[j][i][4 * g + 1])),
+                                               __float_as_uint(acc_read(acc[j][i][4 * g + 2])),
+                                               __float_as_uint(acc_read(acc[j][i][4 * g + 3]))};
+                            const int chunk = 8 * jj + 2 * g + fk;
+                            lds_write16_asm(wrow + ((uint32_t)(chunk ^ sw) << 4), v);
+                        }
+                    u32x4_t v[8];
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) {
+                        const int rr = (lane >> 4) + 4 * k;
+                        v[k] = lds_read16u_asm(stg + (uint32_t)rr * 256u + ((uint32_t)((lane & 15) ^ (rr & 15)) << 4));
+                    }
+                    wait_lgkmcnt0();
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) tie(v[k]);
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) {
+                        const int r = wm * WT + i * 32 + (lane >> 4) + 4 * k;
+                        if (r < t.rows && ocol < a.act_ld)
+                            store16_asm(static_cast<uint8_t*>(a.C2) +
+                                            ((size_t)(t.row0 + r) * 2 * a.act_ld + q * a.act_ld + ocol) * 4 +
+                                            (lane & 15) * 16,
+                                        v[k]);
+                    }
+                }
+            }
             if constexpr (BWD1) {
                 // Second output: the pre-activation (acc) as fp32 rows of C2,
                 // two 64-column halves through the same staging rows.
@@ -1760,10 +1801,15 @@ hipError_t dispatch_swiglu(int bm, GemmArgs a, hipStream_t s) {
     return hipErrorInvalidValue;
 }
 
-// Backward's first-layer recompute for SwiGLU experts: the tiled kernel with
-// 2 x 2 waves (each wave 32 gate + 32 up columns), N = 2 act_ld.
+// Backward's first-layer recompute for SwiGLU experts: the persistent kernel
+// (as the forward), else the tiled kernel with 2 x 2 waves (each wave 32 gate
+// + 32 up columns), N = 2 act_ld.
 hipError_t dispatch_swiglu_bwd(int bm, GemmArgs a, hipStream_t s) {
     if (a.act_n < 1 || a.act_ld < a.act_n || a.act_ld % 64) return hipErrorInvalidValue;
+    if (bm == 256 && a.Kdim >= 128) {
+        a.N = 2 * ((a.act_ld + 127) / 128 * 128);
+        return launch_pp<EPI_SWIGLU_BWD, true>(a, s);
+    }
     a.N = 2 * a.act_ld;
     if (bm == 256) return launch_bf16<256, 128, 2, 2, 64, 2, 1, EPI_SWIGLU_BWD, true>(a, s);
     if (bm == 64) return launch_bf16<64, 128, 2, 2, 64, 3, 2, EPI_SWIGLU_BWD, true>(a, s);
