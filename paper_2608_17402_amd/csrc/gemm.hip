@@ -952,7 +952,8 @@ void k_gemm_pp(const GemmArgs a) {
     static_assert(AP == 8 && BP == 8, "copy schedule is written for 8 + 8 pieces");
     constexpr bool BWD1 = EPI == EPI_GELU_BWD;  // bf16 GELU, then the fp32 pre-activation into C2
     constexpr bool DG = EPI == EPI_DGELU;       // bf16 of acc times GELU'(aux)
-    constexpr bool GATHER = GROUPED && (fc1_epi(EPI) || BWD1 || DG);
+    constexpr bool DSW = EPI == EPI_DSWIGLU;    // dG and dU (bf16) from acc and the stored G, U
+    constexpr bool GATHER = GROUPED && (fc1_epi(EPI) || BWD1 || DG || DSW);
     constexpr bool SWIGLU = EPI == EPI_SWIGLU_STORE || EPI == EPI_SWIGLU_BWD;
     constexpr bool SWBWD = EPI == EPI_SWIGLU_BWD;  // and the fp32 gate / up pre-activations into C2
     constexpr bool SCATTER = EPI == EPI_SCATTER_SLOT || EPI == EPI_SCATTER_SLOT_F32;
@@ -964,7 +965,7 @@ void k_gemm_pp(const GemmArgs a) {
     constexpr bool COMBINE = EPI == EPI_COMBINE;
     constexpr bool STAGE_F32 = OUT_F32 || COMBINE;  // accumulators staged as fp32
     constexpr int OES = OUT_F32 ? 4 : 2;
-    constexpr int NH = STAGE_F32 ? 2 : 1;      // column halves per staged block (256-byte rows)
+    constexpr int NH = (STAGE_F32 || EPI == EPI_DSWIGLU) ? 2 : 1;  // column halves per staged block
     static_assert(!(COMBINE && GROUPED), "the fused combine is a dense (shared expert) epilogue");
     constexpr int STG_WAVE = 32 * 256;         // staging bytes per wave
     static_assert(NW * STG_WAVE == SLAB, "staging must fill exactly one token slot");
@@ -987,6 +988,7 @@ void k_gemm_pp(const GemmArgs a) {
     const int wm = wave >> 1, wn = wave & 1;
     const int Kd = a.Kdim;
     const int nk = Kd / BK;
+    const int ncols = a.ldc > 0 ? a.ldc : a.N;  // real output columns (N may be rounded up to BN)
     // Slab-major operands (weight gradients): a row's piece of one K slab is
     // 128 bytes after the previous row's.
     const uint32_t rowbytes = WG ? 128u : (uint32_t)Kd * 2;
@@ -1044,7 +1046,7 @@ void k_gemm_pp(const GemmArgs a) {
             return make_rsrc(Bw + (size_t)t.e * a.b_group_stride + (size_t)(t.n0 / 2) * Kd,
                              (uint32_t)__builtin_amdgcn_readfirstlane(2 * a.act_n - t.n0 / 2) * rowbytes);
         // Weight gradients: every K slab of rows n0 .. (slab-major operand).
-        if (WG) return make_rsrc(Bw + (size_t)t.n0 * 64, (uint32_t)a.N * (uint32_t)Kd * 2u - (uint32_t)t.n0 * 128u);
+        if (WG) return make_rsrc(Bw + (size_t)t.n0 * 64, (uint32_t)ncols * (uint32_t)Kd * 2u - (uint32_t)t.n0 * 128u);
         const int rows = __builtin_amdgcn_readfirstlane(max(0, min(BN, weight_rows(a) - t.n0)));
         return make_rsrc(Bw + (size_t)t.e * a.b_group_stride + (size_t)t.n0 * Kd, (uint32_t)rows * rowbytes);
     };
@@ -1059,7 +1061,7 @@ void k_gemm_pp(const GemmArgs a) {
         return WG ? (uint32_t)(t.slab0 + s) * (uint32_t)a.dense_rows * 128u : (uint32_t)s * (BK * 2);
     };
     auto soff_b = [&](const Tile& t, int s) -> uint32_t {
-        return WG ? (uint32_t)(t.slab0 + s) * (uint32_t)a.N * 128u : (uint32_t)s * (BK * 2);
+        return WG ? (uint32_t)(t.slab0 + s) * (uint32_t)ncols * 128u : (uint32_t)s * (BK * 2);
     };
     const __amdgpu_buffer_rsrc_t xnull = make_rsrc(Ax, 0);
     const __amdgpu_buffer_rsrc_t wnull = make_rsrc(Bw, 0);
@@ -1294,6 +1296,49 @@ void k_gemm_pp(const GemmArgs a) {
         const uint32_t wrow = stg + (uint32_t)fr * 256u;
         const int sw = fr & 15;
         uint8_t* const cbase = static_cast<uint8_t*>(a.C);
+        // DSW: row stride 2 act_ld, columns past act_ld (N rounded up) not stored.
+        const size_t ostr = DSW ? 2 * (size_t)a.act_ld : (size_t)ncols;
+        // DSW: stage half h of block i (64 columns) as [dG | dU] per 256-byte
+        // row, G and U read once.
+        auto dsw_stage = [&](const Tile& tt, int i, int h) {
+            const int r = wm * WT + i * 32 + fr;
+            const float* grow = static_cast<const float*>(a.aux) +
+                                (size_t)(tt.row0 + min(r, tt.rows - 1)) * 2 * a.act_ld;
+#pragma unroll
+            for (int jj = 0; jj < 2; ++jj) {
+                const int j = 2 * h + jj;
+                __builtin_amdgcn_sched_barrier(0);
+                float4 gv[4], uv[4];
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int c = tt.n0 + wn * WT + j * 32 + 8 * g + 4 * fk;
+                    gv[g] = make_float4(0.f, 0.f, 0.f, 0.f);
+                    uv[g] = gv[g];
+                    if (c < a.act_ld) {  // act_ld is a multiple of 64: whole float4s
+                        gv[g] = *reinterpret_cast<const float4*>(grow + c);
+                        uv[g] = *reinterpret_cast<const float4*>(grow + a.act_ld + c);
+                    }
+                }
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int c = tt.n0 + wn * WT + j * 32 + 8 * g + 4 * fk;
+                    const float gg[4] = {gv[g].x, gv[g].y, gv[g].z, gv[g].w};
+                    const float uu[4] = {uv[g].x, uv[g].y, uv[g].z, uv[g].w};
+                    float dg[4], du[4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        swiglu_grad(gg[q], uu[q], acc_read(acc[j][i][4 * g + q]), dg[q], du[q]);
+                        if (c + q >= a.act_n) dg[q] = du[q] = 0.0f;
+                    }
+                    const uint2 pg = pack4_bf16(dg[0], dg[1], dg[2], dg[3]);
+                    const uint2 pu = pack4_bf16(du[0], du[1], du[2], du[3]);
+                    const int chunk = 4 * jj + g;  // 16-byte chunk of the half's 64 columns
+                    lds_write8_asm(wrow + ((uint32_t)(chunk ^ sw) << 4) + (uint32_t)fk * 8u, (u32x2_t){pg.x, pg.y});
+                    lds_write8_asm(wrow + ((uint32_t)((8 + chunk) ^ sw) << 4) + (uint32_t)fk * 8u,
+                                   (u32x2_t){pu.x, pu.y});
+                }
+            }
+        };
 #pragma unroll
         for (int i = 0; i < FB; ++i) {
 #pragma unroll
@@ -1329,6 +1374,8 @@ void k_gemm_pp(const GemmArgs a) {
                             lds_write8_asm(wrow + ((uint32_t)((4 * j + g) ^ sw) << 4) + (uint32_t)fk * 8u,
                                            (u32x2_t){pk.x, pk.y});
                         }
+                } else if (DSW) {
+                    dsw_stage(t, i, h);
                 } else {
                     // dH: GELU' of the stored pre-activation of this lane's row and columns.
                     float4 fac[FB][4];
@@ -1399,14 +1446,18 @@ void k_gemm_pp(const GemmArgs a) {
                 for (int k = 0; k < 8; ++k) {
                     const int rr = (lane >> 4) + 4 * k;
                     const int r = wm * WT + i * 32 + rr;
-                    if (r < t.rows) {
+                    // DSW: pieces 0..7 of the row are dG, 8..15 dU (act_ld further on).
+                    const int pcol = DSW ? (lane & 7) * 8 : (lane & 15) * (16 / OES);
+                    const int col = t.n0 + wn * WT + h * 64 + pcol;
+                    if (r < t.rows && (!WG || t.n0 + wn * WT + h * 64 < ncols) && (!DSW || col < a.act_ld)) {
                         size_t orw = SCATTER ? (size_t)orow[i][k] : (size_t)(t.row0 + r);
                         uint8_t* ob = cbase;
                         if (WG) {  // the expert's gradient, or the work item's partial block
                             orw += (size_t)(t.dest < 0 ? t.e : t.dest) * a.dense_rows;
                             if (t.dest >= 0) ob = static_cast<uint8_t*>(a.C2);
                         }
-                        uint8_t* out = ob + (orw * a.N + t.n0 + wn * WT + h * 64) * OES + (lane & 15) * 16;
+                        uint8_t* out = ob + (orw * ostr + t.n0 + wn * WT + h * 64) * OES + (lane & 15) * 16;
+                        if (DSW) out = ob + (orw * ostr + ((lane & 8) ? a.act_ld : 0) + col) * 2;
                         store16_asm(out, v[k]);
                     }
                 }
@@ -1770,9 +1821,24 @@ hipError_t dispatch_tiled(int bm, const GemmArgs& a, hipStream_t s) {
     constexpr bool ROW_PRODUCT = EPI == EPI_GELU_BWD || EPI == EPI_DGELU || EPI == EPI_SCATTER_SLOT_F32;
     if constexpr (ROW_PRODUCT)
         if (bm == 256 && a.N % 256 == 0 && a.Kdim >= 128) return launch_pp<EPI, GROUPED>(a, s);
-    // Weight gradients: every work item spans at least two K slabs.
+    // SwiGLU dA: N = act_ld rounded up to the tile width; W2's transposed rows
+    // past act_ld read as zeros and those columns are not stored.
+    if constexpr (EPI == EPI_DSWIGLU)
+        if (bm == 256 && a.Kdim >= 128) {
+            GemmArgs p = a;
+            p.b_rows = a.act_ld;
+            p.N = (a.act_ld + 255) / 256 * 256;
+            return launch_pp<EPI, GROUPED>(p, s);
+        }
+    // Weight gradients: every work item spans at least two K slabs; N is
+    // rounded up to the tile width (B rows past N only feed unstored columns).
     if constexpr (EPI == EPI_WGRAD_F32)
-        if (bm == 256 && a.N % 256 == 0 && a.dense_rows % 256 == 0) return launch_pp<EPI, GROUPED>(a, s);
+        if (bm == 256 && a.dense_rows % 256 == 0) {
+            GemmArgs p = a;
+            p.ldc = a.N;
+            p.N = (a.N + 255) / 256 * 256;
+            return launch_pp<EPI, GROUPED>(p, s);
+        }
     if (bm == 256) {
         if (a.N % 128 == 0) return launch_bf16<256, 128, 2, 2, 64, 2, 1, EPI, GROUPED>(a, s);
         return launch_bf16<256, 64, 4, 1, 64, 2, 1, EPI, GROUPED>(a, s);

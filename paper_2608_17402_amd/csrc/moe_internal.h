@@ -80,6 +80,8 @@ struct GemmArgs {
     uint32_t a_bytes;          // bytes of the A operand buffer (bounds of its buffer resource)
     void* C2;                  // EPI_GELU_BWD: second output (fp32); EPI_WGRAD_F32: partial blocks
     const void* aux;           // EPI_DGELU: the pre-activation (fp32, rows of N); EPI_DSWIGLU: G, U
+    int32_t ldc;               // persistent kernel, EPI_WGRAD_F32 / EPI_DSWIGLU: the real column count when N
+                               // is rounded up to the tile width (0 = N); columns past it are not stored
     int32_t act_n;             // EPI_SWIGLU_STORE: activation width h (valid columns)
     int32_t act_ld;            // EPI_SWIGLU_STORE: activation row stride (h rounded up to 128)
     const float* gate;         // EPI_COMBINE: gates [rows, route_k]
