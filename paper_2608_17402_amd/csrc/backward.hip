@@ -205,6 +205,18 @@ __global__ __launch_bounds__(256) void k_compact_rows(const float* __restrict__ 
         *reinterpret_cast<const float4*>(in + (g * 2 * ld + sr) * (size_t)C + c);
 }
 
+// Zero the K window of every expert with no rows (its two slabs of the
+// slab-major operand [ld / 64][C][64]); one workgroup per expert.
+__global__ __launch_bounds__(256) void k_zero_empty_windows(bf16_t* __restrict__ out, int C,
+                                                           const int32_t* __restrict__ offsets,
+                                                           const int32_t* __restrict__ koff) {
+    const int e = blockIdx.x;
+    if (offsets[e + 1] != offsets[e]) return;
+    uint4* p = reinterpret_cast<uint4*>(out + (size_t)koff[e] * C);
+    const size_t n = (size_t)(koff[e + 1] - koff[e]) * C / 8;
+    for (size_t i = threadIdx.x; i < n; i += blockDim.x) p[i] = make_uint4(0u, 0u, 0u, 0u);
+}
+
 __device__ __forceinline__ uint32_t pack2_bf16_rne(float lo, float hi) {
     uint32_t a = __float_as_uint(lo), b = __float_as_uint(hi);
     a += 0x7fffu + ((a >> 16) & 1u);
@@ -280,6 +292,12 @@ hipError_t launch_transpose_window(const void* in, int C, int mode, const int32_
         hipLaunchKernelGGL(k_transpose_window<TT>, dim3(ld / TT, C / TT), dim3(256), 0, s,
                            static_cast<const bf16_t*>(in), C, mode, row_map, K, offsets, koff, E,
                            static_cast<bf16_t*>(out));
+    return hipGetLastError();
+}
+
+hipError_t launch_zero_empty_windows(void* out, int C, const int32_t* offsets, const int32_t* koff, int E,
+                                     hipStream_t s) {
+    hipLaunchKernelGGL(k_zero_empty_windows, dim3(E), dim3(256), 0, s, static_cast<bf16_t*>(out), C, offsets, koff);
     return hipGetLastError();
 }
 

@@ -150,6 +150,11 @@ __device__ __forceinline__ int weight_rows(const GemmArgs& a) { return a.b_rows 
 __host__ __device__ constexpr bool fc1_epi(int epi) {
     return epi == EPI_GELU_STORE || epi == EPI_SWIGLU_STORE || epi == EPI_SWIGLU_BWD;
 }
+// Epilogues of the persistent kernel that can also write their bf16 result
+// transposed into the weight-gradient windows (GemmArgs::CT).
+__host__ __device__ constexpr bool ct_epi(int epi) {
+    return epi == EPI_GELU_BWD || epi == EPI_SWIGLU_BWD || epi == EPI_DGELU;
+}
 
 // d/dx GELU(x) = Phi(x) + x phi(x) from the same approximation: Q =
 // erfc(|x| / sqrt 2) / 2 as in gelu_as, Phi(x) = 1 - Q for x >= 0 and Q
@@ -187,6 +192,10 @@ __device__ __forceinline__ void wait_vmcnt() {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
+template <int N>
+__device__ __forceinline__ void wait_lgkmcnt() {
+    asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
+}
 __device__ __forceinline__ void wait_lgkmcnt0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
 // Workgroup barrier without the memory fence of __syncthreads (which would
@@ -909,6 +918,10 @@ __device__ __forceinline__ u32x4_t lds_read16u_asm(uint32_t addr) {
     return r;
 }
 __device__ __forceinline__ void tie(u32x4_t& v) { asm volatile("" : "+v"(v)); }
+__device__ __forceinline__ void lds_read_u16_asm(uint32_t& r, uint32_t addr) {
+    asm volatile("ds_read_u16 %0, %1" : "=v"(r) : "v"(addr));
+}
+__device__ __forceinline__ void tie(uint32_t& v) { asm volatile("" : "+v"(v)); }
 // One accumulator moved to a vector register at this point of the program
 // (volatile: not hoisted, so only one staged block's values are live at once).
 __device__ __forceinline__ float acc_read(float x) {
@@ -1291,6 +1304,71 @@ void k_gemm_pp(const GemmArgs a) {
     // `stslot`: per 32-row block (and 64-column half for fp32 output) each
     // lane writes its row's runs into the wave's 8 KB, then reads back 16-byte
     // row pieces (16 lanes per 256-byte row) and stores whole lines.
+    // Backward: the staged bf16 block i (32 rows of this wave, ncc columns of
+    // the 256-byte staging rows) also goes to the weight-gradient K windows,
+    // transposed and slab-major: staged column cc becomes row colmap(cc) (or
+    // nothing for -1); rows past the tile's valid rows are written as 0 up to
+    // the window's end, rows past the window are not written. Window starts
+    // are multiples of 64 and tiles start 256 rows apart inside an expert, so
+    // each 8-row piece lies inside one 64-position slab.
+    constexpr bool HAS_CT = ct_epi(EPI);
+    auto store_ct = [&](const Tile& t, uint32_t stg, int i, int ncc, auto&& colmap) {
+        const int e = t.e;
+        const int gpos = t.row0 - a.goff[e] + wm * WT + i * 32;  // first row of the block within its expert
+        const int wq = a.koff[e] + gpos;
+        const int wlen = a.koff[e + 1] - a.koff[e];
+        const int vrows = t.rows - (wm * WT + i * 32);  // rows of the block that exist
+        uint8_t* const ct = static_cast<uint8_t*>(a.CT);
+        // Piece k of a lane: staged column cc = (lane + 64 k) / 4, rows
+        // 8 rg .. 8 rg + 7 with rg = lane % 4, one zero-extended 16-bit read
+        // per row (a read into half of a register would merge with that
+        // register as it was when issued, not with a read still in flight).
+        // Two pieces in flight: the reads of piece k + 1 are issued before
+        // piece k is stored.
+        const int nit = ncc * 4 / kWave;
+        // The lane index through an opaque copy: the per-piece addresses are
+        // then computed here instead of being hoisted out of the tile loop
+        // (64 live registers).
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+        const int rg = ln & 3;
+        uint32_t w[2][8];
+        auto issue = [&](int k, uint32_t(&dst)[8]) {
+            const int cc = (ln + kWave * k) >> 2;
+            const uint32_t b = stg + (uint32_t)(rg * 8) * 256u + (uint32_t)(cc & 7) * 2u;
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                lds_read_u16_asm(dst[u], b + (uint32_t)u * 256u + ((uint32_t)((cc >> 3) ^ ((rg * 8 + u) & 15)) << 4));
+        };
+        issue(0, w[0]);
+#pragma unroll
+        for (int k = 0; k < nit; ++k) {
+            __builtin_amdgcn_sched_barrier(0);
+            if (k + 1 < nit) {
+                issue(k + 1, w[(k + 1) & 1]);
+                wait_lgkmcnt<8>();
+            } else {
+                wait_lgkmcnt0();
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u) tie(w[k & 1][u]);
+            const int cc = (ln + kWave * k) >> 2;
+            const int orow = colmap(cc);
+            if (orow < 0 || gpos + rg * 8 >= wlen) continue;
+            uint32_t* const r16 = w[k & 1];
+            if (vrows < 32) {  // the expert's last rows: zeros past them
+#pragma unroll
+                for (int u = 0; u < 8; ++u)
+                    if (rg * 8 + u >= vrows) r16[u] = 0u;
+            }
+            u32x4_t v;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) v[u] = r16[2 * u] | (r16[2 * u + 1] << 16);
+            const int q = wq + rg * 8;
+            store16_asm(ct + (((size_t)(q / 64) * a.ct_cols + orow) * 64 + q % 64) * 2, v);
+        }
+    };
+
     auto epilogue = [&](const Tile& t, int stslot) {
         const uint32_t stg = base + (uint32_t)stslot * SLAB + (uint32_t)wave * STG_WAVE;
         const uint32_t wrow = stg + (uint32_t)fr * 256u;
@@ -1412,6 +1490,13 @@ void k_gemm_pp(const GemmArgs a) {
                     combine_block(t, stg, i, h);
                     continue;
                 }
+                if constexpr (SWBWD) {
+                    if (a.CT) {  // the activation only feeds dW2: its transpose alone
+                        const int ocol = t.n0 / 2 + wn * (WT / 2);
+                        store_ct(t, stg, i, WT / 2, [&](int cc) { return ocol < a.act_ld ? ocol + cc : -1; });
+                        continue;
+                    }
+                }
                 if constexpr (SWIGLU) {
                     // 128-byte activation rows: 8 lanes per row, 8 rows per read.
                     const int ocol = t.n0 / 2 + wn * (WT / 2);
@@ -1431,6 +1516,13 @@ void k_gemm_pp(const GemmArgs a) {
                             store16_asm(cbase + ((size_t)(t.row0 + r) * a.act_ld + ocol) * 2 + (lane & 7) * 16, v[k]);
                     }
                     continue;
+                }
+                if constexpr (HAS_CT && !SWIGLU) {
+                    if (a.CT) {
+                        const int c0 = t.n0 + wn * WT + h * 64;
+                        store_ct(t, stg, i, WT, [&](int cc) { return c0 + cc; });
+                        if constexpr (BWD1) continue;  // the activation only feeds dW2
+                    }
                 }
                 u32x4_t v[8];
 #pragma unroll
@@ -1721,6 +1813,7 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const GemmArgs a) {
 
 template <int BM, int BN, int WM, int WN, int BK, int ST, int WPE, int EPI, bool GROUPED>
 hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
+    if (a.CT) return hipErrorInvalidValue;  // transposed outputs exist on the persistent kernel only
     const int n_n = a.N / BN;
     const long long total = (long long)a.max_tiles * n_n;
     const long long grid = (total + kNumXcd - 1) / kNumXcd * kNumXcd;
@@ -1748,6 +1841,7 @@ int persistent_grid(long long tile_bound) {
 
 template <int EPI, bool GROUPED, int KC = 8>
 hipError_t launch_pp(const GemmArgs& a, hipStream_t s) {
+    if (a.CT && !ct_epi(EPI)) return hipErrorInvalidValue;
     const int grid = persistent_grid((long long)a.max_tiles * (a.N / 256));
     hipLaunchKernelGGL((k_gemm_pp<EPI, GROUPED, KC>), dim3((unsigned)grid), dim3(256), 0, s, a);
     return hipGetLastError();
@@ -1944,6 +2038,14 @@ int gemm_dense_bm(int32_t dtype, int64_t rows, int32_t n) {
     // 256-row tiles only when they still give a few workgroups per CU.
     const int64_t tiles = (rows + 255) / 256 * (n / 256 > 0 ? n / 256 : 1);
     return tiles >= 512 ? 256 : 64;
+}
+
+bool gemm_backward_transposed(const moe_desc_t& d, int bm) {
+    // The same conditions under which dispatch_tiled / dispatch_swiglu_bwd pick
+    // the persistent kernel for the recompute (K = d) and dA (K = d) products.
+    if (d.dtype != MOE_BF16 || bm != 256 || d.d < 128) return false;
+    if (d.flags & MOE_FLAG_SWIGLU) return true;  // widths rounded up to the tile
+    return d.h % 256 == 0;
 }
 
 bool gemm_combine_fusable(const moe_desc_t& d, int bm, int n, int kdim) {

@@ -357,6 +357,18 @@ static moe_status_t enqueue_backward(const moe_desc_t& d, const BackwardPlan& b,
     float* dxs = region<float>(ws, b.dxs);
     int32_t* koff = region<int32_t>(ws, b.koff);
     HIP_CHECK(launch_build_tiles(d.E, p.tile_bm, p.max_tiles, offsets, tiles, ntiles, s), "build_tiles");
+    // Weight-gradient windows first: on the persistent kernel the recompute
+    // and dA products write the transposed activation and dH into them.
+    void* gt = region<void>(ws, b.gt);
+    void* at = region<void>(ws, b.at);
+    void* dht = region<void>(ws, b.dht);
+    void* xt = region<void>(ws, b.xt);
+    TileDesc* items = region<TileDesc>(ws, b.items);
+    TileDesc* rlist = region<TileDesc>(ws, b.rlist);
+    int32_t* wcount = region<int32_t>(ws, b.wcount);
+    float* partials = region<float>(ws, b.partials);
+    HIP_CHECK(launch_wgrad_plan(offsets, d.E, koff, items, rlist, wcount, s), "weight-gradient plan");
+    const bool direct_t = gemm_backward_transposed(d, p.tile_bm);
     if (sw) HIP_CHECK(launch_transpose_w13(w1, d.E, d.h, hh, d.d, w1t, s), "transpose w13");
     else HIP_CHECK(launch_transpose_w(w1, d.E, d.h, d.d, w1t, s), "transpose w1");
     HIP_CHECK(launch_transpose_w(w2, d.E, d.d, hh, w2t, s), "transpose w2");
@@ -378,6 +390,12 @@ static moe_status_t enqueue_backward(const moe_desc_t& d, const BackwardPlan& b,
     g.a_bytes = (uint32_t)((size_t)d.T * d.d * 2);
     g.act_n = d.h;
     g.act_ld = hh;
+    if (direct_t) {
+        g.CT = at;
+        g.ct_cols = hh;
+        g.koff = koff;
+        g.goff = offsets;
+    }
     HIP_CHECK(launch_gemm(d, sw ? EPI_SWIGLU_BWD : EPI_GELU_BWD, p.tile_bm, g, s), "backward fc1");
 
     GemmArgs ga = g;  // dH from Gout W2 and the pre-activations
@@ -390,6 +408,12 @@ static moe_status_t enqueue_backward(const moe_desc_t& d, const BackwardPlan& b,
     ga.b_group_stride = (int64_t)hh * d.d;
     ga.row_mode = ROWS_GATHER_SLOTS;
     ga.a_bytes = (uint32_t)(TK * d.d * 2);
+    // SwiGLU dA keeps its row output only: its epilogue already carries the
+    // fp32 gate and up reads, and a second, transposed output costs more
+    // there than the separate gather of dH.
+    const bool direct_dh = direct_t && !sw;
+    ga.CT = direct_dh ? dht : nullptr;
+    ga.ct_cols = hw;
     HIP_CHECK(launch_gemm(d, sw ? EPI_DSWIGLU : EPI_DGELU, p.tile_bm, ga, s), "backward dA");
 
     GemmArgs gx = g;  // slot gradients of x: dH W1, fp32 to slot order
@@ -402,25 +426,24 @@ static moe_status_t enqueue_backward(const moe_desc_t& d, const BackwardPlan& b,
     gx.b_group_stride = (int64_t)d.d * hw;
     gx.row_mode = ROWS_IDENTITY;
     gx.a_bytes = (uint32_t)(TK * hw * 2);
+    gx.CT = nullptr;
     HIP_CHECK(launch_gemm(d, EPI_SCATTER_SLOT_F32, p.tile_bm, gx, s), "backward dx");
     HIP_CHECK(launch_slot_sum(dxs, d.T, d.K, d.d, dx, s), "slot sum");
 
-    // Weight gradients: transposed operands in per-expert K windows.
-    void* gt = region<void>(ws, b.gt);
-    void* at = region<void>(ws, b.at);
-    void* dht = region<void>(ws, b.dht);
-    void* xt = region<void>(ws, b.xt);
-    TileDesc* items = region<TileDesc>(ws, b.items);
-    TileDesc* rlist = region<TileDesc>(ws, b.rlist);
-    int32_t* wcount = region<int32_t>(ws, b.wcount);
-    float* partials = region<float>(ws, b.partials);
-    HIP_CHECK(launch_wgrad_plan(offsets, d.E, koff, items, rlist, wcount, s), "weight-gradient plan");
+    // Weight gradients: transposed operands in per-expert K windows (the
+    // activation and dH ones written above when the products ran persistent).
     HIP_CHECK(launch_transpose_window(gout, d.d, SRC_SLOT, sorted_slots, d.K, offsets, koff, d.E, gt, b.ld, s),
               "transpose G");
-    HIP_CHECK(launch_transpose_window(act, hh, SRC_SORTED, sorted_slots, d.K, offsets, koff, d.E, at, b.ld, s),
-              "transpose A");
-    HIP_CHECK(launch_transpose_window(dh, hw, SRC_SORTED, sorted_slots, d.K, offsets, koff, d.E, dht, b.ld, s),
-              "transpose dH");
+    if (direct_t)
+        HIP_CHECK(launch_zero_empty_windows(at, hh, offsets, koff, d.E, s), "empty windows");
+    else
+        HIP_CHECK(launch_transpose_window(act, hh, SRC_SORTED, sorted_slots, d.K, offsets, koff, d.E, at, b.ld, s),
+                  "transpose A");
+    if (direct_dh)
+        HIP_CHECK(launch_zero_empty_windows(dht, hw, offsets, koff, d.E, s), "empty windows");
+    else
+        HIP_CHECK(launch_transpose_window(dh, hw, SRC_SORTED, sorted_slots, d.K, offsets, koff, d.E, dht, b.ld, s),
+                  "transpose dH");
     HIP_CHECK(launch_transpose_window(x, d.d, SRC_TOKEN, sorted_slots, d.K, offsets, koff, d.E, xt, b.ld, s),
               "transpose x");
     auto wgrad = [&](const void* pa, int m, const void* pb, int n, float* out, const char* what) -> moe_status_t {

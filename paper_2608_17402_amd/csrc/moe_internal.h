@@ -79,6 +79,15 @@ struct GemmArgs {
     int32_t b_rows;            // dense bf16 only: rows of B that exist (0 = N); rows past them read as zeros
     uint32_t a_bytes;          // bytes of the A operand buffer (bounds of its buffer resource)
     void* C2;                  // EPI_GELU_BWD: second output (fp32); EPI_WGRAD_F32: partial blocks
+    // Backward, persistent kernel: the bf16 output (the activation, or dH) also
+    // written transposed into the weight-gradient K windows, slab-major
+    // [windows / 64][ct_cols][64]: sorted position p of expert e goes to window
+    // position koff[e] + p - goff[e]; padding positions of the window get 0.
+    // EPI_GELU_BWD / EPI_SWIGLU_BWD then skip the row-major activation.
+    void* CT;
+    int32_t ct_cols;
+    const int32_t* koff;       // [E + 1] window starts
+    const int32_t* goff;       // [E + 1] group offsets (sorted positions)
     const void* aux;           // EPI_DGELU: the pre-activation (fp32, rows of N); EPI_DSWIGLU: G, U
     int32_t ldc;               // persistent kernel, EPI_WGRAD_F32 / EPI_DSWIGLU: the real column count when N
                                // is rounded up to the tile width (0 = N); columns past it are not stored
@@ -159,6 +168,9 @@ hipError_t launch_build_tiles(int32_t E, int32_t bm, int32_t max_tiles, const in
 hipError_t launch_gemm(const moe_desc_t& d, int epilogue, int bm, const GemmArgs& a, hipStream_t s);
 // Whether launch_gemm(EPI_COMBINE) supports this dense GEMM (M-tile bm, N columns, K = kdim).
 bool gemm_combine_fusable(const moe_desc_t& d, int bm, int n, int kdim);
+// Whether the backward's first-layer recompute and dA products run on the
+// persistent kernel (which can also write their transposed outputs).
+bool gemm_backward_transposed(const moe_desc_t& d, int bm);
 // Backward data movement (backward.hip). Row sources of the transposing
 // gather: rows already in sorted order, slot rows, token rows.
 enum TransposeSource : int { SRC_SORTED = 0, SRC_SLOT = 1, SRC_TOKEN = 2 };
@@ -177,6 +189,9 @@ hipError_t launch_transpose_window(const void* in, int C, int mode, const int32_
                                    const int32_t* offsets, const int32_t* koff, int E, void* out, int ld,
                                    hipStream_t s);
 hipError_t launch_slot_sum(const float* dxs, int T, int K, int d, void* dx, hipStream_t s);
+// Zeroes the windows of experts with no rows in a slab-major operand [ld / 64][C][64].
+hipError_t launch_zero_empty_windows(void* out, int C, const int32_t* offsets, const int32_t* koff, int E,
+                                     hipStream_t s);
 hipError_t launch_bias_update(int32_t E, const int32_t* counts, float* bias, float alpha, int32_t rule,
                               hipStream_t s);
 hipError_t launch_combine(const moe_desc_t& d, const void* expert_out, const float* gate,

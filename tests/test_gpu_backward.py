@@ -137,6 +137,32 @@ def test_backward_split_windows():
     check_grad(dw2, rdw2, "split dw2")
 
 
+def test_backward_transposed_outputs_small_experts():
+    """h a multiple of 256 on 256-row tiles: the recompute and dA products write
+    the activation's and dH's transposes into the weight-gradient windows
+    themselves. Expert 4 holds one row, expert 5 none, expert 3 a ragged tail
+    (rows past it must be written as zeros in its window)."""
+    T, d, E, K, h = 3000, 128, 6, 2, 256
+    rng = np.random.default_rng(11)
+    idx = _idx(rng, T, E, K, np.array([0.3, 0.3, 0.3, 0.1, 0.0, 0.0]))
+    idx[0] = [0, 4]
+    x = _bf16(rng, (T, d), 1.0)
+    w1 = _bf16(rng, (E, h, d), 0.1)
+    w2 = _bf16(rng, (E, d, h), 0.1)
+    g = _bf16(rng, (T * K, d), 0.5)
+    counts = np.bincount(idx.ravel(), minlength=E)
+    assert counts[4] == 1 and counts[5] == 0 and counts[3] % 64 != 0 and counts.sum() // E >= 512
+    dx, dw1, dw2 = run_backward(T, d, E, K, h, idx, x, w1, w2, g)
+    assert np.all(dw1[5] == 0) and np.all(dw2[5] == 0)
+    rdx, rdw1, rdw2 = oracle.grouped_backward(bf16_bits_to_f32(x), idx, bf16_bits_to_f32(w1), bf16_bits_to_f32(w2),
+                                              bf16_bits_to_f32(g), True)
+    check_grad(dw1[4], rdw1[4], "one-row dw1")
+    check_grad(dw2[4], rdw2[4], "one-row dw2")
+    check_grad(dx, rdx, "transposed dx")
+    check_grad(dw1, rdw1, "transposed dw1")
+    check_grad(dw2, rdw2, "transposed dw2")
+
+
 @pytest.mark.slow
 def test_backward_full_vitg_sampled():
     """ViT-G skewed layer at 65 536 tokens with its own routing: the weight
