@@ -140,7 +140,8 @@ moe_status_t moe_permute(const moe_desc_t *desc, const int32_t *topk_idx, int32_
  *                W2[e] (SiLU(W1[e] x_t) * (W3[e] x_t)))
  * For bf16 the activation (GELU(W1 x), or SiLU(W1 x) * W3 x with both
  * projections accumulated in fp32 in the same kernel) is rounded to bf16
- * before fc2; accumulation is fp32. The shared expert can be run through this call with
+ * before fc2; accumulation is fp32. bf16 layers evaluate GELU within 2.6e-5
+ * (absolute) of the erf form, fp32 layers with the device erff. The shared expert can be run through this call with
  * a descriptor {E = 1, K = 1, h = h_s}, sorted_slots = 0..T-1, offsets =
  * {0, T}. Uses the workspace. */
 moe_status_t moe_grouped_mlp(const moe_desc_t *desc, const void *x, const int32_t *sorted_slots,
