@@ -1,7 +1,8 @@
 // Data-movement kernels of the expert-MLP backward: weight transposes, the
 // plan of the weight-gradient products (per-expert K windows cut into work
 // items) and the sum of their partial blocks, the transposing gather into the
-// windows, and the per-token sum of the slot gradients. The
+// windows and the zeroing of empty experts' windows, and the per-token sum of
+// the slot gradients. The
 // products themselves run on the MFMA kernels of gemm.hip.
 #include "moe_internal.h"
 

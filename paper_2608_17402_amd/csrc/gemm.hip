@@ -15,10 +15,22 @@
 // meet in the same L2.
 //
 // bf16: v_mfma_f32_32x32x16_bf16 with fp32 accumulators. Both operands are
-// K-contiguous (token rows and nn.Linear weight rows), staged through LDS in
-// 64-wide K slabs, double-buffered, one barrier per slab. A 16-byte chunk c of
-// LDS row r is stored at chunk c ^ (r & 7), so the 32 rows a fragment read
-// touches spread over all banks.
+// K-contiguous (token rows and nn.Linear weight rows) and stream global -> LDS
+// in 64-wide K slabs through rings of a few slabs (buffer_load ... lds), with
+// 16-byte chunks XOR-swizzled by row so that the rows a fragment read touches
+// spread over the LDS banks. The kernels:
+//   k_gemm_bf16  tiled, one tile per workgroup (256- or 64-row tiles, 64- to
+//                256-column tiles); every epilogue, including the backward's
+//   k_gemm_sp    256 x 256 tiles, four waves of 128 x 128, copies paced by
+//                hand against the MFMAs (used where K is one slab)
+//   k_gemm_pp    the persistent form of k_gemm_sp: one workgroup per CU walks
+//                its tiles with the slab pipeline running across them; the
+//                large-batch forward and backward products
+//   k_gemm_f32   fp32 layers (VALU)
+// Epilogues (EPI_*): GELU or SwiGLU to bf16 (first layer), scatter to slot
+// order (second layer), fp32 store, the gate-weighted combine, and the
+// backward's recompute (with fp32 pre-activations), dA through GELU' or
+// SwiGLU', fp32 slot gradients and fp32 weight gradients.
 #include "moe_internal.h"
 
 #include <math.h>
@@ -1876,16 +1888,12 @@ hipError_t launch_f32(const GemmArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
-// Tile shapes. Large groups (M-tiles of 256 token rows): 256 x 256 when N
-// allows, else 256 x 128 or 256 x 64. Small groups (M-tiles of 64 rows, the
-// weight-read-bound regime where an expert sees a few dozen tokens): 64 x 128
-// or 64 x 64, several workgroups per CU to keep many weight loads in flight.
-// Tile shapes. Large groups (M-tiles of 256 token rows): 256 x 256 with 8
-// waves of 128 x 64 (64-wide K slabs, double-buffered) when N allows, else
-// 256 x 128 or 256 x 64 with 4 waves. Small groups (M-tiles of 64 rows, the
-// weight-read-bound regime where an expert sees a few dozen tokens): 64 x 128
-// or 64 x 64 with three slabs in the ring and several workgroups per CU, to
-// keep many weight loads in flight.
+// Tile shapes. Large groups (M-tiles of 256 token rows): 256 x 256 on the
+// persistent kernel when N allows and K spans at least two slabs (the paced
+// one-tile kernel for one slab), else 256 x 128 or 256 x 64 tiled. Small
+// groups (M-tiles of 64 rows, the weight-read-bound regime where an expert
+// sees a few dozen tokens): 64 x 128 or 64 x 64 with three slabs in the ring
+// and several workgroups per CU, to keep many weight loads in flight.
 template <int EPI, bool GROUPED>
 hipError_t dispatch_bf16(int bm, const GemmArgs& a, hipStream_t s) {
     if (bm == 256) {
@@ -1904,7 +1912,9 @@ hipError_t dispatch_bf16(int bm, const GemmArgs& a, hipStream_t s) {
     return hipErrorInvalidValue;
 }
 
-// Backward products: always the tiled kernel (256- or 64-row tiles).
+// Backward products: the persistent kernel on 256-row tiles where the widths
+// allow (rounded up to the tile for SwiGLU dA and the weight gradients), else
+// the tiled kernel with 256- or 64-row tiles.
 template <int EPI, bool GROUPED>
 hipError_t dispatch_tiled(int bm, const GemmArgs& a, hipStream_t s) {
     constexpr bool ROW_PRODUCT = EPI == EPI_GELU_BWD || EPI == EPI_DGELU || EPI == EPI_SCATTER_SLOT_F32;
