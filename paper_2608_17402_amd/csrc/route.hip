@@ -349,6 +349,66 @@ __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s
     }
 }
 
+// Exact top-K of a token's candidates and their gates, for the chain kernels
+// (TPB tokens of LPT lanes, CPL chains per lane; candidate slot g + LPT c of
+// token tl holds expert ec[c] with exact logit acc[c]). Every candidate's key
+// (sigmoid plus selection bias), sigmoid and expert go to LDS; each lane
+// ranks its own candidates among the token's in (key descending, expert
+// ascending) order, the order of taking the K largest keys one by one; ranks
+// below K are the slots. Then every lane of the token forms the gate
+// denominator in slot order and writes its slots. Called by every thread of
+// the block once its chains are done; lds holds at least
+// TPB (12 LPT CPL + 8 kMaxK) bytes and is no longer read by the chains.
+template <int TPB, int LPT, int CPL>
+__device__ __forceinline__ void chain_select(uint8_t* lds, int tl, int g, int t, int T, int nc, int K,
+                                             const bool (&on)[CPL], const int (&ec)[CPL], const float (&acc)[CPL],
+                                             const float (&bc)[CPL], bool has_bias, int32_t* __restrict__ topk_idx,
+                                             float* __restrict__ topk_gate) {
+    constexpr int NS = LPT * CPL;
+    float* skey = reinterpret_cast<float*>(lds);
+    float* ssig = skey + TPB * NS;
+    int* sexp = reinterpret_cast<int*>(ssig + TPB * NS);
+    float* osig = reinterpret_cast<float*>(sexp + TPB * NS);
+    int* oexp = reinterpret_cast<int*>(osig + TPB * kMaxK);
+    float kc[CPL], sc[CPL];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+        const int j = g + LPT * c;
+        sc[c] = 0.0f;
+        kc[c] = 0.0f;
+        if (on[c]) {
+            sc[c] = sigmoid_fp32(acc[c]);
+            kc[c] = has_bias ? sc[c] + bc[c] : sc[c];
+            skey[tl * NS + j] = kc[c];
+            ssig[tl * NS + j] = sc[c];
+            sexp[tl * NS + j] = ec[c];
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+        if (!on[c]) continue;
+        int rank = 0;  // the candidate itself compares neither greater nor lower
+        for (int q = 0; q < nc; ++q) {
+            const float kq = skey[tl * NS + q];
+            const int eq = sexp[tl * NS + q];
+            rank += (kq > kc[c] || (kq == kc[c] && eq < ec[c])) ? 1 : 0;
+        }
+        if (rank < K) {
+            osig[tl * kMaxK + rank] = sc[c];
+            oexp[tl * kMaxK + rank] = ec[c];
+        }
+    }
+    __syncthreads();
+    if (t >= T || nc == 0) return;
+    float den = osig[tl * kMaxK];
+    for (int j = 1; j < K; ++j) den = den + osig[tl * kMaxK + j];
+    for (int j = g; j < K; j += LPT) {
+        topk_idx[(size_t)t * K + j] = oexp[tl * kMaxK + j];
+        topk_gate[(size_t)t * K + j] = osig[tl * kMaxK + j] / den;
+    }
+}
+
 // Exact logits of the candidates, recipe S, exact top-K and gates. LPT lanes
 // per token, each running CPL candidate chains (slots g, g + LPT, ...) side by
 // side: one fused multiply-add chain per candidate over the model width, in
@@ -475,17 +535,13 @@ __global__ __launch_bounds__(TPB* LPT) void k_router_chain(const bf16_t* __restr
                 if (tid + NT * i < WP && e < E) wrg[i] = *reinterpret_cast<const u32x4_t*>(wr + (size_t)e * d + k1 + c);
             }
         }
-        static_assert(CPL == 1 || CPL == 4, "chain counts handled below");
-        if constexpr (CPL == 1) {
-            if (nmax >= 1) chunk(std::integral_constant<int, 1>{}, buf);
-        } else {
-            switch (nmax) {
-                case 4: chunk(std::integral_constant<int, 4>{}, buf); break;
-                case 3: chunk(std::integral_constant<int, 3>{}, buf); break;
-                case 2: chunk(std::integral_constant<int, 2>{}, buf); break;
-                case 1: chunk(std::integral_constant<int, 1>{}, buf); break;
-                default: break;
-            }
+        static_assert(CPL == 4, "chain counts handled below");
+        switch (nmax) {
+            case 4: chunk(std::integral_constant<int, 4>{}, buf); break;
+            case 3: chunk(std::integral_constant<int, 3>{}, buf); break;
+            case 2: chunk(std::integral_constant<int, 2>{}, buf); break;
+            case 1: chunk(std::integral_constant<int, 1>{}, buf); break;
+            default: break;
         }
         if (ch + 1 < nch) {
             stash(buf ^ 1);
@@ -496,54 +552,87 @@ __global__ __launch_bounds__(TPB* LPT) void k_router_chain(const bf16_t* __restr
         buf ^= 1;
     }
 
-    // Selection: every candidate's exact key, sigmoid and expert go to LDS (the
-    // ring is free after the last barrier). Each lane ranks its own candidates
-    // among the token's in (key descending, expert ascending) order, the order
-    // of taking the K largest keys one by one; ranks below K are the slots.
-    // Then every lane of the token forms the gate denominator in slot order
-    // and writes its slots.
-    float* skey = reinterpret_cast<float*>(lds);
-    float* ssig = skey + TPB * NS;
-    int* sexp = reinterpret_cast<int*>(ssig + TPB * NS);
-    float* osig = reinterpret_cast<float*>(sexp + TPB * NS);
-    int* oexp = reinterpret_cast<int*>(osig + TPB * kMaxK);
-    float kc[CPL], sc[CPL];
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) {
-        const int j = g + LPT * c;
-        sc[c] = 0.0f;
-        kc[c] = 0.0f;
-        if (on[c]) {
-            sc[c] = sigmoid_fp32(acc[c]);
-            kc[c] = bias ? sc[c] + bc[c] : sc[c];
-            skey[tl * NS + j] = kc[c];
-            ssig[tl * NS + j] = sc[c];
-            sexp[tl * NS + j] = ec[c];
-        }
-    }
+    // Selection (the ring is free after the last barrier).
+    chain_select<TPB, LPT, CPL>(lds, tl, g, t, T, nc, K, on, ec, acc, bc, bias != nullptr, topk_idx, topk_gate);
+}
+
+// Exact logits for small batches, where streaming every expert's weights
+// through LDS per block of tokens costs more than the candidates need: one
+// 64-lane wave per TPB = 64 / LPT tokens, one candidate chain per lane (LPT =
+// the candidate slots). The block's x rows are staged in LDS; each lane reads
+// its candidate's router-weight row straight from global memory, in groups of
+// eight 16-byte loads (64 columns), the next group's loads issued before the
+// current group's 64 multiply-adds. The chain is the same fused multiply-add
+// sequence over i = 0..d-1, from +0, as in k_router_chain. Dynamic LDS:
+// max(TPB d bf16, the selection's arrays). d is a multiple of 64.
+template <int LPT>
+__global__ __launch_bounds__(kWave) void k_router_chain_direct(const bf16_t* __restrict__ x,
+                                                             const bf16_t* __restrict__ wr,
+                                                             const float* __restrict__ bias,
+                                                             const uint16_t* __restrict__ cand,
+                                                             const int32_t* __restrict__ ncand, int T, int d, int E,
+                                                             int K, int32_t* __restrict__ topk_idx,
+                                                             float* __restrict__ topk_gate) {
+    constexpr int TPB = kWave / LPT;
+    extern __shared__ __attribute__((aligned(16))) uint8_t lds_dyn[];
+    const int tid = threadIdx.x;
+    const int g = tid % LPT;
+    const int tl = tid / LPT;
+    const int t = blockIdx.x * TPB + tl;
+    int nc = t < T ? ncand[t] : 0;
+    nc = nc < 0 ? 0 : nc;  // queued tokens are routed by the exact-list kernel
+    const bool on[1] = {g < nc};
+    const int ec[1] = {on[0] ? (int)cand[(size_t)t * LPT + g] : 0};
+    const float bc[1] = {(bias && on[0]) ? bias[ec[0]] : 0.0f};
+    (void)E;
+
+    // x rows of the block's tokens (tokens past T copy row T - 1; their
+    // chains are off).
+    bf16_t* xs = reinterpret_cast<bf16_t*>(lds_dyn);
+    const bf16_t* xt = x + (size_t)(t < T ? t : T - 1) * d;
+    for (int i = g * 8; i < d; i += LPT * 8)
+        *reinterpret_cast<u32x4_t*>(xs + tl * d + i) = *reinterpret_cast<const u32x4_t*>(xt + i);
     __syncthreads();
+
+    float acc[1] = {0.0f};
+    if (__ballot(on[0]) != 0) {
+        const bf16_t* we = wr + (size_t)ec[0] * d;
+        const bf16_t* xr = xs + tl * d;
+        const int ng = d / 64;
+        u32x4_t wa[8], wb[8];
+        auto load = [&](u32x4_t(&w)[8], int grp) {
 #pragma unroll
-    for (int c = 0; c < CPL; ++c) {
-        if (!on[c]) continue;
-        int rank = 0;  // the candidate itself compares neither greater nor lower
-        for (int q = 0; q < nc; ++q) {
-            const float kq = skey[tl * NS + q];
-            const int eq = sexp[tl * NS + q];
-            rank += (kq > kc[c] || (kq == kc[c] && eq < ec[c])) ? 1 : 0;
-        }
-        if (rank < K) {
-            osig[tl * kMaxK + rank] = sc[c];
-            oexp[tl * kMaxK + rank] = ec[c];
+            for (int u = 0; u < 8; ++u) w[u] = *reinterpret_cast<const u32x4_t*>(we + grp * 64 + 8 * u);
+        };
+        auto run = [&](const u32x4_t(&w)[8], int grp) {
+            float a = acc[0];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const u32x4_t xv = *reinterpret_cast<const u32x4_t*>(xr + grp * 64 + 8 * u);
+                const u32x4_t wv = w[u];
+                a = fmaf(__uint_as_float(xv.x << 16), __uint_as_float(wv.x << 16), a);
+                a = fmaf(__uint_as_float(xv.x & 0xffff0000u), __uint_as_float(wv.x & 0xffff0000u), a);
+                a = fmaf(__uint_as_float(xv.y << 16), __uint_as_float(wv.y << 16), a);
+                a = fmaf(__uint_as_float(xv.y & 0xffff0000u), __uint_as_float(wv.y & 0xffff0000u), a);
+                a = fmaf(__uint_as_float(xv.z << 16), __uint_as_float(wv.z << 16), a);
+                a = fmaf(__uint_as_float(xv.z & 0xffff0000u), __uint_as_float(wv.z & 0xffff0000u), a);
+                a = fmaf(__uint_as_float(xv.w << 16), __uint_as_float(wv.w << 16), a);
+                a = fmaf(__uint_as_float(xv.w & 0xffff0000u), __uint_as_float(wv.w & 0xffff0000u), a);
+            }
+            acc[0] = a;
+        };
+        load(wa, 0);
+        for (int n = 0; n < ng; n += 2) {
+            if (n + 1 < ng) load(wb, n + 1);
+            run(wa, n);
+            if (n + 1 < ng) {
+                if (n + 2 < ng) load(wa, n + 2);
+                run(wb, n + 1);
+            }
         }
     }
-    __syncthreads();
-    if (t >= T || nc == 0) return;
-    float den = osig[tl * kMaxK];
-    for (int j = 1; j < K; ++j) den = den + osig[tl * kMaxK + j];
-    for (int j = g; j < K; j += LPT) {
-        topk_idx[(size_t)t * K + j] = oexp[tl * kMaxK + j];
-        topk_gate[(size_t)t * K + j] = osig[tl * kMaxK + j] / den;
-    }
+    __syncthreads();  // the selection reuses the x rows' LDS
+    chain_select<TPB, LPT, 1>(lds_dyn, tl, g, t, T, nc, K, on, ec, acc, bc, bias != nullptr, topk_idx, topk_gate);
 }
 
 // Exact routing of the queued tokens: all E logits by the FMA chain, then
@@ -696,8 +785,8 @@ hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, i
     else { if (ns == 16) MOE_CAND(64, 16, 16); else MOE_CAND(64, 16, 32); }
 #undef MOE_CAND
     // Exact chains: 256 (or 128) tokens per block of 1024 threads while that
-    // still gives a block per CU, then 64 tokens per block, then 16 tokens
-    // with one chain per lane for small batches.
+    // still gives a block per CU, then 64 tokens per block, then (small
+    // batches) one wave per 4 (or 2) tokens reading weights directly.
 #define MOE_CHAIN(TPBv, LPTv, CPLv, EMv, DCv)                                                               \
     hipLaunchKernelGGL((k_router_chain<TPBv, LPTv, CPLv, EMv, DCv>), dim3((d.T + TPBv - 1) / TPBv),          \
                        dim3(TPBv * LPTv), 0, s, xb, wb, bias, cand, ncand, d.T, d.d, d.E, d.K, topk_idx, topk_gate)
@@ -712,10 +801,19 @@ hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, i
         if (ns == 16) MOE_CHAIN_E(256, 4, 4, 64); else MOE_CHAIN_E(128, 8, 4, 64);
     } else if (d.T >= 256 * 64) {
         if (ns == 16) MOE_CHAIN_E(64, 4, 4, 64); else MOE_CHAIN_E(64, 8, 4, 64);
-    } else if (d.d % 128 == 0) {
-        if (ns == 16) MOE_CHAIN_E(16, 16, 1, 128); else MOE_CHAIN_E(8, 32, 1, 128);
-    } else {  // the chunk width must divide d (a multiple of 64)
-        if (ns == 16) MOE_CHAIN_E(16, 16, 1, 64); else MOE_CHAIN_E(8, 32, 1, 64);
+    } else {
+        // One wave per 64 / ns tokens, weights straight from global memory.
+        const int tpb = kWave / ns;
+        const size_t sel = (size_t)tpb * (ns * 12 + kMaxK * 8);
+        const size_t xs = (size_t)tpb * d.d * 2;
+        const size_t shm = xs > sel ? xs : sel;
+        const dim3 grid((d.T + tpb - 1) / tpb);
+        if (ns == 16)
+            hipLaunchKernelGGL(k_router_chain_direct<16>, grid, dim3(kWave), shm, s, xb, wb, bias, cand, ncand, d.T,
+                               d.d, d.E, d.K, topk_idx, topk_gate);
+        else
+            hipLaunchKernelGGL(k_router_chain_direct<32>, grid, dim3(kWave), shm, s, xb, wb, bias, cand, ncand, d.T,
+                               d.d, d.E, d.K, topk_idx, topk_gate);
     }
 #undef MOE_CHAIN_E
 #undef MOE_CHAIN
