@@ -242,10 +242,11 @@ static moe_status_t enqueue_route(const moe_desc_t& d, const WorkspacePlan& p, v
 static moe_status_t enqueue_routed_mlp(const moe_desc_t& d, const WorkspacePlan& p, void* ws, const void* x,
                                        const int32_t* sorted_slots, const int32_t* offsets, const void* w1,
                                        const void* w2, void* expert_out, hipStream_t s,
-                                       void* const* events = nullptr) {
+                                       void* const* events = nullptr, bool tiles_built = false) {
     TileDesc* tiles = region<TileDesc>(ws, p.tiles);
     int32_t* ntiles = region<int32_t>(ws, p.ntiles);
-    HIP_CHECK(launch_build_tiles(d.E, p.tile_bm, p.max_tiles, offsets, tiles, ntiles, s), "build_tiles");
+    if (!tiles_built)
+        HIP_CHECK(launch_build_tiles(d.E, p.tile_bm, p.max_tiles, offsets, tiles, ntiles, s), "build_tiles");
     if (events) HIP_CHECK(hipEventRecord(static_cast<hipEvent_t>(events[0]), s), "event record");
     GemmArgs g{};
     g.A = x;
@@ -602,10 +603,12 @@ MOE_API moe_status_t moe_layer_forward(const moe_desc_t* desc, const void* x, co
     float* sout = d.h_shared ? region<float>(workspace, p.sout) : nullptr;
 
     CHECK(enqueue_route(d, p, workspace, x, w_router, bias, idx, gate, s));
+    // The permute's scan also builds the routed experts' tile table.
     HIP_CHECK(launch_permute(d, idx, counts, offsets, slots, region<int32_t>(workspace, p.blockhist),
-                             p.n_hist_blocks, s),
+                             p.n_hist_blocks, s, p.tile_bm, p.max_tiles, region<TileDesc>(workspace, p.tiles),
+                             region<int32_t>(workspace, p.ntiles)),
               "permute");
-    CHECK(enqueue_routed_mlp(d, p, workspace, x, slots, offsets, w1, w2, eout, s, events));
+    CHECK(enqueue_routed_mlp(d, p, workspace, x, slots, offsets, w1, w2, eout, s, events, true));
     bool fused = false;
     if (d.h_shared) {
         const CombineArgs c{eout, gate, y};

@@ -160,9 +160,12 @@ hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, i
                                      uint16_t* cand, int32_t* ncand, int32_t* ovf_count, int32_t* ovf_list,
                                      int32_t* topk_idx, float* topk_gate, hipStream_t s);
 int router_cand_slots(int K);
+// Grouping of slots by expert; with a tile table (tiles != nullptr) the scan
+// kernel also cuts the segments into M-tiles of bm rows (as launch_build_tiles).
 hipError_t launch_permute(const moe_desc_t& d, const int32_t* topk_idx, int32_t* counts,
                           int32_t* offsets, int32_t* sorted_slots, int32_t* blockhist,
-                          int32_t n_blocks, hipStream_t s);
+                          int32_t n_blocks, hipStream_t s, int32_t bm = 0, int32_t max_tiles = 0,
+                          TileDesc* tiles = nullptr, int32_t* n_tiles = nullptr);
 hipError_t launch_build_tiles(int32_t E, int32_t bm, int32_t max_tiles, const int32_t* offsets,
                               TileDesc* tiles, int32_t* n_tiles, hipStream_t s);
 hipError_t launch_gemm(const moe_desc_t& d, int epilogue, int bm, const GemmArgs& a, hipStream_t s);

@@ -45,7 +45,7 @@ __device__ int block_exclusive_scan_1024(int v, int* tmp, int* total) {
     return excl;
 }
 
-__global__ __launch_bounds__(256) void k_hist(const int32_t* __restrict__ idx, int64_t n_slots,
+__global__ __launch_bounds__(1024) void k_hist(const int32_t* __restrict__ idx, int64_t n_slots,
                                               int E, int64_t chunk, int32_t* __restrict__ blockhist) {
     __shared__ int h[kMaxE];
     for (int e = threadIdx.x; e < E; e += blockDim.x) h[e] = 0;
@@ -60,13 +60,55 @@ __global__ __launch_bounds__(256) void k_hist(const int32_t* __restrict__ idx, i
     for (int e = threadIdx.x; e < E; e += blockDim.x) blockhist[(size_t)blockIdx.x * E + e] = h[e];
 }
 
+// M-tiles of height bm over every expert's segment, in expert order, by one
+// 1024-thread block. off: the E + 1 segment offsets (global memory or LDS);
+// start: kMaxE + 1 ints of LDS; tmp: 32 ints of LDS.
+__device__ void build_tiles_block(int E, int bm, int max_tiles, const int32_t* off, TileDesc* __restrict__ tiles,
+                                  int32_t* __restrict__ n_tiles, int* start, int* tmp) {
+    const int e = threadIdx.x;
+    int nt = 0;
+    if (e < E) {
+        const int cnt = off[e + 1] - off[e];
+        nt = cnt > 0 ? (cnt + bm - 1) / bm : 0;
+    }
+    int total;
+    const int excl = block_exclusive_scan_1024(nt, tmp, &total);
+    // Offsets from a caller could describe more tiles than the table holds.
+    total = min(total, max_tiles);
+    if (e < E) start[e] = excl;
+    if (e == 0) start[E] = total;
+    __syncthreads();
+    for (int q = threadIdx.x; q < total; q += blockDim.x) {
+        int lo = 0, hi = E;  // largest expert with start[expert] <= q
+        while (hi - lo > 1) {
+            const int mid = (lo + hi) >> 1;
+            if (start[mid] <= q) lo = mid; else hi = mid;
+        }
+        const int i = q - start[lo];
+        const int seg0 = off[lo];
+        const int cnt = off[lo + 1] - seg0;
+        TileDesc t;
+        t.e = lo;
+        t.row0 = seg0 + i * bm;
+        t.rows = min(bm, cnt - i * bm);
+        t.pad = 0;
+        tiles[q] = t;
+    }
+    if (threadIdx.x == 0) *n_tiles = total;
+}
+
 // One 1024-thread block. blockhist [nb][E] in: chunk histograms; out: the
-// position where chunk b's first slot of expert e goes.
+// position where chunk b's first slot of expert e goes. With a tile table
+// (tiles != nullptr) it also cuts the segments into M-tiles of bm rows, as
+// k_build_tiles does, saving that launch.
 __global__ __launch_bounds__(1024) void k_scan(int32_t* __restrict__ blockhist, int nb, int E,
                                               int32_t* __restrict__ counts,
-                                              int32_t* __restrict__ offsets) {
+                                              int32_t* __restrict__ offsets, int bm, int max_tiles,
+                                              TileDesc* __restrict__ tiles, int32_t* __restrict__ n_tiles) {
     __shared__ int buf[kScanMax];
     __shared__ int tmp[32];
+    __shared__ int offl[kMaxE + 1];
+    __shared__ int start[kMaxE + 1];
     const int n = nb * E;
     for (int i = threadIdx.x; i < n; i += blockDim.x) buf[i] = blockhist[i];
     __syncthreads();
@@ -83,11 +125,16 @@ __global__ __launch_bounds__(1024) void k_scan(int32_t* __restrict__ blockhist, 
     if ((int)threadIdx.x < E) {
         counts[threadIdx.x] = cnt;
         offsets[threadIdx.x] = excl;
+        offl[threadIdx.x] = excl;
         for (int b = 0; b < nb; ++b) buf[b * E + threadIdx.x] += excl;
     }
-    if (threadIdx.x == 0) offsets[E] = total;
+    if (threadIdx.x == 0) {
+        offsets[E] = total;
+        offl[E] = total;
+    }
     __syncthreads();
     for (int i = threadIdx.x; i < n; i += blockDim.x) blockhist[i] = buf[i];
+    if (tiles) build_tiles_block(E, bm, max_tiles, offl, tiles, n_tiles, start, tmp);
 }
 
 // Lanes of the wave whose `key` equals this lane's (only lanes with `valid`
@@ -102,11 +149,11 @@ __device__ __forceinline__ uint64_t match_peers(int key, bool valid, int nbits) 
     return peers;
 }
 
-__global__ __launch_bounds__(256) void k_scatter(const int32_t* __restrict__ idx, int64_t n_slots,
-                                                 int E, int nbits, int64_t chunk,
-                                                 const int32_t* __restrict__ blockbase,
-                                                 int32_t* __restrict__ sorted_slots) {
-    constexpr int kWaves = 4;
+__global__ __launch_bounds__(1024) void k_scatter(const int32_t* __restrict__ idx, int64_t n_slots,
+                                                  int E, int nbits, int64_t chunk,
+                                                  const int32_t* __restrict__ blockbase,
+                                                  int32_t* __restrict__ sorted_slots) {
+    constexpr int kWaves = 16;  // each wave ranks one sixteenth of the chunk, in slot order
     __shared__ int base[kWaves][kMaxE];
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
@@ -155,50 +202,23 @@ __global__ __launch_bounds__(1024) void k_build_tiles(int E, int bm, int max_til
                                                      int32_t* __restrict__ n_tiles) {
     __shared__ int start[kMaxE + 1];
     __shared__ int tmp[32];
-    const int e = threadIdx.x;
-    int nt = 0;
-    if (e < E) {
-        const int cnt = offsets[e + 1] - offsets[e];
-        nt = cnt > 0 ? (cnt + bm - 1) / bm : 0;
-    }
-    int total;
-    const int excl = block_exclusive_scan_1024(nt, tmp, &total);
-    // Offsets from a caller could describe more tiles than the table holds.
-    total = min(total, max_tiles);
-    if (e < E) start[e] = excl;
-    if (e == 0) start[E] = total;
-    __syncthreads();
-    for (int q = threadIdx.x; q < total; q += blockDim.x) {
-        int lo = 0, hi = E;  // largest expert with start[expert] <= q
-        while (hi - lo > 1) {
-            const int mid = (lo + hi) >> 1;
-            if (start[mid] <= q) lo = mid; else hi = mid;
-        }
-        const int i = q - start[lo];
-        const int seg0 = offsets[lo];
-        const int cnt = offsets[lo + 1] - seg0;
-        TileDesc t;
-        t.e = lo;
-        t.row0 = seg0 + i * bm;
-        t.rows = min(bm, cnt - i * bm);
-        t.pad = 0;
-        tiles[q] = t;
-    }
-    if (threadIdx.x == 0) *n_tiles = total;
+    build_tiles_block(E, bm, max_tiles, offsets, tiles, n_tiles, start, tmp);
 }
 
 }  // namespace
 
 hipError_t launch_permute(const moe_desc_t& d, const int32_t* topk_idx, int32_t* counts,
                           int32_t* offsets, int32_t* sorted_slots, int32_t* blockhist,
-                          int32_t n_blocks, hipStream_t s) {
+                          int32_t n_blocks, hipStream_t s, int32_t bm, int32_t max_tiles, TileDesc* tiles,
+                          int32_t* n_tiles) {
     const int64_t n_slots = (int64_t)d.T * d.K;
     const int64_t chunk = (n_slots + n_blocks - 1) / n_blocks;
     int nbits = 0;
     while ((1 << nbits) < d.E) ++nbits;
-    hipLaunchKernelGGL(k_hist, dim3(n_blocks), dim3(256), 0, s, topk_idx, n_slots, d.E, chunk, blockhist);
-    hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, s, blockhist, n_blocks, d.E, counts, offsets);
-    hipLaunchKernelGGL(k_scatter, dim3(n_blocks), dim3(256), 0, s, topk_idx, n_slots, d.E, nbits, chunk,
+    hipLaunchKernelGGL(k_hist, dim3(n_blocks), dim3(1024), 0, s, topk_idx, n_slots, d.E, chunk, blockhist);
+    hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, s, blockhist, n_blocks, d.E, counts, offsets, bm, max_tiles,
+                       tiles, n_tiles);
+    hipLaunchKernelGGL(k_scatter, dim3(n_blocks), dim3(1024), 0, s, topk_idx, n_slots, d.E, nbits, chunk,
                        blockhist, sorted_slots);
     return hipGetLastError();
 }
