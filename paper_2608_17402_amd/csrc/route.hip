@@ -249,13 +249,20 @@ __device__ __forceinline__ float sigmoid_fast(float s) {
 // Upper bound of the 2-norm of every row of a [rows, d] bf16 matrix (fp32 sum
 // of squares, inflated to cover its rounding). One wave per row. Block 0 also
 // clears the overflow counter used by the repair kernel.
-__global__ __launch_bounds__(256) void k_row_norms(const bf16_t* __restrict__ a, int rows, int d,
-                                                   float* __restrict__ out, int32_t* __restrict__ clear) {
+__global__ __launch_bounds__(256) void k_row_norms(const bf16_t* __restrict__ a, int rows_a,
+                                                   float* __restrict__ out_a, const bf16_t* __restrict__ b,
+                                                   int rows_b, float* __restrict__ out_b, int d,
+                                                   int32_t* __restrict__ clear) {
     if (clear && blockIdx.x == 0 && threadIdx.x == 0) *clear = 0;
     const int lane = threadIdx.x & (kWave - 1);
-    const int row = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
-    if (row >= rows) return;
-    const bf16_t* p = a + (size_t)row * d;
+    // One wave per row: the rows of a, then (from the next block on) those of b.
+    const int wpb = blockDim.x / kWave;
+    const int blocks_a = (rows_a + wpb - 1) / wpb;
+    const bool second = (int)blockIdx.x >= blocks_a;
+    const int row = ((int)blockIdx.x - (second ? blocks_a : 0)) * wpb + threadIdx.x / kWave;
+    if (row >= (second ? rows_b : rows_a)) return;
+    const bf16_t* p = (second ? b : a) + (size_t)row * d;
+    float* out = second ? out_b : out_a;
     float acc = 0.0f;
     for (int i = lane * 8; i < d; i += kWave * 8) {
         float v[8];
@@ -286,7 +293,7 @@ __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s
     static_assert(LPA <= kWave && kWave % LPA == 0, "token groups inside a wave");
     const int lane = threadIdx.x & (kWave - 1);
     const int g = lane % LPA;
-    const int t = blockIdx.x * (256 / LPA) + threadIdx.x / LPA;
+    const int t = blockIdx.x * (blockDim.x / LPA) + threadIdx.x / LPA;
     const bool live = t < T;  // uniform within the group: dead groups compute on -inf
     const uint64_t grp = (LPA == kWave ? ~0ull : ((1ull << LPA) - 1ull)) << (lane - g);
     const uint64_t below = grp & ((1ull << lane) - 1ull);
@@ -771,15 +778,17 @@ hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, i
                                      int32_t* topk_idx, float* topk_gate, hipStream_t s) {
     const bf16_t* xb = static_cast<const bf16_t*>(x);
     const bf16_t* wb = static_cast<const bf16_t*>(w_router);
-    hipLaunchKernelGGL(k_row_norms, dim3((d.T + 3) / 4), dim3(256), 0, s, xb, d.T, d.d, xnorm, ovf_count);
-    hipLaunchKernelGGL(k_row_norms, dim3((d.E + 3) / 4), dim3(256), 0, s, wb, d.E, d.d, wnorm, nullptr);
+    hipLaunchKernelGGL(k_row_norms, dim3((d.T + 3) / 4 + (d.E + 3) / 4), dim3(256), 0, s, xb, d.T, xnorm, wb, d.E,
+                       wnorm, d.d, ovf_count);
     const float cst = router_fast_bound_constant(d.d);
     const int ns = router_cand_slots(d.K);
-    // Candidates: 16 lanes per token (64 for more than 256 experts).
+    // Candidates: 16 lanes per token (64 for more than 256 experts); blocks
+    // of one wave for small batches, so that every CU gets work.
+    const int cand_threads = d.T >= 16384 ? 256 : kWave;
 #define MOE_CAND(LPAv, PERv, NSv)                                                                           \
-    hipLaunchKernelGGL((k_router_cand<LPAv, PERv, NSv>), dim3((d.T + 256 / LPAv - 1) / (256 / LPAv)),        \
-                       dim3(256), 0, s, s_fast, xnorm, wnorm, bias, d.T, d.E, ld, d.K, cst, cand, ncand,        \
-                       ovf_count, ovf_list)
+    hipLaunchKernelGGL((k_router_cand<LPAv, PERv, NSv>),                                                    \
+                       dim3((d.T + cand_threads / LPAv - 1) / (cand_threads / LPAv)), dim3(cand_threads), 0, s, \
+                       s_fast, xnorm, wnorm, bias, d.T, d.E, ld, d.K, cst, cand, ncand, ovf_count, ovf_list)
     if (d.E <= 64) { if (ns == 16) MOE_CAND(16, 4, 16); else MOE_CAND(16, 4, 32); }
     else if (d.E <= 256) { if (ns == 16) MOE_CAND(16, 16, 16); else MOE_CAND(16, 16, 32); }
     else { if (ns == 16) MOE_CAND(64, 16, 16); else MOE_CAND(64, 16, 32); }
