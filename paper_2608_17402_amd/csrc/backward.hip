@@ -66,18 +66,20 @@ __global__ __launch_bounds__(256) void k_transpose_w(const bf16_t* __restrict__ 
 __global__ __launch_bounds__(1024) void k_wgrad_plan(const int32_t* __restrict__ offsets, int E,
                                                     int32_t* __restrict__ koff, TileDesc* __restrict__ items,
                                                     TileDesc* __restrict__ rlist, int32_t* __restrict__ wcount) {
-    __shared__ int32_t len[kMaxE], pieces[kMaxE], ifirst[kMaxE], pfirst[kMaxE], rslot[kMaxE];
+    __shared__ int32_t len[kMaxE], pieces[kMaxE], pfirst[kMaxE], rslot[kMaxE];
+    __shared__ int32_t cursor[kWgradSlabs + 1];  // next item position per piece length (slabs)
+    __shared__ int32_t nitems_s;
     constexpr int CHUNK = kWgradSlabs * 64;
     for (int e = threadIdx.x; e < E; e += blockDim.x) {
         len[e] = max(128, (offsets[e + 1] - offsets[e] + 63) / 64 * 64);
         pieces[e] = (len[e] + CHUNK - 1) / CHUNK;
     }
     __syncthreads();
+    for (int i = threadIdx.x; i <= kWgradSlabs; i += blockDim.x) cursor[i] = 0;
     if (threadIdx.x == 0) {
         int32_t k = 0, it = 0, pt = 0, rs = 0;
         for (int e = 0; e < E; ++e) {
             koff[e] = k;
-            ifirst[e] = it;
             pfirst[e] = pieces[e] > 1 ? pt : -1;
             rslot[e] = pieces[e] > 1 ? rs : -1;
             k += len[e];
@@ -89,7 +91,33 @@ __global__ __launch_bounds__(1024) void k_wgrad_plan(const int32_t* __restrict__
         }
         koff[E] = k;
         wcount[0] = it;
+        nitems_s = it;
         wcount[1] = rs;
+    }
+    __syncthreads();
+    // Items in descending order of length (slabs, 2 .. kWgradSlabs), so that
+    // the persistent workgroups running neighbouring items stay in step and
+    // the row and column tiles of one item meet in L2 slab by slab (and the
+    // longest items start first), dealt round-robin over the XCDs: each XCD
+    // walks a contiguous range of the list, so rank p goes to range p % 8 as
+    // its (p / 8)-th item, and every range gets the same mix of lengths.
+    // Placement within one length follows LDS atomics; every item writes
+    // fixed outputs, so the order changes no result.
+    for (int e = threadIdx.x; e < E; e += blockDim.x) {
+        const int slabs = len[e] / 64, n = pieces[e];
+        const int base = slabs / n, extra = slabs % n;
+        if (extra) atomicAdd(&cursor[base + 1], extra);
+        if (n > extra) atomicAdd(&cursor[base], n - extra);
+    }
+    __syncthreads();
+    const int nitems = nitems_s;
+    if (threadIdx.x == 0) {
+        int run = 0;
+        for (int sz = kWgradSlabs; sz >= 0; --sz) {
+            const int c = cursor[sz];
+            cursor[sz] = run;
+            run += c;
+        }
     }
     __syncthreads();
     for (int e = threadIdx.x; e < E; e += blockDim.x) {
@@ -103,7 +131,8 @@ __global__ __launch_bounds__(1024) void k_wgrad_plan(const int32_t* __restrict__
             t.row0 = koff[e] + s0 * 64;
             t.rows = sz * 64;
             t.pad = pfirst[e] < 0 ? -1 : pfirst[e] + c;
-            items[ifirst[e] + c] = t;
+            const int p = atomicAdd(&cursor[sz], 1), b = p % kNumXcd;
+            items[b * (nitems / kNumXcd) + min(b, nitems % kNumXcd) + p / kNumXcd] = t;
             s0 += sz;
         }
         if (rslot[e] >= 0) rlist[rslot[e]] = TileDesc{e, pfirst[e], pieces[e], 0};
