@@ -9,6 +9,14 @@
 namespace moe {
 namespace {
 
+// 16-byte store with the non-temporal hint: the transposed operands are read
+// by a later kernel, and keeping their lines in L2 only evicts data still in
+// use (1 % of the backward at ViT-G).
+__device__ __forceinline__ void store16_nt(void* p, const uint4& v) {
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    __builtin_nontemporal_store(u32x4{v.x, v.y, v.z, v.w}, reinterpret_cast<u32x4*>(p));
+}
+
 constexpr int TT = 64;  // transpose tile (rows x columns)
 
 // out[g][c][r] = in[g][src(r)][c]: the transpose of a [G][Rs][C] bf16 tensor
@@ -46,7 +54,7 @@ __global__ __launch_bounds__(256) void k_transpose_w(const bf16_t* __restrict__ 
         bf16_t* e = reinterpret_cast<bf16_t*>(&v);
 #pragma unroll
         for (int k = 0; k < 8; ++k) e[k] = tile[r + k][c];
-        *reinterpret_cast<uint4*>(dst + (size_t)(c0 + c) * R + r0 + r) = v;
+        store16_nt(dst + (size_t)(c0 + c) * R + r0 + r, v);
     }
 }
 
@@ -216,7 +224,7 @@ __global__ __launch_bounds__(256) void k_transpose_window(const bf16_t* __restri
         bf16_t* e = reinterpret_cast<bf16_t*>(&v);
 #pragma unroll
         for (int k = 0; k < 8; ++k) e[k] = tile[r + k][c];
-        *reinterpret_cast<uint4*>(out + ((size_t)(q0 / TT) * C + c0 + c) * TT + r) = v;
+        store16_nt(out + ((size_t)(q0 / TT) * C + c0 + c) * TT + r, v);
     }
 }
 
