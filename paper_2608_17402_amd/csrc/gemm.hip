@@ -1306,7 +1306,7 @@ void k_gemm_pp(const GemmArgs a) {
                 // y is written only here and read by nothing in this kernel, so
                 // the store needs no memory clobber.
                 const uint32_t yoff = ((uint32_t)r * (uint32_t)a.N + (uint32_t)c0) * 2u;
-                asm volatile("buffer_store_dwordx4 %0, %1, %2, 0 offen\n\ts_nop 0" ::"v"(out), "v"(yoff), "s"(yres));
+                asm volatile("buffer_store_dwordx4 %0, %1, %2, 0 offen nt\n\ts_nop 0" ::"v"(out), "v"(yoff), "s"(yres));
             }
         }
     };
