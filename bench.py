@@ -245,20 +245,26 @@ def main():
     }
 
     def measure(c, reps):
-        """Whole-layer time and the routed grouped GEMM pair (HIP events that
-        moe_layer_forward records around fc1 and fc2) of layer config c."""
+        """Whole-layer time of layer config c, then (a second pass of the same
+        length) the routed grouped GEMM pair from the HIP events that
+        moe_layer_forward records around fc1 and fc2. Each recorded event
+        leaves a gap of several microseconds in the queue, which would inflate
+        the layer time of these short layers, so the first pass records none."""
         L = Layer(c)
         for _ in range(3):
             L.forward()
-        ev = binding.HipEvents(3 * reps)
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
-        for i in range(reps):
-            L.forward(ev.handles[3 * i:3 * i + 3])
+        for _ in range(reps):
+            L.forward()
         e1.record(stream)
         torch.cuda.synchronize()
         l_ms = e0.elapsed_time(e1) / reps
+        ev = binding.HipEvents(3 * reps)
+        for i in range(reps):
+            L.forward(ev.handles[3 * i:3 * i + 3])
+        torch.cuda.synchronize()
         f1 = sum(ev.elapsed_ms(3 * i, 3 * i + 1) for i in range(reps)) / reps
         f2 = sum(ev.elapsed_ms(3 * i + 1, 3 * i + 2) for i in range(reps)) / reps
         ev.close()
