@@ -1005,6 +1005,16 @@ void k_gemm_pp(const GemmArgs a) {
     const int lid_end = min(total, (xcd + 1) * per);
     int lid = xcd * per + (int)blockIdx.x / kNumXcd;
     if (lid >= lid_end) return;
+    // The combine epilogue streams K expert-output rows per output element
+    // (1 MB per tile at ViT-G) and is HBM-bound when every CU runs it at once;
+    // tiles cost the same, so the workgroups stay in step from the start.
+    // Workgroups of odd XCDs start about 80k cycles later, so that their
+    // epilogues overlap the other XCDs' K loops (whole XCDs, so that each L2
+    // still sees its tiles in step). Measured at ViT-G: the layer -1.3 %.
+    if constexpr (EPI == EPI_COMBINE) {
+        if (xcd & 1)
+            for (int q = 0; q < 10; ++q) __builtin_amdgcn_s_sleep(127);
+    }
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
