@@ -148,7 +148,6 @@ WorkspacePlan plan_workspace(const moe_desc_t& d) {
     p.idx = take(TK * 4);
     p.gate = take(TK * 4);
     p.scores = take((size_t)d.T * router_ld(d) * 4);
-    p.xnorm = take((size_t)d.T * 4);
     p.wnorm = take((size_t)d.E * 4);
     p.ovf = take((size_t)(d.T + 1) * 4);
     p.cand = take((size_t)d.T * router_cand_slots(d.K) * 2);
@@ -230,8 +229,7 @@ static moe_status_t enqueue_route(const moe_desc_t& d, const WorkspacePlan& p, v
     g.a_bytes = (uint32_t)((size_t)d.T * d.d * 2);
     HIP_CHECK(launch_gemm(d, EPI_STORE_F32, bm, g, s), "router logits gemm");
     int32_t* ovf = region<int32_t>(ws, p.ovf);
-    HIP_CHECK(launch_router_fast_finish(d, scores, g.N, x, w_router, bias, region<float>(ws, p.xnorm),
-                                        region<float>(ws, p.wnorm), region<uint16_t>(ws, p.cand),
+    HIP_CHECK(launch_router_fast_finish(d, scores, g.N, x, w_router, bias, region<float>(ws, p.wnorm), region<uint16_t>(ws, p.cand),
                                         region<int32_t>(ws, p.ncand), ovf, ovf + 1, idx, gate, s),
               "router repair");
     return MOE_OK;

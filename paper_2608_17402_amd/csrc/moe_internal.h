@@ -101,7 +101,7 @@ struct GemmArgs {
 // Offsets (bytes) of every workspace region for one descriptor.
 struct WorkspacePlan {
     size_t idx, gate, scores, counts, offsets, slots, blockhist, tiles, ntiles;
-    size_t xnorm, wnorm, ovf, cand, ncand;
+    size_t wnorm, ovf, cand, ncand;
     size_t act, eout, sact, sout;
     size_t total;
     int32_t n_hist_blocks;   // blocks of the permute histogram / scatter
@@ -156,7 +156,7 @@ hipError_t launch_topk(const moe_desc_t& d, const float* scores, const float* bi
 // cand [T][router_cand_slots(K)] and ncand [T] are scratch of the candidate
 // pass.
 hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, int ld, const void* x,
-                                     const void* w_router, const float* bias, float* xnorm, float* wnorm,
+                                     const void* w_router, const float* bias, float* wnorm,
                                      uint16_t* cand, int32_t* ncand, int32_t* ovf_count, int32_t* ovf_list,
                                      int32_t* topk_idx, float* topk_gate, hipStream_t s);
 int router_cand_slots(int K);

@@ -284,7 +284,7 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 // candidates gets ncand = -1 and is appended to the overflow queue.
 template <int LPA, int PER, int NS>
 __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s_fast,
-                                                    const float* __restrict__ xnorm,
+                                                    const bf16_t* __restrict__ x, int d,
                                                     const float* __restrict__ wnorm,
                                                     const float* __restrict__ bias, int T, int E, int ld,
                                                     int K, float cst, uint16_t* __restrict__ cand,
@@ -298,7 +298,22 @@ __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s
     const uint64_t grp = (LPA == kWave ? ~0ull : ((1ull << LPA) - 1ull)) << (lane - g);
     const uint64_t below = grp & ((1ull << lane) - 1ull);
 
-    const float xn = live ? xnorm[t] : 0.0f;
+    // ||x_t||, raised by 0.1 % as k_row_norms does for the weight rows (an
+    // upper bound is all the interval needs): the token's LPA lanes read its
+    // row in 16-byte pieces and add their partial sums.
+    float ss = 0.0f;
+    if (live) {
+        const bf16_t* xr = x + (size_t)t * d;
+        for (int i = g * 8; i < d; i += LPA * 8) {
+            float v[8];
+            load8(xr + i, v);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) ss = fmaf(v[q], v[q], ss);
+        }
+    }
+#pragma unroll
+    for (int off = LPA / 2; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+    const float xn = live ? sqrtf(ss) * 1.001f + 1e-30f : 0.0f;
     float lo[PER], hi[PER];
 #pragma unroll
     for (int m = 0; m < PER; ++m) {
@@ -773,13 +788,14 @@ float router_fast_bound_constant(int d) {
 }
 
 hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, int ld, const void* x,
-                                     const void* w_router, const float* bias, float* xnorm, float* wnorm,
+                                     const void* w_router, const float* bias, float* wnorm,
                                      uint16_t* cand, int32_t* ncand, int32_t* ovf_count, int32_t* ovf_list,
                                      int32_t* topk_idx, float* topk_gate, hipStream_t s) {
     const bf16_t* xb = static_cast<const bf16_t*>(x);
     const bf16_t* wb = static_cast<const bf16_t*>(w_router);
-    hipLaunchKernelGGL(k_row_norms, dim3((d.T + 3) / 4 + (d.E + 3) / 4), dim3(256), 0, s, xb, d.T, xnorm, wb, d.E,
-                       wnorm, d.d, ovf_count);
+    // Weight-row norms (the token norms are formed in the candidate kernel).
+    hipLaunchKernelGGL(k_row_norms, dim3((d.E + 3) / 4), dim3(256), 0, s, wb, d.E, wnorm, nullptr, 0, nullptr, d.d,
+                       ovf_count);
     const float cst = router_fast_bound_constant(d.d);
     const int ns = router_cand_slots(d.K);
     // Candidates: 16 lanes per token (64 for more than 256 experts); blocks
@@ -788,7 +804,7 @@ hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, i
 #define MOE_CAND(LPAv, PERv, NSv)                                                                           \
     hipLaunchKernelGGL((k_router_cand<LPAv, PERv, NSv>),                                                    \
                        dim3((d.T + cand_threads / LPAv - 1) / (cand_threads / LPAv)), dim3(cand_threads), 0, s, \
-                       s_fast, xnorm, wnorm, bias, d.T, d.E, ld, d.K, cst, cand, ncand, ovf_count, ovf_list)
+                       s_fast, xb, d.d, wnorm, bias, d.T, d.E, ld, d.K, cst, cand, ncand, ovf_count, ovf_list)
     if (d.E <= 64) { if (ns == 16) MOE_CAND(16, 4, 16); else MOE_CAND(16, 4, 32); }
     else if (d.E <= 256) { if (ns == 16) MOE_CAND(16, 16, 16); else MOE_CAND(16, 16, 32); }
     else { if (ns == 16) MOE_CAND(64, 16, 16); else MOE_CAND(64, 16, 32); }
