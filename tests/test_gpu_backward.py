@@ -77,6 +77,8 @@ CASES = {
     "tiles256": dict(T=3000, d=256, E=8, K=2, h=192),
     # K = 1, a single expert
     "one_expert": dict(T=333, d=128, E=1, K=1, h=128),
+    # the largest model width, d = 8192 (128 K slabs in dA and its windows)
+    "max_width": dict(T=64, d=8192, E=2, K=1, h=2048),
 }
 
 

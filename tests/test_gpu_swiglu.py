@@ -23,9 +23,9 @@ from workloads.configs import LayerConfig
 pytestmark = pytest.mark.gpu
 
 
-def _synthetic(name, T, d, E, K, h, hs, seed):
+def _synthetic(name, T, d, E, K, h, hs, seed, weight_std=0.02):
     return LayerConfig(name=name, T=T, d=d, E=E, K=K, h=h, h_shared=hs, dtype="bf16", bias="uniform", seed=seed,
-                       act="swiglu")
+                       act="swiglu", weight_std=weight_std)
 
 
 # Cases small enough for the oracle over every token. The comment names the
@@ -44,6 +44,9 @@ SMALL = {
     "h40_d64": _synthetic("sw_h40", 700, 64, 6, 3, 40, 100, seed=22),
     # the smallest widths
     "h1": _synthetic("sw_h1", 130, 128, 4, 2, 1, 1, seed=23),
+    # the largest: d = 8192, h = 8191 (ldh 8192), h_s = 8192; weights of std
+    # 0.02 sqrt(1280 / 8192) keep values at the H layer's magnitudes
+    "max_widths": _synthetic("sw_max", 40, 8192, 3, 2, 8191, 8192, seed=26, weight_std=0.02 * (1280 / 8192) ** 0.5),
 }
 
 
