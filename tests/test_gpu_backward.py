@@ -238,3 +238,42 @@ def test_swiglu_backward_matches_oracle(name):
     check_grad(dx, rdx, f"{name} dx")
     check_grad(dw13, rdw13, f"{name} dw13")
     check_grad(dw2[:, :, :h], rdw2, f"{name} dw2")
+
+
+@pytest.mark.slow
+def test_swiglu_backward_full_vith_sampled():
+    """The H layer (SwiGLU, 65 536 tokens, K = 7 of 31 experts) at full size on
+    256-row persistent tiles: routing drawn without replacement with experts 0-2
+    rare (a few dozen rows each), so that the oracle checks their whole dW13 and
+    dW2; dx on sampled tokens, each from the backward of its own K slots."""
+    from workloads import pad_last_dim
+
+    cfg = get_config("vith_swiglu_bf16")
+    inp = make_inputs(cfg, parts=["x", "w1", "w2"])
+    T, d, E, K, h = cfg.T, cfg.d, cfg.E, cfg.K, cfg.h
+    rng = np.random.default_rng(12)
+    p = np.full(E, 1.0)
+    p[:3] = 1e-4
+    keys = np.log(p)[None, :] - np.log(-np.log(rng.random((T, E))))  # Gumbel top-K: K distinct experts per token
+    idx = np.argsort(-keys, axis=1)[:, :K].astype(np.int32)
+    g = _bf16(rng, (T * K, d), 0.5)
+    w2p = pad_last_dim(inp.w2, 64)
+    dx, dw13, dw2 = run_backward(T, d, E, K, h, idx, inp.x, inp.w1, w2p, g, swiglu=True)
+    counts, offsets, slots = oracle.permute(idx, E)
+    assert 0 < counts[:3].max() < 200 and counts[3:].min() > 10000
+    x32, w1f, w2f, g32 = inp.f32("x"), inp.f32("w1"), inp.f32("w2"), bf16_bits_to_f32(g)
+    assert np.all(dw2[:, :, h:] == 0)
+    for e in range(3):
+        seg = slots[offsets[e]:offsets[e + 1]]
+        _, rw1, rw2 = oracle.expert_backward(x32[seg // K], w1f[e], w2f[e], g32[seg], True, act="swiglu")
+        check_grad(dw13[e], rw1, f"dw13[{e}] ({counts[e]} rows)")
+        check_grad(dw2[e][:, :h], rw2, f"dw2[{e}] ({counts[e]} rows)")
+    tok = np.unique(np.r_[0, T - 1, rng.choice(T, 14, replace=False)])
+    ref = np.zeros((tok.size, d))
+    for n_t, t in enumerate(tok):
+        for j in range(K):
+            e = idx[t, j]
+            rdx, _, _ = oracle.expert_backward(x32[t:t + 1], w1f[e], w2f[e], g32[t * K + j:t * K + j + 1], True,
+                                               act="swiglu")
+            ref[n_t] += rdx[0]
+    check_grad(dx[tok], ref, "sampled dx")
