@@ -183,7 +183,7 @@ hipError_t launch_transpose_w13(const void* in, int G, int h, int ld, int C, voi
 // [G][2 ld][C] fp32 with padded gate/up halves -> [G][2h][C].
 hipError_t launch_compact_rows(const float* in, int G, int h, int ld, int C, float* out, hipStream_t s);
 // Longest K window of one weight-gradient work item, in 64-column slabs.
-constexpr int kWgradSlabs = 64;
+constexpr int kWgradSlabs = 128;
 hipError_t launch_wgrad_plan(const int32_t* offsets, int E, int32_t* koff, TileDesc* items, TileDesc* rlist,
                              int32_t* wcount, hipStream_t s);
 hipError_t launch_wgrad_reduce(const float* partials, const TileDesc* rlist, const int32_t* wcount, int E,

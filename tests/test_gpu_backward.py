@@ -120,9 +120,10 @@ def test_backward_empty_and_dominant_experts():
 
 
 def test_backward_split_windows():
-    # One expert with ~8 000 rows: its K window is cut into two work items
-    # whose partial sums are added afterwards; one small expert, one empty.
-    T, d, E, K, h = 9000, 128, 3, 1, 64
+    # One expert with ~18 000 rows: its K window (work items take at most 128
+    # slabs of 64 rows) is cut into three work items whose partial sums are
+    # added afterwards; one small expert, one empty.
+    T, d, E, K, h = 20000, 128, 3, 1, 64
     rng = np.random.default_rng(6)
     idx = _idx(rng, T, E, K, np.array([0.9, 0.1, 0.0]))
     x = _bf16(rng, (T, d), 1.0)
@@ -130,7 +131,7 @@ def test_backward_split_windows():
     w2 = _bf16(rng, (E, d, h), 0.1)
     g = _bf16(rng, (T * K, d), 0.5)
     dx, dw1, dw2 = run_backward(T, d, E, K, h, idx, x, w1, w2, g)
-    assert np.sum(idx == 0) > 64 * 64  # more rows than one work item takes
+    assert np.sum(idx == 0) > 2 * 128 * 64  # more rows than two work items take
     assert np.all(dw1[2] == 0) and np.all(dw2[2] == 0)
     rdx, rdw1, rdw2 = oracle.grouped_backward(bf16_bits_to_f32(x), idx, bf16_bits_to_f32(w1), bf16_bits_to_f32(w2),
                                               bf16_bits_to_f32(g), True)
