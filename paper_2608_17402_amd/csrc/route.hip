@@ -461,7 +461,43 @@ __global__ __launch_bounds__(TPB* LPT) void k_router_chain(const bf16_t* __restr
     const int tid = threadIdx.x;
     const int g = tid % LPT;
     const int tl = tid / LPT;
-    const int t = blockIdx.x * TPB + tl;
+
+    // Token slots grouped by the chains per lane each token needs (0..CPL).
+    // A wave runs as many chains per lane as its busiest token; in token
+    // order nearly every wave holds some token with a few extra candidates,
+    // grouped most waves run only the chains of a token with K candidates.
+    // The order is ascending token within a group; a token's results do not
+    // depend on the lanes that compute it.
+    static_assert(TPB % kWave == 0 && NT >= TPB, "token slots fill whole waves");
+    constexpr int TW = TPB / kWave;
+    __shared__ int32_t sperm[TPB];
+    __shared__ int32_t sgrp[TW][CPL + 1];
+    {
+        const int lane = tid & (kWave - 1), wv = tid / kWave;
+        int key = 0;
+        uint64_t same = 0;
+        if (tid < TPB) {  // whole waves
+            const int u = blockIdx.x * TPB + tid;
+            const int n = u < T ? ncand[u] : 0;
+            key = n <= 0 ? 0 : min((n + LPT - 1) / LPT, CPL);
+#pragma unroll
+            for (int k = 0; k <= CPL; ++k) {
+                const uint64_t m = __ballot(key == k);
+                if (k == key) same = m;
+                if (lane == 0) sgrp[wv][k] = __popcll(m);
+            }
+        }
+        __syncthreads();
+        if (tid < TPB) {
+            int pos = __popcll(same & ((1ull << lane) - 1ull));
+            for (int k = 0; k < key; ++k)
+                for (int w = 0; w < TW; ++w) pos += sgrp[w][k];
+            for (int w = 0; w < wv; ++w) pos += sgrp[w][key];
+            sperm[pos] = tid;
+        }
+        __syncthreads();
+    }
+    const int t = blockIdx.x * TPB + sperm[tl];
     int nc = t < T ? ncand[t] : 0;
     nc = nc < 0 ? 0 : nc;  // queued tokens are routed by the exact-list kernel
     int ec[CPL];
