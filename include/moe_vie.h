@@ -19,7 +19,8 @@
  * Conventions shared by every entry point
  *  - All tensors are row-major and live in device memory of the current HIP
  *    device; the caller allocates and owns every buffer, the library
- *    allocates nothing and keeps no state between calls.
+ *    allocates nothing and keeps no state between calls (the one exception
+ *    is the device scratch of moe_layer_forward_noalloc, below).
  *  - "Layer dtype" (desc->dtype) is the element type of x, all weights,
  *    expert outputs and y: MOE_F32 (fp32) or MOE_BF16 (bf16 bit patterns,
  *    round-to-nearest-even). Biases and gates are fp32, indices int32.
@@ -176,6 +177,30 @@ moe_status_t moe_layer_forward(const moe_desc_t *desc, const void *x, const void
                                const void *w1s, const void *w2s, void *y, int32_t *topk_idx_out,
                                float *topk_gate_out, void *workspace, size_t workspace_bytes,
                                void *const *events, void *stream);
+
+/* Bytes of device scratch that moe_layer_forward_noalloc holds on each GPU
+ * it runs on: 64 MiB, enough for the single-image ViT-G layer (1025 tokens,
+ * d = 1536, 256 experts, K = 8, h = 768, h_s = 1536 needs about 46 MiB). */
+#define MOE_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/* moe_layer_forward for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same layer, the same kernels and the same results bit for
+ * bit, with no workspace argument and no timing events. Its scratch is a
+ * device array of MOE_NOALLOC_SCRATCH_BYTES inside the library, one per GPU,
+ * held from the first call on that GPU until the process ends; the call
+ * allocates nothing (no hipMalloc, hipFree or allocating library routine).
+ *   Arguments as for moe_layer_forward.
+ * Errors: MOE_ERR_WORKSPACE (nothing enqueued) when the layer's workspace
+ * (moe_workspace_size) exceeds MOE_NOALLOC_SCRATCH_BYTES; MOE_ERR_HIP if the
+ * scratch's device address cannot be found. Every call on one GPU uses that
+ * GPU's single scratch array, so calls that overlap on one GPU (different
+ * streams, or different host threads without ordering) race and give
+ * undefined results; calls ordered on one stream are safe. */
+moe_status_t moe_layer_forward_noalloc(const moe_desc_t *desc, const void *x, const void *w_router,
+                                       const float *bias, const void *w1, const void *w2,
+                                       const void *w1s, const void *w2s, void *y, int32_t *topk_idx_out,
+                                       float *topk_gate_out, void *stream);
 
 /* Bytes of device workspace that moe_grouped_mlp_backward needs for `desc`
  * (bf16 layers). Writes *bytes; validates desc. */

@@ -28,7 +28,7 @@ STATUS = {0: "MOE_OK", 1: "MOE_ERR_INVALID_ARG", 2: "MOE_ERR_UNSUPPORTED", 3: "M
 # Public entry points declared in include/moe_vie.h.
 EXPORTS = ("moe_status_string", "moe_last_error", "moe_workspace_size", "moe_route", "moe_permute",
            "moe_grouped_mlp", "moe_combine", "moe_layer_forward", "moe_bias_update", "moe_backward_workspace_size",
-           "moe_grouped_mlp_backward")
+           "moe_grouped_mlp_backward", "moe_layer_forward_noalloc")
 MOE_BIAS_SIGN = 0
 MOE_BIAS_ZSCORE = 1
 
@@ -86,6 +86,8 @@ def load(path: Optional[str] = None):
     lib.moe_combine.restype = st
     lib.moe_layer_forward.argtypes = [D, P, P, P, P, P, P, P, P, P, P, P, S, P, P]
     lib.moe_layer_forward.restype = st
+    lib.moe_layer_forward_noalloc.argtypes = [D, P, P, P, P, P, P, P, P, P, P, P]
+    lib.moe_layer_forward_noalloc.restype = st
     lib.moe_bias_update.argtypes = [D, P, P, ctypes.c_float, ctypes.c_int32, P]
     lib.moe_bias_update.restype = st
     lib.moe_backward_workspace_size.argtypes = [D, ctypes.POINTER(ctypes.c_size_t)]
@@ -189,6 +191,20 @@ def moe_layer_forward(desc, x, w_router, bias, w1, w2, w1s, w2s, y, topk_idx_out
                                     _ptr(topk_gate_out, "topk_gate_out", torch.float32),
                                     _ptr(workspace, "workspace"), workspace.numel(), ev, _stream(stream)),
            "moe_layer_forward")
+
+
+def moe_layer_forward_noalloc(desc, x, w_router, bias, w1, w2, w1s, w2s, y, topk_idx_out=None,
+                              topk_gate_out=None, stream=None):
+    """moe_layer_forward on the library's own per-GPU scratch (no workspace)."""
+    dt = torch_dtype(desc)
+    _check(load().moe_layer_forward_noalloc(
+        ctypes.byref(desc), _ptr(x, "x", dt), _ptr(w_router, "w_router", dt), _ptr(bias, "bias", torch.float32),
+        _ptr(w1, "w1", dt), _ptr(w2, "w2", dt), _ptr(w1s, "w1s", dt), _ptr(w2s, "w2s", dt), _ptr(y, "y", dt),
+        _ptr(topk_idx_out, "topk_idx_out", torch.int32), _ptr(topk_gate_out, "topk_gate_out", torch.float32),
+        _stream(stream)), "moe_layer_forward_noalloc")
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20
 
 
 def backward_workspace_size(desc: MoeDesc) -> int:

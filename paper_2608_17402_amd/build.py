@@ -43,7 +43,7 @@ EXTRA = {
     "route.hip": ["-ffp-contract=off"],
     "balance.hip": ["-ffp-contract=off"],
 }
-SOURCES = ["route.hip", "permute.hip", "gemm.hip", "combine.hip", "balance.hip", "backward.hip", "moe_api.cpp"]
+SOURCES = ["route.hip", "permute.hip", "gemm.hip", "combine.hip", "balance.hip", "backward.hip", "noalloc.hip", "moe_api.cpp"]
 
 
 def _compile(src: str) -> str:

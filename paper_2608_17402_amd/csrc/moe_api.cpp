@@ -19,10 +19,15 @@ namespace {
 
 thread_local char g_err[512];
 
+moe_status_t vfail(moe_status_t st, const char* fmt, va_list ap) {
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    return st;
+}
+
 moe_status_t fail(moe_status_t st, const char* fmt, ...) {
     va_list ap;
     va_start(ap, fmt);
-    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    vfail(st, fmt, ap);
     va_end(ap);
     return st;
 }
@@ -31,6 +36,18 @@ moe_status_t ok() {
     g_err[0] = 0;
     return MOE_OK;
 }
+
+}  // namespace
+
+moe_status_t set_last_error(moe_status_t st, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vfail(st, fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+namespace {
 
 moe_status_t hip_fail(hipError_t e, const char* where) {
     return fail(MOE_ERR_HIP, "%s: %s", where, hipGetErrorString(e));

@@ -110,6 +110,9 @@ struct WorkspacePlan {
 };
 
 size_t elem_size(int32_t dtype);
+// Records the message of a failing call (read back by moe_last_error) and
+// returns `st`.
+moe_status_t set_last_error(moe_status_t st, const char* fmt, ...);
 WorkspacePlan plan_workspace(const moe_desc_t& d);
 
 // Workspace of the expert-MLP backward: the forward plan (tile table,

@@ -171,3 +171,25 @@ def test_backward_validation(lib):
                                         None) == 3
     assert lib.moe_grouped_mlp_backward(d, fake, fake, fake, fake, fake, fake, fake, fake, P((1 << 20) + 8),
                                         fake, S(1 << 40), None) == 1
+
+
+def test_noalloc_rejects_before_any_hip_call(lib):
+    """The allocation-free layer forward validates the descriptor and its
+    scratch need on the host first: a layer whose workspace exceeds the
+    library's scratch, or a bad descriptor, is refused without a HIP call."""
+    P = ctypes.c_void_p
+    fake = P(1 << 20)
+    big = binding.make_desc(65536, 1536, 256, 8, 768, 1536, 1.0, "bf16")
+    _, need = _ws(big)
+    assert need > binding.NOALLOC_SCRATCH_BYTES
+    assert lib.moe_layer_forward_noalloc(ctypes.byref(big), fake, fake, None, fake, fake, fake, fake, fake, None,
+                                         None, None) == 3
+    assert b"scratch" in lib.moe_last_error()
+    bad = binding.make_desc(100, 64, 8, 0, 64)
+    assert lib.moe_layer_forward_noalloc(ctypes.byref(bad), fake, fake, None, fake, fake, None, None, fake, None,
+                                         None, None) == 1
+    # The single-image ViT-G layer fits.
+    one = binding.make_desc(1025, 1536, 256, 8, 768, 1536, 1.0, "bf16")
+    assert _ws(one)[1] <= binding.NOALLOC_SCRATCH_BYTES
+    text = open(HEADER).read()
+    assert "#define MOE_NOALLOC_SCRATCH_BYTES (64u << 20)" in text and binding.NOALLOC_SCRATCH_BYTES == 64 << 20
