@@ -8,7 +8,10 @@
  *   sel    = top-K of Sigmoid(s) + b                 b only selects experts
  *   g'_e   = Sigmoid(s_e) / sum_{i in sel} Sigmoid(s_i)     for e in sel
  *   y      = sum_{e in sel} g'_e E_e(x) + lambda * E_shared(x)
- *   E(x)   = W2 GELU(W1 x)                           fc1 -> exact-erf GELU -> fc2
+ *   E(x)   = W2 GELU(W1 x)                           fc1 -> GELU -> fc2
+ * GELU(v) = v Phi(v): fp32 layers evaluate the erf form with the device erff;
+ * bf16 layers use v times the sigmoid of a clamped odd quintic in v, within
+ * 2.6e-5 (absolute) of the erf form (see moe_grouped_mlp).
  * or, with MOE_FLAG_SWIGLU, SwiGLU experts (appendix "MoE Kernel",
  * Algorithm 1, Phase 2, and the SwiGLU MLPs of appendix "Implementation
  * Details"):
@@ -71,9 +74,11 @@ typedef enum { MOE_F32 = 0, MOE_BF16 = 1 } moe_dtype_t;
 
 /* Layer descriptor. Limits: 1 <= T, T*K < 2^31; 1 <= K <= 16; K <= E <= 1024;
  * 64 <= d <= 8192 a multiple of 64; h and h_shared (0 = no shared expert)
- * at most 8192 and, for GELU experts, multiples of 64 and >= 64; T*d,
- * T*K*ldh and T*ldh_s elements below 4 GiB (ldh = h for GELU experts); flags
- * a combination of MOE_FLAG_* bits (MOE_FLAG_SWIGLU needs dtype MOE_BF16). */
+ * at most 8192 and, for GELU experts, multiples of 64 and >= 64; x
+ * (T*d elements), the expert activations (T*K*ldh) and the shared
+ * activations (T*ldh_s) each below 4 GiB in bytes of the layer dtype (ldh = h
+ * for GELU experts); flags a combination of MOE_FLAG_* bits (MOE_FLAG_SWIGLU
+ * needs dtype MOE_BF16). */
 typedef struct {
     int32_t T;        /* tokens                                   */
     int32_t d;        /* model width                              */

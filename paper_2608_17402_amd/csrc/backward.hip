@@ -63,8 +63,9 @@ __global__ __launch_bounds__(256) void k_transpose_w(const bf16_t* __restrict__ 
 //    operands, its row count rounded up to a multiple of 64 (the K slab) and
 //    to at least two slabs (the persistent kernel's pipeline holds two; an
 //    empty expert's window is all zeros, so its gradient comes out 0);
-//  - work items: each window cut into pieces of at most kWgradSlabs slabs, of
-//    even size (so every piece keeps two slabs or more), so that no tile runs
+//  - work items: each window cut into pieces of at most kWgradSlabs slabs,
+//    split evenly (sizes differ by at most one slab, and every piece keeps
+//    at least two slabs, as a window does), so that no tile runs
 //    much longer than the others under a skewed load. An expert with one
 //    piece writes its gradient directly (dest = -1); the pieces of a longer
 //    window write partial blocks dest = first .. first + n - 1, summed

@@ -113,8 +113,8 @@ def test_swiglu_shared_expert_through_grouped_mlp():
     check_close(host(out), ref, True, "swiglu shared via grouped")
 
 
-# Larger shapes, checked on the whole routing and on sampled tokens.
-SAMPLED = {
+# Larger shapes, checked on every token.
+FULL = {
     # the paper's H layer at 64 x 1024 tokens: routed and shared experts on
     # 256-row persistent tiles, K = 7 (separate combine)
     "vith_full": (get_config("vith_swiglu_bf16"), None),
@@ -129,22 +129,19 @@ SAMPLED = {
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("name", sorted(SAMPLED))
-def test_swiglu_sampled_layer(name):
-    cfg, tail0 = SAMPLED[name]
+@pytest.mark.parametrize("name", sorted(FULL))
+def test_swiglu_full_layer_every_token(name):
+    cfg, tail0 = FULL[name]
     inp = make_inputs(cfg)
     lay = _device_layer(inp)
     y, idx, gate = lay.forward()
     torch.cuda.synchronize()
-    x, wr = inp.f32("x"), inp.f32("w_router")
-    ref_idx, ref_gate = oracle.route(x, wr, inp.bias, cfg.K)
-    assert np.array_equal(host(idx), ref_idx) and np.array_equal(host(gate), ref_gate)
-    rng = np.random.default_rng(2)
-    tok = [0, cfg.T - 1, *rng.choice(cfg.T, 40, replace=False)]
+    print(f"[{name}] T={cfg.T}: GPU layer done, oracle over every token", flush=True)
+    o_idx, o_gate, y_ref = oracle.layer(inp.f32("x"), inp.f32("w_router"), inp.bias, inp.f32("w1"),
+                                        inp.f32("w2"), inp.f32("w1s"), inp.f32("w2s"), cfg.K, cfg.lam, True,
+                                        act="swiglu")
+    assert np.array_equal(host(idx), o_idx) and np.array_equal(host(gate), o_gate)
+    yh = host(y)
+    check_close(yh, y_ref, True, f"{name} y (every token)")
     if tail0 is not None:
-        tok += list(range(tail0, cfg.T, 5))
-    tok = np.unique(np.asarray(tok)).astype(np.int32)
-    o_idx, _, y_ref = oracle.layer(x, wr, inp.bias, inp.f32("w1"), inp.f32("w2"), inp.f32("w1s"),
-                                   inp.f32("w2s"), cfg.K, cfg.lam, True, tokens=tok, act="swiglu")
-    assert np.array_equal(o_idx, ref_idx[tok])
-    check_close(host(y)[tok], y_ref, True, f"{name} sampled y")
+        check_close(yh[tail0:], y_ref[tail0:], True, f"{name} y (tail tile)")
