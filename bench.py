@@ -5,11 +5,14 @@
 
 One step is one moe_layer_forward (route, permute, grouped routed experts,
 shared expert, combine) over a seeded synthetic batch already resident in
-HBM. Prints ONE JSON line: whole-layer tokens/s over the K timed steps, the
-roofline of the dominant kernel pair (the routed grouped GEMM, fc1 + fc2),
-per-stage times, the single-image (weight-read bound) layer, the SwiGLU-expert
-layers (the paper's H layer and the single-image shape), and the CPU oracle
-timed on a bounded sample of the same workload.
+HBM. Prints ONE JSON line: whole-layer tokens/s over the K timed steps (with
+the median, p10 and p90 of the per-step times), the roofline of the dominant
+kernel pair (the routed grouped GEMM, fc1 + fc2), per-stage times and
+algorithmic GB/s, the ViT-L and ViT-B layers (MFMA bound), the single-image
+(weight-read bound) layer, the SwiGLU-expert layers (the paper's H layer and
+the single-image shape), a same-box dense bf16 GEMM reference (hipBLASLt
+through torch) at the routed GEMMs' shapes, and the CPU oracle timed on a
+bounded sample of the same workload.
 """
 
 from __future__ import annotations
@@ -42,13 +45,20 @@ TRAFFIC_BYTES = {"vitg_skew_bf16": 6933255540, "single_image_bf16": 1285204920,
                  "vith_swiglu_bf16": 6586777491, "single_image_swiglu_bf16": 1891910413}
 
 
+# Every source that changes the GEMM pair's HBM bytes: the kernels, the tile
+# size choice and workspace plan, the tile table, and the workloads (the
+# skewed layer's stored bias decides its expert loads).
+TRAFFIC_SOURCES = ("paper_2608_17402_amd/csrc/gemm.hip", "paper_2608_17402_amd/csrc/moe_internal.h",
+                   "paper_2608_17402_amd/csrc/moe_api.cpp", "paper_2608_17402_amd/csrc/permute.hip",
+                   "workloads/configs.py", "workloads/generate.py", "tests/golden/vitg_skew_bias_seed0.txt")
+
+
 def gemm_source_hash():
     import hashlib
 
-    csrc = os.path.join(ROOT, "paper_2608_17402_amd", "csrc")
     m = hashlib.sha256()
-    for f in ("gemm.hip", "moe_internal.h"):
-        with open(os.path.join(csrc, f), "rb") as fh:
+    for f in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
             m.update(fh.read())
     return m.hexdigest()[:16]
 
@@ -57,6 +67,26 @@ def traffic_bytes(workload):
     if gemm_source_hash() != TRAFFIC_SOURCE_HASH:
         return None
     return TRAFFIC_BYTES.get(workload)
+
+
+def stage_bytes(c):
+    """Algorithmic HBM bytes of the memory-bound stages (each tensor read or
+    written once): route reads x and the router weights and writes the
+    indices and gates; permute reads the indices and writes the slots (plus
+    counts and offsets); combine reads the K expert-output rows, the shared
+    output and the gates and writes y."""
+    es = 2 if c.dtype == "bf16" else 4
+    T, K, d, E = c.T, c.K, c.d, c.E
+    return {
+        "route": T * d * es + E * d * es + T * K * 8,
+        "permute": T * K * 4 * 2 + (2 * E + 1) * 4,
+        "combine": T * K * d * es + (T * d * es if c.h_shared else 0) + T * K * 4 + T * d * es,
+    }
+
+
+def stage_gbs(c, stages_ms):
+    b = stage_bytes(c)
+    return {k: round(b[k] / (stages_ms[k] * 1e-3) / 1e9, 1) for k in b if k in stages_ms}
 
 
 def parse():
@@ -69,14 +99,19 @@ def parse():
     p.add_argument("--no-single-image", action="store_true")
     p.add_argument("--swiglu-configs", default="vith_swiglu_bf16,single_image_swiglu_bf16",
                    help="SwiGLU-expert layers measured beside the main workload (comma-separated, '' for none)")
+    p.add_argument("--mfma-configs", default="vitl_bf16,vitb_bf16",
+                   help="further MFMA-bound GELU layers measured beside the main workload ('' for none)")
+    p.add_argument("--no-dense-reference", action="store_true",
+                   help="skip the same-box hipBLASLt dense GEMM reference")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-backward", action="store_true",
                    help="skip the expert-MLP backward (training) measurement on the main workload")
     p.add_argument("--cpu-seconds", type=float, default=15.0,
                    help="target CPU time of the oracle sample")
     p.add_argument("--stage-reps", type=int, default=10)
-    p.add_argument("--mode", choices=("layer", "gemm", "copy"), default="layer",
+    p.add_argument("--mode", choices=("layer", "gemm", "stages", "copy"), default="layer",
                    help="layer: the benchmark; gemm: only the routed grouped GEMMs of --config, repeated "
+                        "(hardware-counter runs); stages: route, permute and combine of --config, repeated "
                         "(hardware-counter runs); copy: a plain device copy of --copy-mib MiB "
                         "(calibration of the byte counters)")
     p.add_argument("--copy-mib", type=int, default=1024)
@@ -184,6 +219,18 @@ def main():
     cfg = get_config(args.config)
     lay = Layer(cfg)
 
+    if args.mode == "stages":
+        # The non-GEMM stages, each repeated, for the byte counters: route,
+        # permute and the separate combine kernel (on the layer's own routing).
+        st = lay.stages()
+        lay.forward()
+        for name in ("route", "permute", "combine"):
+            for _ in range(args.steps):
+                st[name]()
+        torch.cuda.synchronize()
+        print(json.dumps({"mode": "stages", "workload": cfg.name, "launches_per_stage": args.steps}), flush=True)
+        return
+
     if args.mode == "gemm":
         st = lay.stages()
         st["route"]()
@@ -200,15 +247,18 @@ def main():
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
     hev = binding.HipEvents(3 * args.steps)
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # One event between consecutive steps (per-step times for the median and
+    # percentiles); the first and the last bracket the timed region.
+    sev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     wall0 = time.perf_counter()
-    ev0.record(stream)
+    sev[0].record(stream)
     for i in range(args.steps):
         lay.forward(hev.handles[3 * i:3 * i + 3])
-    ev1.record(stream)
+        sev[i + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    ms = ev0.elapsed_time(ev1) / args.steps
+    ms = sev[0].elapsed_time(sev[-1]) / args.steps
+    step_ms = np.array([sev[i].elapsed_time(sev[i + 1]) for i in range(args.steps)])
     value = cfg.T / (ms * 1e-3)
     fc1_ms = sum(hev.elapsed_ms(3 * i, 3 * i + 1) for i in range(args.steps)) / args.steps
     fc2_ms = sum(hev.elapsed_ms(3 * i + 1, 3 * i + 2) for i in range(args.steps)) / args.steps
@@ -237,10 +287,15 @@ def main():
                    "tokens_per_image": cfg.tokens_per_image, "d_model": cfg.d, "experts": cfg.E, "top_k": cfg.K,
                    "expert_hidden": cfg.h, "shared_hidden": cfg.h_shared, "bias": cfg.bias},
         "us_per_layer": round(ms * 1e3, 1),
+        "step_us": {"median": round(float(np.median(step_ms)) * 1e3, 1),
+                    "p10": round(float(np.percentile(step_ms, 10)) * 1e3, 1),
+                    "p90": round(float(np.percentile(step_ms, 90)) * 1e3, 1),
+                    "min": round(float(step_ms.min()) * 1e3, 1), "max": round(float(step_ms.max()) * 1e3, 1)},
         "layer_gemm_tflops": round(layer_flops / (ms * 1e-3) / 1e12, 2),
         "layer_gemm_frac_of_bf16_peak": round(layer_flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         "roofline": roofline,
         "stages_us": {k: round(v * 1e3, 1) for k, v in stages_ms.items()},
+        "stages_gbs": stage_gbs(cfg, stages_ms),
         "timed_wall_s": round(wall, 3),
     }
 
@@ -269,6 +324,57 @@ def main():
         f2 = sum(ev.elapsed_ms(3 * i + 1, 3 * i + 2) for i in range(reps)) / reps
         ev.close()
         return L, l_ms, f1, f2
+
+    def dense_reference(c, routed_tflops):
+        """Same-box context for the routed grouped GEMM: hipBLASLt (through
+        torch) bf16 GEMMs of the same total shape, fc1 [T K, d] x [d, h] and
+        fc2 [T K, h] x [h, d] as single dense products, and as a batch of E
+        equal expert blocks of T K / E rows (torch.bmm with contiguous
+        operands); and the GB/s of a 1 GiB device copy, the context of the
+        HBM-bound stages. Random operands; weights in the [out, in] layout."""
+        M, d, h, E = c.T * c.K, c.d, c.h, c.E
+        g = torch.Generator(device="cuda").manual_seed(3)
+
+        def rnd(*shape):
+            return torch.randn(*shape, device="cuda", generator=g).to(torch.bfloat16)
+
+        res = {}
+        a1, w1 = rnd(M, d), rnd(h, d)
+        a2, w2 = rnd(M, h), rnd(d, h)
+        fl = 2.0 * M * d * h
+        reps = 10
+        t1 = time_calls(lambda: torch.nn.functional.linear(a1, w1), reps)
+        t2 = time_calls(lambda: torch.nn.functional.linear(a2, w2), reps)
+        del a1, a2
+        m = M // E
+        b1, wb1 = rnd(E, m, d), rnd(E, d, h)
+        b2, wb2 = rnd(E, m, h), rnd(E, h, d)
+        fb = 2.0 * E * m * d * h
+        t3 = time_calls(lambda: torch.bmm(b1, wb1), reps)
+        t4 = time_calls(lambda: torch.bmm(b2, wb2), reps)
+        del b1, b2, wb1, wb2
+        # A plain device copy of 1 GiB: the HBM bandwidth a streaming kernel reaches here.
+        ca = torch.empty(1 << 29, dtype=torch.bfloat16, device="cuda").fill_(1)
+        cb = torch.empty_like(ca)
+        tc = time_calls(lambda: cb.copy_(ca), reps)
+        del ca, cb
+
+        def tf(f, t):
+            return round(f / (t * 1e-3) / 1e12, 1)
+
+        pair = tf(2 * fl, t1 + t2)
+        res = {
+            "library": "hipBLASLt via torch (bf16 in, fp32 accumulate, bf16 out)",
+            "dense_fc1": {"shape": [M, d, h], "us": round(t1 * 1e3, 1), "tflops": tf(fl, t1)},
+            "dense_fc2": {"shape": [M, h, d], "us": round(t2 * 1e3, 1), "tflops": tf(fl, t2)},
+            "dense_pair_tflops": pair, "dense_pair_frac": round(pair / PEAK_BF16_TFLOPS, 4),
+            "batched_fc1": {"shape": [E, m, d, h], "us": round(t3 * 1e3, 1), "tflops": tf(fb, t3)},
+            "batched_fc2": {"shape": [E, m, h, d], "us": round(t4 * 1e3, 1), "tflops": tf(fb, t4)},
+            "batched_pair_tflops": tf(2 * fb, t3 + t4),
+            "routed_pair_over_dense_pair": round(routed_tflops / pair, 4),
+            "copy_gbs": round(2 * (1 << 30) / (tc * 1e-3) / 1e9, 1),
+        }
+        return res
 
     def backward_line(c, L):
         """Expert-MLP backward on layer L's own routing: five products of
@@ -329,6 +435,22 @@ def main():
                          "algorithmic_flops_per_launch": fl, "avg_launch_us": round((f1 + f2) * 1e3, 2),
                          "fc1_us": round(f1 * 1e3, 2), "fc2_us": round(f2 * 1e3, 2)},
         }
+
+    if not args.no_dense_reference and cfg.dtype == "bf16":
+        out["dense_reference"] = dense_reference(cfg, achieved)
+
+    mf_names = [n for n in args.mfma_configs.split(",") if n]
+    if mf_names:
+        out["mfma_layers"] = {}
+        for name in mf_names:
+            c = get_config(name)
+            L, l_ms, f1, f2 = measure(c, max(args.steps, 20))
+            line = mfma_line(c, l_ms, f1, f2)
+            st_ms = {k: time_calls(f, args.stage_reps) for k, f in L.stages().items()}
+            line["stages_us"] = {k: round(v * 1e3, 1) for k, v in st_ms.items()}
+            line["stages_gbs"] = stage_gbs(c, st_ms)
+            out["mfma_layers"][name] = line
+            del L
 
     if not args.no_single_image:
         c5 = get_config(args.single_image_config)
