@@ -109,11 +109,12 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=15.0,
                    help="target CPU time of the oracle sample")
     p.add_argument("--stage-reps", type=int, default=10)
-    p.add_argument("--mode", choices=("layer", "gemm", "stages", "copy"), default="layer",
+    p.add_argument("--mode", choices=("layer", "gemm", "stages", "dense", "copy"), default="layer",
                    help="layer: the benchmark; gemm: only the routed grouped GEMMs of --config, repeated "
                         "(hardware-counter runs); stages: route, permute and combine of --config, repeated "
-                        "(hardware-counter runs); copy: a plain device copy of --copy-mib MiB "
-                        "(calibration of the byte counters)")
+                        "(hardware-counter runs); dense: hipBLASLt (torch) dense bf16 GEMMs of the routed "
+                        "GEMMs' total shapes, repeated (hardware-counter runs); copy: a plain device copy of "
+                        "--copy-mib MiB (calibration of the byte counters)")
     p.add_argument("--copy-mib", type=int, default=1024)
     return p.parse_args()
 
@@ -217,6 +218,21 @@ def main():
         return
 
     cfg = get_config(args.config)
+    if args.mode == "dense":
+        # fc1 [T K, d] x [d, h] and fc2 [T K, h] x [h, d], weights in the [out, in] layout.
+        M = cfg.T * cfg.K
+        g = torch.Generator(device="cuda").manual_seed(3)
+        a1 = torch.randn(M, cfg.d, device="cuda", generator=g).to(torch.bfloat16)
+        w1 = torch.randn(cfg.h, cfg.d, device="cuda", generator=g).to(torch.bfloat16)
+        a2 = torch.randn(M, cfg.h, device="cuda", generator=g).to(torch.bfloat16)
+        w2 = torch.randn(cfg.d, cfg.h, device="cuda", generator=g).to(torch.bfloat16)
+        for _ in range(args.warmup + args.steps):
+            torch.nn.functional.linear(a1, w1)
+            torch.nn.functional.linear(a2, w2)
+        torch.cuda.synchronize()
+        print(json.dumps({"mode": "dense", "workload": cfg.name, "shapes": [[M, cfg.d, cfg.h], [M, cfg.h, cfg.d]],
+                          "launch_pairs": args.warmup + args.steps}), flush=True)
+        return
     lay = Layer(cfg)
 
     if args.mode == "stages":
