@@ -385,7 +385,8 @@ void k_gemm_bf16(const GemmArgs a) {
         xoff[ks] = base + (wm * WTM) * ROWB + k;
         woff[ks] = base + BM * ROWB + (wn * WTN) * ROWB + k;
     }
-    // K range: the whole row, or (weight gradients) the group's window.
+    // K range: the whole row, or (weight gradients) the group's window, or
+    // (split K, dense fp32 output) part blockIdx.y of gridDim.y equal parts.
     int nk = Kd / BK;
     uint32_t kbase = 0;
     TileDesc item{};
@@ -393,6 +394,10 @@ void k_gemm_bf16(const GemmArgs a) {
         item = a.tiles[tc.e];
         nk = item.rows / BK;
         kbase = (uint32_t)item.row0 * 2;
+    }
+    if constexpr (!GROUPED && EPI == EPI_STORE_F32) {
+        nk /= (int)gridDim.y;
+        kbase = (uint32_t)blockIdx.y * (uint32_t)nk * BK * 2;
     }
 
     auto issue = [&](int stage, int kslab) {
@@ -560,6 +565,8 @@ void k_gemm_bf16(const GemmArgs a) {
             if (r < tc.rows && (!SWIGLU || ocol0 < a.act_ld)) {
                 size_t orow = O_SCATTER ? (size_t)srow[r] : (size_t)(tc.row0 + r);
                 void* obase = a.C;
+                if constexpr (!GROUPED && EPI == EPI_STORE_F32)  // split K: this part's partial sums
+                    obase = static_cast<float*>(a.C) + (size_t)blockIdx.y * a.dense_rows * a.N;
                 if (WGRAD) {  // the expert's gradient, or the item's partial block
                     orow += (size_t)(item.pad < 0 ? item.e : item.pad) * a.dense_rows;
                     if (item.pad >= 0) obase = a.C2;
@@ -1838,7 +1845,10 @@ hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
     const int n_n = a.N / BN;
     const long long total = (long long)a.max_tiles * n_n;
     const long long grid = (total + kNumXcd - 1) / kNumXcd * kNumXcd;
-    hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, BK, ST, EPI, GROUPED, WPE>), dim3((unsigned)grid),
+    // Split K (dense fp32 output only): the parts along the grid's y.
+    const int splits = (!GROUPED && EPI == EPI_STORE_F32 && a.k_splits > 1) ? a.k_splits : 1;
+    if (splits > 1 && (a.Kdim / BK) % splits) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, BK, ST, EPI, GROUPED, WPE>), dim3((unsigned)grid, splits),
                        dim3(WM * WN * kWave), 0, s, a);
     return hipGetLastError();
 }

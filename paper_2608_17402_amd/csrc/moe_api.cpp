@@ -146,6 +146,24 @@ size_t elem_size(int32_t dtype) { return dtype == MOE_BF16 ? 2 : 4; }
 // of the MFMA logits GEMM (columns past E are computed from zero weight rows).
 static int32_t router_ld(const moe_desc_t& d) { return (d.E + 63) / 64 * 64; }
 
+static bool fast_router(const moe_desc_t& d) { return d.dtype == MOE_BF16 && !(d.flags & MOE_FLAG_EXACT_ROUTER); }
+
+// Rows of the router logits GEMM's M-tiles (256 once the batch gives each CU
+// tiles of 256 rows, else 64).
+static int router_bm(const moe_desc_t& d) { return (int64_t)d.T * router_ld(d) >= (int64_t)200 * 65536 ? 256 : 64; }
+
+// K split of the fast router's logits GEMM. Small batches have too few
+// 64-row tiles to occupy the chip (17 x 4 for one image against 256 CUs), so
+// the d / 64 K slabs are split over up to 8 parts of at least two slabs, each
+// writing its own partial logits; the candidate kernel adds them in order.
+static int32_t router_splits(const moe_desc_t& d) {
+    if (!fast_router(d) || router_bm(d) != 64 || d.T >= 8192) return 1;
+    const int nk = d.d / 64;
+    for (int p = 8; p >= 2; p /= 2)
+        if (nk % p == 0 && nk / p >= 2) return p;
+    return 1;
+}
+
 WorkspacePlan plan_workspace(const moe_desc_t& d) {
     WorkspacePlan p;
     const size_t es = elem_size(d.dtype);
@@ -164,8 +182,10 @@ WorkspacePlan plan_workspace(const moe_desc_t& d) {
     };
     p.idx = take(TK * 4);
     p.gate = take(TK * 4);
-    p.scores = take((size_t)d.T * router_ld(d) * 4);
+    p.router_splits = router_splits(d);
+    p.scores = take((size_t)p.router_splits * d.T * router_ld(d) * 4);
     p.wnorm = take((size_t)d.E * 4);
+    p.wr32 = take(fast_router(d) && router_small_batch(d) ? (size_t)d.E * d.d * 4 : 0);
     p.ovf = take((size_t)(d.T + 1) * 4);
     p.cand = take((size_t)d.T * router_cand_slots(d.K) * 2);
     p.ncand = take((size_t)d.T * 4);
@@ -218,8 +238,6 @@ BackwardPlan plan_backward(const moe_desc_t& d) {
     return b;
 }
 
-static bool fast_router(const moe_desc_t& d) { return d.dtype == MOE_BF16 && !(d.flags & MOE_FLAG_EXACT_ROUTER); }
-
 // Router and gating: exact chain for every logit, or MFMA logits plus exact
 // repair of the candidates (same result).
 static moe_status_t enqueue_route(const moe_desc_t& d, const WorkspacePlan& p, void* ws, const void* x,
@@ -241,12 +259,14 @@ static moe_status_t enqueue_route(const moe_desc_t& d, const WorkspacePlan& p, v
     g.Kdim = d.d;
     g.route_k = 1;
     g.row_mode = ROWS_IDENTITY;
-    const int bm = (int64_t)d.T * g.N >= (int64_t)200 * 65536 ? 256 : 64;
+    const int bm = router_bm(d);
     g.max_tiles = (d.T + bm - 1) / bm;
     g.a_bytes = (uint32_t)((size_t)d.T * d.d * 2);
+    g.k_splits = p.router_splits;
     HIP_CHECK(launch_gemm(d, EPI_STORE_F32, bm, g, s), "router logits gemm");
     int32_t* ovf = region<int32_t>(ws, p.ovf);
-    HIP_CHECK(launch_router_fast_finish(d, scores, g.N, x, w_router, bias, region<float>(ws, p.wnorm), region<uint16_t>(ws, p.cand),
+    HIP_CHECK(launch_router_fast_finish(d, scores, g.N, p.router_splits, x, w_router, bias, region<float>(ws, p.wnorm),
+                                        region<float>(ws, p.wr32), region<uint16_t>(ws, p.cand),
                                         region<int32_t>(ws, p.ncand), ovf, ovf + 1, idx, gate, s),
               "router repair");
     return MOE_OK;

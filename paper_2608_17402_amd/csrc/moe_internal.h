@@ -96,12 +96,15 @@ struct GemmArgs {
     const float* gate;         // EPI_COMBINE: gates [rows, route_k]
     const void* eo;            // EPI_COMBINE: expert outputs [rows * route_k, N] in slot order
     float lambda;              // EPI_COMBINE: shared-expert weight
+    int32_t k_splits;          // tiled kernel, dense EPI_STORE_F32 only: K split into this many parts (0 or
+                               // 1 = none), part p writing its partial sums to C + p * dense_rows * N
 };
 
 // Offsets (bytes) of every workspace region for one descriptor.
 struct WorkspacePlan {
     size_t idx, gate, scores, counts, offsets, slots, blockhist, tiles, ntiles;
-    size_t wnorm, ovf, cand, ncand;
+    size_t wnorm, ovf, cand, ncand, wr32;
+    int32_t router_splits;   // split-K parts of the fast router's logits GEMM
     size_t act, eout, sact, sout;
     size_t total;
     int32_t n_hist_blocks;   // blocks of the permute histogram / scatter
@@ -158,10 +161,15 @@ hipError_t launch_topk(const moe_desc_t& d, const float* scores, const float* bi
 // rows of ld >= E floats.
 // cand [T][router_cand_slots(K)] and ncand [T] are scratch of the candidate
 // pass.
-hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, int ld, const void* x,
-                                     const void* w_router, const float* bias, float* wnorm,
+// The logits come in nsplit partial arrays of T x ld (split K), summed in
+// order. Small batches (router_small_batch) read the weights as fp32 from
+// wr32 [E, d], which the norm kernel writes; larger ones ignore it.
+hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, int ld, int nsplit, const void* x,
+                                     const void* w_router, const float* bias, float* wnorm, float* wr32,
                                      uint16_t* cand, int32_t* ncand, int32_t* ovf_count, int32_t* ovf_list,
                                      int32_t* topk_idx, float* topk_gate, hipStream_t s);
+// Whether the fast router takes the small-batch chain kernel (fp32 weight copy).
+bool router_small_batch(const moe_desc_t& d);
 int router_cand_slots(int K);
 // Grouping of slots by expert; with a tile table (tiles != nullptr) the scan
 // kernel also cuts the segments into M-tiles of bm rows (as launch_build_tiles).

@@ -13,6 +13,7 @@
 #include <math.h>
 
 #include <type_traits>
+#include <utility>
 
 namespace moe {
 namespace {
@@ -252,7 +253,7 @@ __device__ __forceinline__ float sigmoid_fast(float s) {
 __global__ __launch_bounds__(256) void k_row_norms(const bf16_t* __restrict__ a, int rows_a,
                                                    float* __restrict__ out_a, const bf16_t* __restrict__ b,
                                                    int rows_b, float* __restrict__ out_b, int d,
-                                                   int32_t* __restrict__ clear) {
+                                                   int32_t* __restrict__ clear, float* __restrict__ a32) {
     if (clear && blockIdx.x == 0 && threadIdx.x == 0) *clear = 0;
     const int lane = threadIdx.x & (kWave - 1);
     // One wave per row: the rows of a, then (from the next block on) those of b.
@@ -264,11 +265,18 @@ __global__ __launch_bounds__(256) void k_row_norms(const bf16_t* __restrict__ a,
     const bf16_t* p = (second ? b : a) + (size_t)row * d;
     float* out = second ? out_b : out_a;
     float acc = 0.0f;
+    // a32 (optional): the rows of a widened to fp32 (exact), for the
+    // small-batch chain kernel.
+    float* const r32 = (a32 && !second) ? a32 + (size_t)row * d : nullptr;
     for (int i = lane * 8; i < d; i += kWave * 8) {
         float v[8];
         load8(p + i, v);
 #pragma unroll
         for (int q = 0; q < 8; ++q) acc = fmaf(v[q], v[q], acc);
+        if (r32) {
+            *reinterpret_cast<float4*>(r32 + i) = make_float4(v[0], v[1], v[2], v[3]);
+            *reinterpret_cast<float4*>(r32 + i + 4) = make_float4(v[4], v[5], v[6], v[7]);
+        }
     }
 #pragma unroll
     for (int off = kWave / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
@@ -278,10 +286,22 @@ __global__ __launch_bounds__(256) void k_row_norms(const bf16_t* __restrict__ a,
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 // Candidates of each token: LPA lanes per token, lane g holding experts
-// g, g + LPA, ... (PER of them); the MFMA logits have rows of ld >= E. L = the K-th largest lower end of the key
+// g, g + LPA, ... (PER of them); the MFMA logits have rows of ld >= E, in
+// nsplit partial arrays (split K) sstride floats apart. L = the K-th largest lower end of the key
 // intervals; the candidates are the experts whose upper end reaches L, written
 // to cand[t][0 .. NS) with their count in ncand[t]. A token with more than NS
 // candidates gets ncand = -1 and is appended to the overflow queue.
+// Compile-time loop: f(std::integral_constant<int, i>) for i = 0 .. N-1.
+template <typename F, int... Is>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, Is...>) {
+    (f(std::integral_constant<int, Is>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+constexpr int kMaxSplit = 8;  // K-split parts of the logits GEMM, at most
 template <int LPA, int PER, int NS>
 __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s_fast,
                                                     const bf16_t* __restrict__ x, int d,
@@ -289,7 +309,7 @@ __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s
                                                     const float* __restrict__ bias, int T, int E, int ld,
                                                     int K, float cst, uint16_t* __restrict__ cand,
                                                     int32_t* __restrict__ ncand, int32_t* __restrict__ ovf_count,
-                                                    int32_t* __restrict__ ovf_list) {
+                                                    int32_t* __restrict__ ovf_list, int nsplit, size_t sstride) {
     static_assert(LPA <= kWave && kWave % LPA == 0, "token groups inside a wave");
     const int lane = threadIdx.x & (kWave - 1);
     const int g = lane % LPA;
@@ -322,7 +342,18 @@ __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s
         hi[m] = -INFINITY;
         if (live && e < E) {
             const float b = bias ? bias[e] : 0.0f;
-            const float key = sigmoid_fast(s_fast[(size_t)t * ld + e]) + b;
+            // Split-K logits: the partial sums in a fixed order (any order
+            // of the d products is covered by the bound). All parts' loads
+            // are issued before the adds.
+            float part[kMaxSplit];
+#pragma unroll
+            for (int q = 0; q < kMaxSplit; ++q)
+                part[q] = q < nsplit ? s_fast[q * sstride + (size_t)t * ld + e] : 0.0f;
+            float sf = part[0];
+#pragma unroll
+            for (int q = 1; q < kMaxSplit; ++q)
+                if (q < nsplit) sf += part[q];
+            const float key = sigmoid_fast(sf) + b;
             const float delta = 0.25f * (cst * xn * wnorm[e]) + 4e-6f + 1e-6f * fabsf(b);
             lo[m] = key - delta;
             hi[m] = key + delta;
@@ -614,99 +645,19 @@ __global__ __launch_bounds__(TPB* LPT) void k_router_chain(const bf16_t* __restr
     chain_select<TPB, LPT, CPL>(lds, tl, g, t, T, nc, K, on, ec, acc, bc, bias != nullptr, topk_idx, topk_gate);
 }
 
-// Exact logits for small batches, where streaming every expert's weights
-// through LDS per block of tokens costs more than the candidates need: one
-// 64-lane wave per TPB = 64 / LPT tokens, one candidate chain per lane (LPT =
-// the candidate slots). The block's x rows are staged in LDS; each lane reads
-// its candidate's router-weight row straight from global memory, in groups of
-// eight 16-byte loads (64 columns), the next group's loads issued before the
-// current group's 64 multiply-adds. The chain is the same fused multiply-add
-// sequence over i = 0..d-1, from +0, as in k_router_chain. Dynamic LDS:
-// max(TPB d bf16, the selection's arrays). d is a multiple of 64.
-template <int LPT>
-__global__ __launch_bounds__(kWave) void k_router_chain_direct(const bf16_t* __restrict__ x,
-                                                             const bf16_t* __restrict__ wr,
-                                                             const float* __restrict__ bias,
-                                                             const uint16_t* __restrict__ cand,
-                                                             const int32_t* __restrict__ ncand, int T, int d, int E,
-                                                             int K, int32_t* __restrict__ topk_idx,
-                                                             float* __restrict__ topk_gate) {
-    constexpr int TPB = kWave / LPT;
-    extern __shared__ __attribute__((aligned(16))) uint8_t lds_dyn[];
-    const int tid = threadIdx.x;
-    const int g = tid % LPT;
-    const int tl = tid / LPT;
-    const int t = blockIdx.x * TPB + tl;
-    int nc = t < T ? ncand[t] : 0;
-    nc = nc < 0 ? 0 : nc;  // queued tokens are routed by the exact-list kernel
-    const bool on[1] = {g < nc};
-    const int ec[1] = {on[0] ? (int)cand[(size_t)t * LPT + g] : 0};
-    const float bc[1] = {(bias && on[0]) ? bias[ec[0]] : 0.0f};
-    (void)E;
-
-    // x rows of the block's tokens (tokens past T copy row T - 1; their
-    // chains are off).
-    bf16_t* xs = reinterpret_cast<bf16_t*>(lds_dyn);
-    const bf16_t* xt = x + (size_t)(t < T ? t : T - 1) * d;
-    for (int i = g * 8; i < d; i += LPT * 8)
-        *reinterpret_cast<u32x4_t*>(xs + tl * d + i) = *reinterpret_cast<const u32x4_t*>(xt + i);
-    __syncthreads();
-
-    float acc[1] = {0.0f};
-    if (__ballot(on[0]) != 0) {
-        const bf16_t* we = wr + (size_t)ec[0] * d;
-        const bf16_t* xr = xs + tl * d;
-        const int ng = d / 64;
-        u32x4_t wa[8], wb[8];
-        auto load = [&](u32x4_t(&w)[8], int grp) {
-#pragma unroll
-            for (int u = 0; u < 8; ++u) w[u] = *reinterpret_cast<const u32x4_t*>(we + grp * 64 + 8 * u);
-        };
-        auto run = [&](const u32x4_t(&w)[8], int grp) {
-            float a = acc[0];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                const u32x4_t xv = *reinterpret_cast<const u32x4_t*>(xr + grp * 64 + 8 * u);
-                const u32x4_t wv = w[u];
-                a = fmaf(__uint_as_float(xv.x << 16), __uint_as_float(wv.x << 16), a);
-                a = fmaf(__uint_as_float(xv.x & 0xffff0000u), __uint_as_float(wv.x & 0xffff0000u), a);
-                a = fmaf(__uint_as_float(xv.y << 16), __uint_as_float(wv.y << 16), a);
-                a = fmaf(__uint_as_float(xv.y & 0xffff0000u), __uint_as_float(wv.y & 0xffff0000u), a);
-                a = fmaf(__uint_as_float(xv.z << 16), __uint_as_float(wv.z << 16), a);
-                a = fmaf(__uint_as_float(xv.z & 0xffff0000u), __uint_as_float(wv.z & 0xffff0000u), a);
-                a = fmaf(__uint_as_float(xv.w << 16), __uint_as_float(wv.w << 16), a);
-                a = fmaf(__uint_as_float(xv.w & 0xffff0000u), __uint_as_float(wv.w & 0xffff0000u), a);
-            }
-            acc[0] = a;
-        };
-        load(wa, 0);
-        for (int n = 0; n < ng; n += 2) {
-            if (n + 1 < ng) load(wb, n + 1);
-            run(wa, n);
-            if (n + 1 < ng) {
-                if (n + 2 < ng) load(wa, n + 2);
-                run(wb, n + 1);
-            }
-        }
-    }
-    __syncthreads();  // the selection reuses the x rows' LDS
-    chain_select<TPB, LPT, 1>(lds_dyn, tl, g, t, T, nc, K, on, ec, acc, bc, bias != nullptr, topk_idx, topk_gate);
-}
-
 // Exact routing of the queued tokens: all E logits by the FMA chain, then
-// the same top-K. Persistent blocks walk the queue; every block exits once
-// the queue (fixed by the time this kernel starts) is exhausted.
-__global__ __launch_bounds__(256) void k_router_exact_list(const bf16_t* __restrict__ x,
-                                                          const bf16_t* __restrict__ wr,
-                                                          const float* __restrict__ bias, int d, int E, int K,
-                                                          const int32_t* __restrict__ ovf_count,
-                                                          const int32_t* __restrict__ ovf_list,
-                                                          int32_t* __restrict__ topk_idx,
-                                                          float* __restrict__ topk_gate) {
+// the same top-K. Blocks first, first + stride, ... walk the queue (fixed by
+// the time this runs); every block exits once it is exhausted. Any block
+// size that is a multiple of the wave works (the selection uses wave 0).
+__device__ __forceinline__ void exact_list_run(const bf16_t* __restrict__ x, const bf16_t* __restrict__ wr,
+                               const float* __restrict__ bias, int d, int E, int K,
+                               const int32_t* __restrict__ ovf_count, const int32_t* __restrict__ ovf_list,
+                               int32_t* __restrict__ topk_idx, float* __restrict__ topk_gate, int first,
+                               int stride) {
     __shared__ float sig[kMaxE];
     const int n = *ovf_count;
     const int lane = threadIdx.x & (kWave - 1);
-    for (int it = blockIdx.x; it < n; it += gridDim.x) {
+    for (int it = first; it < n; it += stride) {
         const int t = ovf_list[it];
         const bf16_t* xt = x + (size_t)t * d;
         for (int e = threadIdx.x; e < E; e += blockDim.x) {
@@ -788,6 +739,123 @@ __global__ __launch_bounds__(256) void k_router_exact_list(const bf16_t* __restr
     }
 }
 
+
+__global__ __launch_bounds__(256) void k_router_exact_list(const bf16_t* __restrict__ x,
+                                                          const bf16_t* __restrict__ wr,
+                                                          const float* __restrict__ bias, int d, int E, int K,
+                                                          const int32_t* __restrict__ ovf_count,
+                                                          const int32_t* __restrict__ ovf_list,
+                                                          int32_t* __restrict__ topk_idx,
+                                                          float* __restrict__ topk_gate) {
+    exact_list_run(x, wr, bias, d, E, K, ovf_count, ovf_list, topk_idx, topk_gate, blockIdx.x, gridDim.x);
+}
+
+// Exact logits for small batches, where streaming every expert's weights
+// through LDS per block of tokens costs more than the candidates need: one
+// 64-lane wave per TPB = 64 / LPT tokens, one candidate chain per lane (LPT =
+// the candidate slots). The block's x rows are staged in LDS widened to fp32;
+// each lane reads its candidate's router-weight row, widened to fp32 by the
+// norm kernel (wr32), straight from global memory in groups of 32 columns,
+// two groups ahead of the multiply-adds. A multiply-add then costs one FMA
+// plus a quarter of an LDS and of a global read, against three VALU
+// operations with bf16 operands (both widenings); at a few waves per CU the
+// kernel is bound by each wave's issue and latency, not by bandwidth. The
+// chain is the same fused multiply-add sequence over i = 0..d-1, from +0, on
+// the same (exactly widened) values as in k_router_chain.
+//
+// Blocks from chain_blocks on route the tokens of the overflow queue instead
+// (exact_list_run), so that no separate launch is needed; the chain blocks
+// skip queued tokens and write nothing for them. Dynamic LDS: max(TPB d fp32,
+// the selection's arrays). d is a multiple of 64.
+template <int LPT>
+__global__ __launch_bounds__(kWave) void k_router_chain_direct(const bf16_t* __restrict__ x,
+                                                             const float* __restrict__ wr32,
+                                                             const bf16_t* __restrict__ wr,
+                                                             const float* __restrict__ bias,
+                                                             const uint16_t* __restrict__ cand,
+                                                             const int32_t* __restrict__ ncand, int T, int d, int E,
+                                                             int K, int32_t* __restrict__ topk_idx,
+                                                             float* __restrict__ topk_gate, int chain_blocks,
+                                                             const int32_t* __restrict__ ovf_count,
+                                                             const int32_t* __restrict__ ovf_list) {
+    if ((int)blockIdx.x >= chain_blocks) {
+        exact_list_run(x, wr, bias, d, E, K, ovf_count, ovf_list, topk_idx, topk_gate,
+                       (int)blockIdx.x - chain_blocks, (int)gridDim.x - chain_blocks);
+        return;
+    }
+    constexpr int TPB = kWave / LPT;
+    extern __shared__ __attribute__((aligned(16))) uint8_t lds_dyn[];
+    const int tid = threadIdx.x;
+    const int g = tid % LPT;
+    const int tl = tid / LPT;
+    const int t = blockIdx.x * TPB + tl;
+    int nc = t < T ? ncand[t] : 0;
+    nc = nc < 0 ? 0 : nc;  // queued tokens are routed by the queue blocks
+    const bool on[1] = {g < nc};
+    const int ec[1] = {on[0] ? (int)cand[(size_t)t * LPT + g] : 0};
+    const float bc[1] = {(bias && on[0]) ? bias[ec[0]] : 0.0f};
+
+    // x rows of the block's tokens, widened to fp32 (tokens past T copy row
+    // T - 1; their chains are off).
+    float* xs = reinterpret_cast<float*>(lds_dyn);
+    const bf16_t* xt = x + (size_t)(t < T ? t : T - 1) * d;
+    for (int i = g * 8; i < d; i += LPT * 8) {
+        const u32x4_t v = *reinterpret_cast<const u32x4_t*>(xt + i);
+        *reinterpret_cast<float4*>(xs + tl * d + i) =
+            make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u),
+                        __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xffff0000u));
+        *reinterpret_cast<float4*>(xs + tl * d + i + 4) =
+            make_float4(__uint_as_float(v.z << 16), __uint_as_float(v.z & 0xffff0000u),
+                        __uint_as_float(v.w << 16), __uint_as_float(v.w & 0xffff0000u));
+    }
+    __syncthreads();
+
+    float acc[1] = {0.0f};
+    if (__ballot(on[0]) != 0) {
+        const float* we = wr32 + (size_t)ec[0] * d;
+        const float* xr = xs + tl * d;
+        const int ng = d / 32;  // even, >= 2
+        // Ring of RB groups of 32 columns of weights in registers, RB - 1
+        // groups ahead of the multiply-adds, and the x values of the next
+        // group read from LDS while the current group's multiply-adds run: at
+        // a wave or two per SIMD nothing else hides either latency.
+        constexpr int RB = 4;
+        float4 w[RB][8], xv[2][8];
+        auto load = [&](int b, int grp) {
+#pragma unroll
+            for (int u = 0; u < 8; ++u) w[b][u] = *reinterpret_cast<const float4*>(we + grp * 32 + 4 * u);
+        };
+        auto read_x = [&](int b, int grp) {
+#pragma unroll
+            for (int u = 0; u < 8; ++u) xv[b][u] = *reinterpret_cast<const float4*>(xr + grp * 32 + 4 * u);
+        };
+        float a = 0.0f;
+#pragma unroll
+        for (int b = 0; b < RB - 1; ++b)
+            if (b < ng) load(b, b);
+        read_x(0, 0);
+        for (int n = 0; n < ng; n += RB) {
+            static_for<RB>([&](auto BC) {
+                constexpr int b = decltype(BC)::value;
+                if (n + b < ng) {
+                    if (n + b + RB - 1 < ng) load((b + RB - 1) % RB, n + b + RB - 1);
+                    if (n + b + 1 < ng) read_x((b + 1) & 1, n + b + 1);
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) {
+                        a = fmaf(xv[b & 1][u].x, w[b][u].x, a);
+                        a = fmaf(xv[b & 1][u].y, w[b][u].y, a);
+                        a = fmaf(xv[b & 1][u].z, w[b][u].z, a);
+                        a = fmaf(xv[b & 1][u].w, w[b][u].w, a);
+                    }
+                }
+            });
+        }
+        acc[0] = a;
+    }
+    __syncthreads();  // the selection reuses the x rows' LDS
+    chain_select<TPB, LPT, 1>(lds_dyn, tl, g, t, T, nc, K, on, ec, acc, bc, bias != nullptr, topk_idx, topk_gate);
+}
+
 }  // namespace
 
 hipError_t launch_router_scores(const moe_desc_t& d, const void* x, const void* w_router,
@@ -823,15 +891,20 @@ float router_fast_bound_constant(int d) {
     return (float)((gamma + 4.0 * d * u) * 1.01);
 }
 
-hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, int ld, const void* x,
-                                     const void* w_router, const float* bias, float* wnorm,
+bool router_small_batch(const moe_desc_t& d) { return d.T < 256 * 64; }
+
+hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, int ld, int nsplit, const void* x,
+                                     const void* w_router, const float* bias, float* wnorm, float* wr32,
                                      uint16_t* cand, int32_t* ncand, int32_t* ovf_count, int32_t* ovf_list,
                                      int32_t* topk_idx, float* topk_gate, hipStream_t s) {
     const bf16_t* xb = static_cast<const bf16_t*>(x);
     const bf16_t* wb = static_cast<const bf16_t*>(w_router);
-    // Weight-row norms (the token norms are formed in the candidate kernel).
+    const bool small = router_small_batch(d);
+    // Weight-row norms (the token norms are formed in the candidate kernel);
+    // for small batches also the fp32 copy of the weights the chains read.
     hipLaunchKernelGGL(k_row_norms, dim3((d.E + 3) / 4), dim3(256), 0, s, wb, d.E, wnorm, nullptr, 0, nullptr, d.d,
-                       ovf_count);
+                       ovf_count, small ? wr32 : nullptr);
+    const size_t sstride = (size_t)d.T * ld;
     const float cst = router_fast_bound_constant(d.d);
     const int ns = router_cand_slots(d.K);
     // Candidates: 16 lanes per token (64 for more than 256 experts); blocks
@@ -840,7 +913,8 @@ hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, i
 #define MOE_CAND(LPAv, PERv, NSv)                                                                           \
     hipLaunchKernelGGL((k_router_cand<LPAv, PERv, NSv>),                                                    \
                        dim3((d.T + cand_threads / LPAv - 1) / (cand_threads / LPAv)), dim3(cand_threads), 0, s, \
-                       s_fast, xb, d.d, wnorm, bias, d.T, d.E, ld, d.K, cst, cand, ncand, ovf_count, ovf_list)
+                       s_fast, xb, d.d, wnorm, bias, d.T, d.E, ld, d.K, cst, cand, ncand, ovf_count, ovf_list, \
+                       nsplit, sstride)
     if (d.E <= 64) { if (ns == 16) MOE_CAND(16, 4, 16); else MOE_CAND(16, 4, 32); }
     else if (d.E <= 256) { if (ns == 16) MOE_CAND(16, 16, 16); else MOE_CAND(16, 16, 32); }
     else { if (ns == 16) MOE_CAND(64, 16, 16); else MOE_CAND(64, 16, 32); }
@@ -863,18 +937,25 @@ hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, i
     } else if (d.T >= 256 * 64) {
         if (ns == 16) MOE_CHAIN_E(64, 4, 4, 64); else MOE_CHAIN_E(64, 8, 4, 64);
     } else {
-        // One wave per 64 / ns tokens, weights straight from global memory.
+        // One wave per 64 / ns tokens, fp32 weights straight from global
+        // memory; 64 more one-wave blocks route the overflow queue.
         const int tpb = kWave / ns;
         const size_t sel = (size_t)tpb * (ns * 12 + kMaxK * 8);
-        const size_t xs = (size_t)tpb * d.d * 2;
+        const size_t xs = (size_t)tpb * d.d * 4;
         const size_t shm = xs > sel ? xs : sel;
-        const dim3 grid((d.T + tpb - 1) / tpb);
-        if (ns == 16)
-            hipLaunchKernelGGL(k_router_chain_direct<16>, grid, dim3(kWave), shm, s, xb, wb, bias, cand, ncand, d.T,
-                               d.d, d.E, d.K, topk_idx, topk_gate);
-        else
-            hipLaunchKernelGGL(k_router_chain_direct<32>, grid, dim3(kWave), shm, s, xb, wb, bias, cand, ncand, d.T,
-                               d.d, d.E, d.K, topk_idx, topk_gate);
+        const int chain_blocks = (d.T + tpb - 1) / tpb;
+        const dim3 grid(chain_blocks + 64);
+        auto launch = [&](auto kern) -> hipError_t {
+            if (shm > 65536) {  // x rows of d > 4096 in LDS
+                const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
+                if (e != hipSuccess) return e;
+            }
+            hipLaunchKernelGGL(kern, grid, dim3(kWave), shm, s, xb, wr32, wb, bias, cand, ncand, d.T, d.d, d.E, d.K,
+                               topk_idx, topk_gate, chain_blocks, ovf_count, ovf_list);
+            return hipGetLastError();
+        };
+        return ns == 16 ? launch(k_router_chain_direct<16>) : launch(k_router_chain_direct<32>);
     }
 #undef MOE_CHAIN_E
 #undef MOE_CHAIN
