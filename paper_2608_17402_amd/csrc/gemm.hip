@@ -1569,7 +1569,7 @@ void k_gemm_pp(const GemmArgs a) {
                     // DSW: pieces 0..7 of the row are dG, 8..15 dU (act_ld further on).
                     const int pcol = DSW ? (lane & 7) * 8 : (lane & 15) * (16 / OES);
                     const int col = t.n0 + wn * WT + h * 64 + pcol;
-                    if (r < t.rows && (!WG || t.n0 + wn * WT + h * 64 < ncols) && (!DSW || col < a.act_ld)) {
+                    if (r < t.rows && t.n0 + wn * WT + h * 64 < ncols && (!DSW || col < a.act_ld)) {
                         size_t orw = SCATTER ? (size_t)orow[i][k] : (size_t)(t.row0 + r);
                         uint8_t* ob = cbase;
                         if (WG) {  // the expert's gradient, or the work item's partial block
@@ -1926,6 +1926,19 @@ hipError_t dispatch_bf16(int bm, const GemmArgs& a, hipStream_t s) {
             if (a.Kdim >= 128 && gather_ok) return launch_pp<EPI, GROUPED>(a, s);
             return launch_sp<EPI, GROUPED>(a, s);
         }
+        // The grouped layers with N an odd multiple of 128 (ViT-B's h = 384):
+        // N rounded up to the persistent kernel's 256-column tile, weight rows
+        // past N read as zeros and columns past N not stored. A third more
+        // MFMA work than the 256 x 128 tiles, but on the persistent kernel.
+        if constexpr (GROUPED && (EPI == EPI_GELU_STORE || EPI == EPI_SCATTER_SLOT))
+            if (a.N % 128 == 0 && a.Kdim >= 128 &&
+                (EPI == EPI_SCATTER_SLOT || a.row_mode == ROWS_GATHER_TOKENS)) {
+                GemmArgs p = a;
+                p.b_rows = a.N;
+                p.ldc = a.N;
+                p.N = (a.N + 255) / 256 * 256;
+                return launch_pp<EPI, GROUPED>(p, s);
+            }
         if (a.N % 128 == 0) return launch_bf16<256, 128, 2, 2, 64, 2, 1, EPI, GROUPED>(a, s);
         return launch_bf16<256, 64, 4, 1, 64, 2, 1, EPI, GROUPED>(a, s);
     }
