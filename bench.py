@@ -347,8 +347,9 @@ def main():
         torch) bf16 GEMMs of the same total shape, fc1 [T K, d] x [d, h] and
         fc2 [T K, h] x [h, d] as single dense products, and as a batch of E
         equal expert blocks of T K / E rows (torch.bmm with contiguous
-        operands); and the GB/s of a 1 GiB device copy, the context of the
-        HBM-bound stages. Random operands; weights in the [out, in] layout."""
+        operands); a square 8192^3 product (a long contraction); and the GB/s
+        of a 1 GiB device copy, the context of the HBM-bound stages. Random
+        operands; weights in the [out, in] layout."""
         M, d, h, E = c.T * c.K, c.d, c.h, c.E
         g = torch.Generator(device="cuda").manual_seed(3)
 
@@ -370,6 +371,12 @@ def main():
         t3 = time_calls(lambda: torch.bmm(b1, wb1), reps)
         t4 = time_calls(lambda: torch.bmm(b2, wb2), reps)
         del b1, b2, wb1, wb2
+        # A long contraction (8192^3): what the library reaches on this machine
+        # when the K loop is long against the tile's start-up and epilogue.
+        q, wq = rnd(8192, 8192), rnd(8192, 8192)
+        fq = 2.0 * 8192 ** 3
+        t5 = time_calls(lambda: torch.nn.functional.linear(q, wq), reps)
+        del q, wq
         # A plain device copy of 1 GiB: the HBM bandwidth a streaming kernel reaches here.
         ca = torch.empty(1 << 29, dtype=torch.bfloat16, device="cuda").fill_(1)
         cb = torch.empty_like(ca)
@@ -389,6 +396,8 @@ def main():
             "batched_fc2": {"shape": [E, m, h, d], "us": round(t4 * 1e3, 1), "tflops": tf(fb, t4)},
             "batched_pair_tflops": tf(2 * fb, t3 + t4),
             "routed_pair_over_dense_pair": round(routed_tflops / pair, 4),
+            "square_8192": {"shape": [8192, 8192, 8192], "us": round(t5 * 1e3, 1), "tflops": tf(fq, t5),
+                            "frac": round(tf(fq, t5) / PEAK_BF16_TFLOPS, 4)},
             "copy_gbs": round(2 * (1 << 30) / (tc * 1e-3) / 1e9, 1),
         }
         return res

@@ -9,14 +9,14 @@
  *   g'_e   = Sigmoid(s_e) / sum_{i in sel} Sigmoid(s_i)     for e in sel
  *   y      = sum_{e in sel} g'_e E_e(x) + lambda * E_shared(x)
  *   E(x)   = W2 GELU(W1 x)                           fc1 -> GELU -> fc2
- * GELU(v) = v Phi(v): fp32 layers evaluate the erf form with the device erff;
- * bf16 layers use v times the sigmoid of a clamped odd quintic in v, within
- * 2.6e-5 (absolute) of the erf form (see moe_grouped_mlp).
  * or, with MOE_FLAG_SWIGLU, SwiGLU experts (appendix "MoE Kernel",
  * Algorithm 1, Phase 2, and the SwiGLU MLPs of appendix "Implementation
  * Details"):
  *   E(x)   = W2 (SiLU(W1 x) * (W3 x)),  SiLU(v) = v / (1 + exp(-v))
- * The five stages (route, permute, grouped expert MLP, combine) are exposed
+ * GELU(v) = v Phi(v): fp32 layers evaluate the erf form with the device erff;
+ * bf16 layers use v times the sigmoid of a clamped odd quintic in v, within
+ * 2.6e-5 (absolute) of the erf form (see moe_grouped_mlp).
+ * The stages (route, permute, grouped expert MLP, combine) are exposed
  * separately and fused in moe_layer_forward.
  *
  * Conventions shared by every entry point

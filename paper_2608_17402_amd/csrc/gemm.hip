@@ -924,6 +924,9 @@ typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ void store16_asm(void* p, u32x4_t v) {
     asm volatile("global_store_dwordx4 %0, %1, off nt\n\ts_nop 0" ::"v"(p), "v"(v) : "memory");
 }
+__device__ __forceinline__ void store4_asm(void* p, uint32_t v) {
+    asm volatile("global_store_dword %0, %1, off" ::"v"(p), "v"(v) : "memory");
+}
 __device__ __forceinline__ void lds_write8_asm(uint32_t addr, u32x2_t v) {
     asm volatile("ds_write_b64 %0, %1" ::"v"(addr), "v"(v) : "memory");
 }
@@ -992,7 +995,8 @@ void k_gemm_pp(const GemmArgs a) {
     // output to the expert's gradient or a partial block.
     constexpr bool WG = EPI == EPI_WGRAD_F32;
     static_assert(!WG || GROUPED, "weight-gradient tiles come from the work-item table");
-    constexpr bool OUT_F32 = EPI == EPI_STORE_F32 || EPI == EPI_SCATTER_SLOT_F32 || WG;
+    constexpr bool RNORM = EPI == EPI_ROUTER_F32;  // EPI_STORE_F32 and the token rows' sums of squares
+    constexpr bool OUT_F32 = EPI == EPI_STORE_F32 || EPI == EPI_SCATTER_SLOT_F32 || WG || RNORM;
     constexpr bool COMBINE = EPI == EPI_COMBINE;
     constexpr bool STAGE_F32 = OUT_F32 || COMBINE;  // accumulators staged as fp32
     constexpr int OES = OUT_F32 ? 4 : 2;
@@ -1226,14 +1230,29 @@ void k_gemm_pp(const GemmArgs a) {
 #pragma unroll
         for (int j = 0; j < FB; ++j) tie(wf[cb][j]);
     };
+    // Router logits: per lane, the sums of squares of its four token rows'
+    // values in the token fragments (lanes l and l + 32 hold the two halves
+    // of each K step of row l % 32 of a 32-row block).
+    float xsq[FB];
+#pragma unroll
+    for (int i = 0; i < FB; ++i) xsq[i] = 0.0f;
+
     // One K step: 16 MFMAs on buffer CB, fragment q of the next K step after
     // MFMA q (q < 8), copy q / 4 of the step's four after MFMA q when q % 4 == 1.
+    // Router logits: after MFMA q, the squares of the two values in 32-bit
+    // word q % 4 of token fragment q / 4 (VALU work beside the MFMAs).
     auto kstep = [&](auto CBC, uint32_t rabase, uint32_t rwbase, int rks, auto&& copy) {
         constexpr int cb = decltype(CBC)::value;
         static_for<FB * FB>([&](auto QC) {
             constexpr int q = decltype(QC)::value;
             constexpr int j = q / FB, i = q % FB;
             acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[cb][j], xf[cb][i], acc[j][i], 0, 0, 0);
+            if constexpr (RNORM) {
+                const uint32_t u = __builtin_bit_cast(u32x4_t, xf[cb][q / 4])[q % 4];
+                const float lo = __uint_as_float(u << 16), hi = __uint_as_float(u & 0xffff0000u);
+                xsq[q / 4] = fmaf(lo, lo, xsq[q / 4]);
+                xsq[q / 4] = fmaf(hi, hi, xsq[q / 4]);
+            }
             if constexpr (q < 2 * FB)
                 read_frag(std::integral_constant<int, cb ^ 1>{}, QC, rabase, rwbase, rks);
             if constexpr (q % 4 == 1) copy(std::integral_constant<int, q / 4>{});
@@ -1726,6 +1745,19 @@ void k_gemm_pp(const GemmArgs a) {
         settle(std::integral_constant<int, 0>{});
         // Gathered rows of the tile after next: read now, used after the epilogue.
         if (GATHER && has_nn) load_tokens(tnn, tok);
+        // Router logits: the tile's token rows' sums of squares (the first
+        // column tile's waves of column block 0 write them), then zero for
+        // the next tile.
+        if constexpr (RNORM) {
+#pragma unroll
+            for (int i = 0; i < FB; ++i) {
+                const float v = xsq[i] + __shfl_xor(xsq[i], 32);
+                const int r = wm * WT + i * 32 + fr;
+                if (tc.n0 == 0 && wn == 0 && fk == 0 && r < tc.rows)
+                    store4_asm(static_cast<float*>(a.C2) + tc.row0 + r, __float_as_uint(v));
+                xsq[i] = 0.0f;
+            }
+        }
         // The last slab's token slot is free (and read by no wave any more).
         epilogue(tc, as == 0 ? AST - 1 : as - 1);
         // The combine's loads land in registers the next K loop reuses; a wait
@@ -2047,6 +2079,10 @@ hipError_t dispatch(const moe_desc_t& d, int epilogue, int bm, const GemmArgs& a
                 break;
             case EPI_STORE_F32:
                 if (!GROUPED) return dispatch_bf16<EPI_STORE_F32, false>(bm, a, s);
+                break;
+            case EPI_ROUTER_F32:
+                if (!GROUPED && bm == 256 && a.N % 256 == 0 && a.Kdim >= 128 && a.k_splits <= 1 && a.C2)
+                    return launch_pp<EPI_ROUTER_F32, false>(a, s);
                 break;
             case EPI_COMBINE:
                 if (!GROUPED && gemm_combine_fusable(d, bm, a.N, a.Kdim) && a.route_k == d.K)

@@ -164,6 +164,14 @@ static int32_t router_splits(const moe_desc_t& d) {
     return 1;
 }
 
+// Whether the router's logits GEMM also forms the tokens' sums of squares:
+// large batches whose logits run on the persistent kernel (256-row tiles, the
+// logit row a multiple of 256 wide, no K split). The candidate kernel then
+// reads T floats instead of x again (201 MB at ViT-G widths).
+static bool router_norms_in_gemm(const moe_desc_t& d) {
+    return fast_router(d) && router_bm(d) == 256 && router_ld(d) % 256 == 0 && d.d >= 128 && router_splits(d) == 1;
+}
+
 WorkspacePlan plan_workspace(const moe_desc_t& d) {
     WorkspacePlan p;
     const size_t es = elem_size(d.dtype);
@@ -186,6 +194,7 @@ WorkspacePlan plan_workspace(const moe_desc_t& d) {
     p.scores = take((size_t)p.router_splits * d.T * router_ld(d) * 4);
     p.wnorm = take((size_t)d.E * 4);
     p.wr32 = take(fast_router(d) && router_small_batch(d) ? (size_t)d.E * d.d * 4 : 0);
+    p.xnorm2 = take(router_norms_in_gemm(d) ? (size_t)d.T * 4 : 0);
     p.ovf = take((size_t)(d.T + 1) * 4);
     p.cand = take((size_t)d.T * router_cand_slots(d.K) * 2);
     p.ncand = take((size_t)d.T * 4);
@@ -263,9 +272,13 @@ static moe_status_t enqueue_route(const moe_desc_t& d, const WorkspacePlan& p, v
     g.max_tiles = (d.T + bm - 1) / bm;
     g.a_bytes = (uint32_t)((size_t)d.T * d.d * 2);
     g.k_splits = p.router_splits;
-    HIP_CHECK(launch_gemm(d, EPI_STORE_F32, bm, g, s), "router logits gemm");
+    const bool norms = router_norms_in_gemm(d);
+    float* xnorm2 = norms ? region<float>(ws, p.xnorm2) : nullptr;
+    g.C2 = xnorm2;
+    HIP_CHECK(launch_gemm(d, norms ? EPI_ROUTER_F32 : EPI_STORE_F32, bm, g, s), "router logits gemm");
     int32_t* ovf = region<int32_t>(ws, p.ovf);
-    HIP_CHECK(launch_router_fast_finish(d, scores, g.N, p.router_splits, x, w_router, bias, region<float>(ws, p.wnorm),
+    HIP_CHECK(launch_router_fast_finish(d, scores, g.N, p.router_splits, x, xnorm2, w_router, bias,
+                                        region<float>(ws, p.wnorm),
                                         region<float>(ws, p.wr32), region<uint16_t>(ws, p.cand),
                                         region<int32_t>(ws, p.ncand), ovf, ovf + 1, idx, gate, s),
               "router repair");

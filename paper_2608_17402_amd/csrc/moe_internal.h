@@ -60,6 +60,10 @@ enum GemmEpilogue : int {
     EPI_DSWIGLU = 10,       // dA = acc (N = act_ld columns); with G, U from aux [rows, 2 act_ld] (fp32):
                             // C[p, c] = bf16(dA U SiLU'(G)), C[p, act_ld + c] = bf16(dA SiLU(G)) for
                             // c < act_n, 0 for act_n <= c < act_ld
+    // Router logits (dense, persistent kernel only):
+    EPI_ROUTER_F32 = 11,    // EPI_STORE_F32, and C2[p] = sum over k of A[p, k]^2 (fp32, any order): the
+                            // token norms of the router's interval test, formed from the fragments the
+                            // K loop already holds
 };
 
 struct GemmArgs {
@@ -78,7 +82,8 @@ struct GemmArgs {
     int64_t b_group_stride;    // elements between consecutive experts' weights
     int32_t b_rows;            // dense bf16 only: rows of B that exist (0 = N); rows past them read as zeros
     uint32_t a_bytes;          // bytes of the A operand buffer (bounds of its buffer resource)
-    void* C2;                  // EPI_GELU_BWD: second output (fp32); EPI_WGRAD_F32: partial blocks
+    void* C2;                  // EPI_GELU_BWD: second output (fp32); EPI_WGRAD_F32: partial blocks;
+                               // EPI_ROUTER_F32: the rows' sums of squares [dense_rows] (fp32)
     // Backward, persistent kernel: the bf16 output (the activation, or dH) also
     // written transposed into the weight-gradient K windows, slab-major
     // [windows / 64][ct_cols][64]: sorted position p of expert e goes to window
@@ -103,7 +108,7 @@ struct GemmArgs {
 // Offsets (bytes) of every workspace region for one descriptor.
 struct WorkspacePlan {
     size_t idx, gate, scores, counts, offsets, slots, blockhist, tiles, ntiles;
-    size_t wnorm, ovf, cand, ncand, wr32;
+    size_t wnorm, ovf, cand, ncand, wr32, xnorm2;
     int32_t router_splits;   // split-K parts of the fast router's logits GEMM
     size_t act, eout, sact, sout;
     size_t total;
@@ -163,9 +168,12 @@ hipError_t launch_topk(const moe_desc_t& d, const float* scores, const float* bi
 // pass.
 // The logits come in nsplit partial arrays of T x ld (split K), summed in
 // order. Small batches (router_small_batch) read the weights as fp32 from
-// wr32 [E, d], which the norm kernel writes; larger ones ignore it.
+// wr32 [E, d], which the norm kernel writes; larger ones ignore it. xnorm2
+// [T]: the tokens' sums of squares if the logits GEMM formed them
+// (EPI_ROUTER_F32), else nullptr and the candidate kernel reads x for them.
 hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, int ld, int nsplit, const void* x,
-                                     const void* w_router, const float* bias, float* wnorm, float* wr32,
+                                     const float* xnorm2, const void* w_router, const float* bias, float* wnorm,
+                                     float* wr32,
                                      uint16_t* cand, int32_t* ncand, int32_t* ovf_count, int32_t* ovf_list,
                                      int32_t* topk_idx, float* topk_gate, hipStream_t s);
 // Whether the fast router takes the small-batch chain kernel (fp32 weight copy).

@@ -304,7 +304,8 @@ __device__ __forceinline__ void static_for(F&& f) {
 constexpr int kMaxSplit = 8;  // K-split parts of the logits GEMM, at most
 template <int LPA, int PER, int NS>
 __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s_fast,
-                                                    const bf16_t* __restrict__ x, int d,
+                                                    const bf16_t* __restrict__ x,
+                                                    const float* __restrict__ xnorm2, int d,
                                                     const float* __restrict__ wnorm,
                                                     const float* __restrict__ bias, int T, int E, int ld,
                                                     int K, float cst, uint16_t* __restrict__ cand,
@@ -319,20 +320,27 @@ __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s
     const uint64_t below = grp & ((1ull << lane) - 1ull);
 
     // ||x_t||, raised by 0.1 % as k_row_norms does for the weight rows (an
-    // upper bound is all the interval needs): the token's LPA lanes read its
-    // row in 16-byte pieces and add their partial sums.
+    // upper bound is all the interval needs; the rounding of the sum of
+    // squares, in any order, is far inside that margin). The sum of squares
+    // comes from the logits GEMM (xnorm2) or, without it, from the token's
+    // LPA lanes reading its row in 16-byte pieces and adding their partial
+    // sums.
     float ss = 0.0f;
-    if (live) {
-        const bf16_t* xr = x + (size_t)t * d;
-        for (int i = g * 8; i < d; i += LPA * 8) {
-            float v[8];
-            load8(xr + i, v);
+    if (xnorm2) {
+        ss = live ? xnorm2[t] : 0.0f;
+    } else {
+        if (live) {
+            const bf16_t* xr = x + (size_t)t * d;
+            for (int i = g * 8; i < d; i += LPA * 8) {
+                float v[8];
+                load8(xr + i, v);
 #pragma unroll
-            for (int q = 0; q < 8; ++q) ss = fmaf(v[q], v[q], ss);
+                for (int q = 0; q < 8; ++q) ss = fmaf(v[q], v[q], ss);
+            }
         }
-    }
 #pragma unroll
-    for (int off = LPA / 2; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+        for (int off = LPA / 2; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+    }
     const float xn = live ? sqrtf(ss) * 1.001f + 1e-30f : 0.0f;
     float lo[PER], hi[PER];
 #pragma unroll
@@ -894,7 +902,8 @@ float router_fast_bound_constant(int d) {
 bool router_small_batch(const moe_desc_t& d) { return d.T < 256 * 64; }
 
 hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, int ld, int nsplit, const void* x,
-                                     const void* w_router, const float* bias, float* wnorm, float* wr32,
+                                     const float* xnorm2, const void* w_router, const float* bias, float* wnorm,
+                                     float* wr32,
                                      uint16_t* cand, int32_t* ncand, int32_t* ovf_count, int32_t* ovf_list,
                                      int32_t* topk_idx, float* topk_gate, hipStream_t s) {
     const bf16_t* xb = static_cast<const bf16_t*>(x);
@@ -913,8 +922,8 @@ hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, i
 #define MOE_CAND(LPAv, PERv, NSv)                                                                           \
     hipLaunchKernelGGL((k_router_cand<LPAv, PERv, NSv>),                                                    \
                        dim3((d.T + cand_threads / LPAv - 1) / (cand_threads / LPAv)), dim3(cand_threads), 0, s, \
-                       s_fast, xb, d.d, wnorm, bias, d.T, d.E, ld, d.K, cst, cand, ncand, ovf_count, ovf_list, \
-                       nsplit, sstride)
+                       s_fast, xb, xnorm2, d.d, wnorm, bias, d.T, d.E, ld, d.K, cst, cand, ncand, ovf_count,    \
+                       ovf_list, nsplit, sstride)
     if (d.E <= 64) { if (ns == 16) MOE_CAND(16, 4, 16); else MOE_CAND(16, 4, 32); }
     else if (d.E <= 256) { if (ns == 16) MOE_CAND(16, 16, 16); else MOE_CAND(16, 16, 32); }
     else { if (ns == 16) MOE_CAND(64, 16, 16); else MOE_CAND(64, 16, 32); }

@@ -462,6 +462,32 @@ def test_route_near_ties_block_kernels(T, dup):
     assert np.array_equal(host(idx), ref_idx) and np.array_equal(host(gate), ref_gate)
 
 
+@pytest.mark.parametrize("dup", [1, 16, 128])
+def test_route_norms_from_logits_gemm(dup):
+    """256 experts at a token count (51 200 + 77) whose router logits run on
+    256-row tiles of the persistent kernel, which also forms the token norms
+    of the interval test; a partial last tile; token rows of very different
+    norms; exact ties in groups of `dup` router rows (dup = 1: none), with a
+    selection bias. Every token's indices and gates equal the oracle's."""
+    from workloads import bf16_bits_to_f32, f32_to_bf16_bits
+
+    T, d, E, K = 51200 + 77, 128, 256, 8
+    rng = np.random.default_rng(7 + dup)
+    scale = np.exp(rng.uniform(-3.0, 1.5, (T, 1))).astype(np.float32)
+    x = f32_to_bf16_bits(rng.standard_normal((T, d)).astype(np.float32) * scale)
+    base = f32_to_bf16_bits((rng.standard_normal((E // dup, d)) * 0.05).astype(np.float32))
+    wr = np.repeat(base, dup, axis=0)
+    bias = rng.uniform(-0.02, 0.02, E).astype(np.float32)
+    desc = binding.make_desc(T, d, E, K, 64)
+    ws = binding.alloc_workspace(desc)
+    idx = torch.empty(T, K, dtype=torch.int32, device="cuda")
+    gate = torch.empty(T, K, dtype=torch.float32, device="cuda")
+    binding.moe_route(desc, dev(x), dev(wr), dev(bias), idx, gate, ws)
+    torch.cuda.synchronize()
+    ref_idx, ref_gate = oracle.route(bf16_bits_to_f32(x), bf16_bits_to_f32(wr), bias, K)
+    assert np.array_equal(host(idx), ref_idx) and np.array_equal(host(gate), ref_gate)
+
+
 @pytest.mark.parametrize("E", [1, 3, 8, 64, 256, 1024])
 def test_bias_update_bit_exact(E):
     """Loss-free balancing update (Eqs. (8)-(9)) through the C ABI against the
