@@ -286,11 +286,13 @@ __global__ __launch_bounds__(256) void k_row_norms(const bf16_t* __restrict__ a,
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 // Candidates of each token: LPA lanes per token, lane g holding experts
-// g, g + LPA, ... (PER of them); the MFMA logits have rows of ld >= E, in
-// nsplit partial arrays (split K) sstride floats apart. L = the K-th largest lower end of the key
-// intervals; the candidates are the experts whose upper end reaches L, written
-// to cand[t][0 .. NS) with their count in ncand[t]. A token with more than NS
-// candidates gets ncand = -1 and is appended to the overflow queue.
+// g PER .. g PER + PER - 1 (contiguous, so that its logits are PER / 4
+// 16-byte loads); the MFMA logits have rows of ld >= E (a multiple of 64), in
+// nsplit partial arrays (split K) sstride floats apart. L = the K-th largest
+// lower end of the key intervals; the candidates are the experts whose upper
+// end reaches L, written to cand[t][0 .. NS) (in no particular order) with
+// their count in ncand[t]. A token with more than NS candidates gets
+// ncand = -1 and is appended to the overflow queue.
 // Compile-time loop: f(std::integral_constant<int, i>) for i = 0 .. N-1.
 template <typename F, int... Is>
 __device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, Is...>) {
@@ -301,7 +303,46 @@ __device__ __forceinline__ void static_for(F&& f) {
     static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
-constexpr int kMaxSplit = 8;  // K-split parts of the logits GEMM, at most
+
+// Maximum over each aligned group of 16 lanes (a DPP row), in every lane of
+// the group: swaps inside quads (xor 1, xor 2), then the mirror inside each
+// half row and the mirror of the whole row.
+template <int CTRL>
+__device__ __forceinline__ float dpp_max(float a) {
+    return fmaxf(a, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(a), CTRL, 0xF, 0xF, false)));
+}
+__device__ __forceinline__ float row16_max(float v) {
+    v = dpp_max<0xB1>(v);   // quad_perm [1, 0, 3, 2]
+    v = dpp_max<0x4E>(v);   // quad_perm [2, 3, 0, 1]
+    v = dpp_max<0x141>(v);  // row_half_mirror
+    v = dpp_max<0x140>(v);  // row_mirror
+    return v;
+}
+
+// Maximum over each aligned group of LPA lanes (16 or 64).
+template <int LPA>
+__device__ __forceinline__ float group_max(float v) {
+    static_assert(LPA == 16 || LPA == 64, "groups of 16 or 64 lanes");
+    v = row16_max(v);
+    if constexpr (LPA == 64) {
+        v = fmaxf(v, __shfl_xor(v, 16));
+        v = fmaxf(v, __shfl_xor(v, 32));
+    }
+    return v;
+}
+
+// PER consecutive floats from a 16-byte aligned address.
+template <int PER>
+__device__ __forceinline__ void load_row(const float* p, float (&v)[PER]) {
+#pragma unroll
+    for (int i = 0; i < PER / 4; ++i) {
+        const float4 q = *reinterpret_cast<const float4*>(p + 4 * i);
+        v[4 * i] = q.x;
+        v[4 * i + 1] = q.y;
+        v[4 * i + 2] = q.z;
+        v[4 * i + 3] = q.w;
+    }
+}
 template <int LPA, int PER, int NS>
 __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s_fast,
                                                     const bf16_t* __restrict__ x,
@@ -312,12 +353,20 @@ __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s
                                                     int32_t* __restrict__ ncand, int32_t* __restrict__ ovf_count,
                                                     int32_t* __restrict__ ovf_list, int nsplit, size_t sstride) {
     static_assert(LPA <= kWave && kWave % LPA == 0, "token groups inside a wave");
+    static_assert(PER % 4 == 0 && 64 % PER == 0, "whole 16-byte loads inside a row of a multiple of 64");
     const int lane = threadIdx.x & (kWave - 1);
     const int g = lane % LPA;
     const int t = blockIdx.x * (blockDim.x / LPA) + threadIdx.x / LPA;
     const bool live = t < T;  // uniform within the group: dead groups compute on -inf
     const uint64_t grp = (LPA == kWave ? ~0ull : ((1ull << LPA) - 1ull)) << (lane - g);
     const uint64_t below = grp & ((1ull << lane) - 1ull);
+
+    // Selection biases and weight-row norms of all experts, in LDS.
+    __shared__ float sb[kMaxE], swn[kMaxE];
+    for (int e = threadIdx.x; e < E; e += blockDim.x) {
+        sb[e] = bias ? bias[e] : 0.0f;
+        swn[e] = wnorm[e];
+    }
 
     // ||x_t||, raised by 0.1 % as k_row_norms does for the weight rows (an
     // upper bound is all the interval needs; the rounding of the sum of
@@ -342,27 +391,34 @@ __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s
         for (int off = LPA / 2; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
     }
     const float xn = live ? sqrtf(ss) * 1.001f + 1e-30f : 0.0f;
+
+    // Fast logits of the lane's experts. Split-K logits: the partial sums in
+    // part order (any order of the d products is covered by the bound).
+    const int e0 = g * PER;
+    float sf[PER];
+#pragma unroll
+    for (int m = 0; m < PER; ++m) sf[m] = 0.0f;
+    if (live && e0 < ld) {
+        const float* row = s_fast + (size_t)t * ld + e0;
+        load_row<PER>(row, sf);
+        for (int q = 1; q < nsplit; ++q) {
+            float pv[PER];
+            load_row<PER>(row + q * sstride, pv);
+#pragma unroll
+            for (int m = 0; m < PER; ++m) sf[m] += pv[m];
+        }
+    }
+    __syncthreads();
     float lo[PER], hi[PER];
 #pragma unroll
     for (int m = 0; m < PER; ++m) {
-        const int e = g + LPA * m;
+        const int e = e0 + m;
         lo[m] = -INFINITY;
         hi[m] = -INFINITY;
         if (live && e < E) {
-            const float b = bias ? bias[e] : 0.0f;
-            // Split-K logits: the partial sums in a fixed order (any order
-            // of the d products is covered by the bound). All parts' loads
-            // are issued before the adds.
-            float part[kMaxSplit];
-#pragma unroll
-            for (int q = 0; q < kMaxSplit; ++q)
-                part[q] = q < nsplit ? s_fast[q * sstride + (size_t)t * ld + e] : 0.0f;
-            float sf = part[0];
-#pragma unroll
-            for (int q = 1; q < kMaxSplit; ++q)
-                if (q < nsplit) sf += part[q];
-            const float key = sigmoid_fast(sf) + b;
-            const float delta = 0.25f * (cst * xn * wnorm[e]) + 4e-6f + 1e-6f * fabsf(b);
+            const float b = sb[e];
+            const float key = sigmoid_fast(sf[m]) + b;
+            const float delta = 0.25f * (cst * xn * swn[e]) + 4e-6f + 1e-6f * fabsf(b);
             lo[m] = key - delta;
             hi[m] = key + delta;
         }
@@ -382,9 +438,7 @@ __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s
     int used = 0;  // 0: t1 and t2 available, 1: t2 available, 2: none
     for (int j = 0; j < K; ++j) {
         const float mine = used == 0 ? t1 : (used == 1 ? t2 : -INFINITY);
-        float gmax = mine;
-#pragma unroll
-        for (int off = LPA / 2; off > 0; off >>= 1) gmax = fmaxf(gmax, __shfl_xor(gmax, off));
+        const float gmax = group_max<LPA>(mine);
         const uint64_t holders = __ballot(used < 2 && mine == gmax) & grp;
         if (holders && lane == __ffsll((unsigned long long)holders) - 1) ++used;
         L = gmax;
@@ -396,7 +450,7 @@ __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s
         const uint64_t bal = __ballot(c) & grp;
         if (c) {
             const int pos = nc + __popcll(bal & below);
-            if (pos < NS) cand[(size_t)t * NS + pos] = (uint16_t)(g + LPA * m);
+            if (pos < NS) cand[(size_t)t * NS + pos] = (uint16_t)(e0 + m);
         }
         nc += __popcll(bal);
     }
