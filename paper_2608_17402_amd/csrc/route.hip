@@ -343,7 +343,7 @@ __device__ __forceinline__ void load_row(const float* p, float (&v)[PER]) {
         v[4 * i + 3] = q.w;
     }
 }
-template <int LPA, int PER, int NS>
+template <int LPA, int PER, int NS, bool SPLIT>
 __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s_fast,
                                                     const bf16_t* __restrict__ x,
                                                     const float* __restrict__ xnorm2, int d,
@@ -379,12 +379,18 @@ __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s
         ss = live ? xnorm2[t] : 0.0f;
     } else {
         if (live) {
+            // Four pieces per round, all loaded before the adds.
             const bf16_t* xr = x + (size_t)t * d;
-            for (int i = g * 8; i < d; i += LPA * 8) {
-                float v[8];
-                load8(xr + i, v);
+            for (int i = g * 8; i < d; i += 4 * LPA * 8) {
+                float v[4][8];
 #pragma unroll
-                for (int q = 0; q < 8; ++q) ss = fmaf(v[q], v[q], ss);
+                for (int u = 0; u < 4; ++u)
+                    if (i + u * LPA * 8 < d) load8(xr + i + u * LPA * 8, v[u]);
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    if (i + u * LPA * 8 < d)
+#pragma unroll
+                        for (int q = 0; q < 8; ++q) ss = fmaf(v[u][q], v[u][q], ss);
             }
         }
 #pragma unroll
@@ -392,20 +398,28 @@ __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s
     }
     const float xn = live ? sqrtf(ss) * 1.001f + 1e-30f : 0.0f;
 
-    // Fast logits of the lane's experts. Split-K logits: the partial sums in
-    // part order (any order of the d products is covered by the bound).
+    // Fast logits of the lane's experts. Split-K logits (SPLIT, up to 8
+    // parts): the partial sums in part order (any order of the d products is
+    // covered by the bound), with every part's loads issued before the first
+    // add (parts past nsplit re-read part 0 and are not added).
     const int e0 = g * PER;
     float sf[PER];
 #pragma unroll
     for (int m = 0; m < PER; ++m) sf[m] = 0.0f;
     if (live && e0 < ld) {
         const float* row = s_fast + (size_t)t * ld + e0;
-        load_row<PER>(row, sf);
-        for (int q = 1; q < nsplit; ++q) {
-            float pv[PER];
-            load_row<PER>(row + q * sstride, pv);
+        if constexpr (SPLIT) {
+            float pv[8][PER];
 #pragma unroll
-            for (int m = 0; m < PER; ++m) sf[m] += pv[m];
+            for (int q = 0; q < 8; ++q) load_row<PER>(row + (q < nsplit ? q * sstride : 0), pv[q]);
+#pragma unroll
+            for (int m = 0; m < PER; ++m) sf[m] = pv[0][m];
+#pragma unroll
+            for (int q = 1; q < 8; ++q)
+#pragma unroll
+                for (int m = 0; m < PER; ++m) sf[m] = q < nsplit ? sf[m] + pv[q][m] : sf[m];
+        } else {
+            load_row<PER>(row, sf);
         }
     }
     __syncthreads();
@@ -860,15 +874,25 @@ __global__ __launch_bounds__(kWave) void k_router_chain_direct(const bf16_t* __r
     // x rows of the block's tokens, widened to fp32 (tokens past T copy row
     // T - 1; their chains are off).
     float* xs = reinterpret_cast<float*>(lds_dyn);
+    // Four 16-byte pieces per lane and round, all loaded before the writes.
     const bf16_t* xt = x + (size_t)(t < T ? t : T - 1) * d;
-    for (int i = g * 8; i < d; i += LPT * 8) {
-        const u32x4_t v = *reinterpret_cast<const u32x4_t*>(xt + i);
-        *reinterpret_cast<float4*>(xs + tl * d + i) =
-            make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u),
-                        __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xffff0000u));
-        *reinterpret_cast<float4*>(xs + tl * d + i + 4) =
-            make_float4(__uint_as_float(v.z << 16), __uint_as_float(v.z & 0xffff0000u),
-                        __uint_as_float(v.w << 16), __uint_as_float(v.w & 0xffff0000u));
+    for (int i0 = g * 8; i0 < d; i0 += 4 * LPT * 8) {
+        u32x4_t v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (i0 + u * LPT * 8 < d) v[u] = *reinterpret_cast<const u32x4_t*>(xt + i0 + u * LPT * 8);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int i = i0 + u * LPT * 8;
+            if (i < d) {
+                *reinterpret_cast<float4*>(xs + tl * d + i) =
+                    make_float4(__uint_as_float(v[u].x << 16), __uint_as_float(v[u].x & 0xffff0000u),
+                                __uint_as_float(v[u].y << 16), __uint_as_float(v[u].y & 0xffff0000u));
+                *reinterpret_cast<float4*>(xs + tl * d + i + 4) =
+                    make_float4(__uint_as_float(v[u].z << 16), __uint_as_float(v[u].z & 0xffff0000u),
+                                __uint_as_float(v[u].w << 16), __uint_as_float(v[u].w & 0xffff0000u));
+            }
+        }
     }
     __syncthreads();
 
@@ -967,6 +991,7 @@ hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, i
     // for small batches also the fp32 copy of the weights the chains read.
     hipLaunchKernelGGL(k_row_norms, dim3((d.E + 3) / 4), dim3(256), 0, s, wb, d.E, wnorm, nullptr, 0, nullptr, d.d,
                        ovf_count, small ? wr32 : nullptr);
+    if (nsplit < 1 || nsplit > 8) return hipErrorInvalidValue;  // the candidate kernel adds at most 8 parts
     const size_t sstride = (size_t)d.T * ld;
     const float cst = router_fast_bound_constant(d.d);
     const int ns = router_cand_slots(d.K);
@@ -974,7 +999,7 @@ hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, i
     // of one wave for small batches, so that every CU gets work.
     const int cand_threads = d.T >= 16384 ? 256 : kWave;
 #define MOE_CAND(LPAv, PERv, NSv)                                                                           \
-    hipLaunchKernelGGL((k_router_cand<LPAv, PERv, NSv>),                                                    \
+    hipLaunchKernelGGL((nsplit > 1 ? k_router_cand<LPAv, PERv, NSv, true> : k_router_cand<LPAv, PERv, NSv, false>), \
                        dim3((d.T + cand_threads / LPAv - 1) / (cand_threads / LPAv)), dim3(cand_threads), 0, s, \
                        s_fast, xb, xnorm2, d.d, wnorm, bias, d.T, d.E, ld, d.K, cst, cand, ncand, ovf_count,    \
                        ovf_list, nsplit, sstride)
