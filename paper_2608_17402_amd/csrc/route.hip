@@ -437,23 +437,24 @@ __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s
             hi[m] = key + delta;
         }
     }
-    // L: the K-th largest of the lanes' two largest lower ends. These are a
+    // L: the K-th largest of the lanes' three largest lower ends. These are a
     // subset of all lower ends, so L is at most the K-th largest lower end and
     // still a lower bound of the true K-th key; it equals it unless one lane
-    // holds three or more of the K largest.
-    float t1 = -INFINITY, t2 = -INFINITY;
+    // holds four or more of the K largest.
+    float t1 = -INFINITY, t2 = -INFINITY, t3 = -INFINITY;
 #pragma unroll
     for (int m = 0; m < PER; ++m) {
         const float v = lo[m];
+        t3 = fmaxf(t3, fminf(t2, v));
         t2 = fmaxf(t2, fminf(t1, v));
         t1 = fmaxf(t1, v);
     }
     float L = -INFINITY;
-    int used = 0;  // 0: t1 and t2 available, 1: t2 available, 2: none
+    int used = 0;  // how many of t1, t2, t3 (in that order) have been taken
     for (int j = 0; j < K; ++j) {
-        const float mine = used == 0 ? t1 : (used == 1 ? t2 : -INFINITY);
+        const float mine = used == 0 ? t1 : (used == 1 ? t2 : (used == 2 ? t3 : -INFINITY));
         const float gmax = group_max<LPA>(mine);
-        const uint64_t holders = __ballot(used < 2 && mine == gmax) & grp;
+        const uint64_t holders = __ballot(used < 3 && mine == gmax) & grp;
         if (holders && lane == __ffsll((unsigned long long)holders) - 1) ++used;
         L = gmax;
     }
@@ -738,13 +739,20 @@ __device__ __forceinline__ void exact_list_run(const bf16_t* __restrict__ x, con
         const bf16_t* xt = x + (size_t)t * d;
         for (int e = threadIdx.x; e < E; e += blockDim.x) {
             const bf16_t* we = wr + (size_t)e * d;
+            // The same fma sequence over i = 0..d-1; the loads of 32 columns
+            // are issued before their multiply-adds (d is a multiple of 64).
             float a = 0.0f;
-            for (int i = 0; i < d; i += 8) {
-                float xv[8], wv[8];
-                load8(xt + i, xv);
-                load8(we + i, wv);
+            for (int i = 0; i < d; i += 32) {
+                float xv[4][8], wv[4][8];
 #pragma unroll
-                for (int u = 0; u < 8; ++u) a = fmaf(xv[u], wv[u], a);
+                for (int q = 0; q < 4; ++q) {
+                    load8(xt + i + 8 * q, xv[q]);
+                    load8(we + i + 8 * q, wv[q]);
+                }
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) a = fmaf(xv[q][u], wv[q][u], a);
             }
             sig[e] = sigmoid_fp32(a);
         }
@@ -1003,8 +1011,12 @@ hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, i
                        dim3((d.T + cand_threads / LPAv - 1) / (cand_threads / LPAv)), dim3(cand_threads), 0, s, \
                        s_fast, xb, xnorm2, d.d, wnorm, bias, d.T, d.E, ld, d.K, cst, cand, ncand, ovf_count,    \
                        ovf_list, nsplit, sstride)
+    // E / LPA experts per lane (at least 4), so that every lane of a token
+    // holds experts and L is taken over all of them.
     if (d.E <= 64) { if (ns == 16) MOE_CAND(16, 4, 16); else MOE_CAND(16, 4, 32); }
+    else if (d.E <= 128) { if (ns == 16) MOE_CAND(16, 8, 16); else MOE_CAND(16, 8, 32); }
     else if (d.E <= 256) { if (ns == 16) MOE_CAND(16, 16, 16); else MOE_CAND(16, 16, 32); }
+    else if (d.E <= 512) { if (ns == 16) MOE_CAND(64, 8, 16); else MOE_CAND(64, 8, 32); }
     else { if (ns == 16) MOE_CAND(64, 16, 16); else MOE_CAND(64, 16, 32); }
 #undef MOE_CAND
     // Exact chains: 256 (or 128) tokens per block of 1024 threads while that

@@ -90,7 +90,8 @@ def test_route_near_ties_take_exact_fallback(dup):
         assert np.all(ref_idx == np.arange(K)[None, :])
 
 
-@pytest.mark.parametrize("E,K", [(1, 1), (5, 3), (31, 7), (63, 8), (65, 8), (100, 16), (200, 4)])
+@pytest.mark.parametrize("E,K", [(1, 1), (5, 3), (31, 7), (63, 8), (65, 8), (100, 16), (128, 8), (200, 4),
+                                 (300, 8), (1000, 12)])
 def test_route_fast_path_any_expert_count(E, K):
     # The MFMA pre-pass pads the logits to a multiple of 64 columns; routing
     # must still equal the oracle's and the all-exact path's, bit for bit.
