@@ -164,12 +164,19 @@ static int32_t router_splits(const moe_desc_t& d) {
     return 1;
 }
 
-// Whether the router's logits GEMM also forms the tokens' sums of squares:
-// large batches whose logits run on the persistent kernel (256-row tiles, the
-// logit row a multiple of 256 wide, no K split). The candidate kernel then
-// reads T floats instead of x again (201 MB at ViT-G widths).
+// Width of the router logits GEMM on the persistent kernel: the logit row
+// rounded up to its 256-column tile.
+static int32_t router_n256(const moe_desc_t& d) { return (router_ld(d) + 255) / 256 * 256; }
+
+// Whether the router's logits GEMM runs on the persistent kernel and also
+// forms the tokens' sums of squares: large batches (the 256-row tiles of at
+// least 128 logit columns, rounded up to 256, give every CU a tile), no K
+// split. The candidate kernel then reads T floats instead of x again (201 MB
+// at ViT-G widths, 134 MB at ViT-L's). Rounding 128 columns up to 256 doubles
+// that small GEMM's MFMA work, which costs less than the second read of x.
 static bool router_norms_in_gemm(const moe_desc_t& d) {
-    return fast_router(d) && router_bm(d) == 256 && router_ld(d) % 256 == 0 && d.d >= 128 && router_splits(d) == 1;
+    return fast_router(d) && router_ld(d) >= 128 && (int64_t)d.T * router_n256(d) >= (int64_t)200 * 65536 &&
+           d.d >= 128 && router_splits(d) == 1;
 }
 
 WorkspacePlan plan_workspace(const moe_desc_t& d) {
@@ -274,10 +281,15 @@ static moe_status_t enqueue_route(const moe_desc_t& d, const WorkspacePlan& p, v
     g.k_splits = p.router_splits;
     const bool norms = router_norms_in_gemm(d);
     float* xnorm2 = norms ? region<float>(ws, p.xnorm2) : nullptr;
-    g.C2 = xnorm2;
-    HIP_CHECK(launch_gemm(d, norms ? EPI_ROUTER_F32 : EPI_STORE_F32, bm, g, s), "router logits gemm");
+    if (norms) {  // 256-column tiles; the columns past the logit row are not stored
+        g.N = router_n256(d);
+        g.ldc = router_ld(d);
+        g.max_tiles = (d.T + 255) / 256;
+        g.C2 = xnorm2;
+    }
+    HIP_CHECK(launch_gemm(d, norms ? EPI_ROUTER_F32 : EPI_STORE_F32, norms ? 256 : bm, g, s), "router logits gemm");
     int32_t* ovf = region<int32_t>(ws, p.ovf);
-    HIP_CHECK(launch_router_fast_finish(d, scores, g.N, p.router_splits, x, xnorm2, w_router, bias,
+    HIP_CHECK(launch_router_fast_finish(d, scores, router_ld(d), p.router_splits, x, xnorm2, w_router, bias,
                                         region<float>(ws, p.wnorm),
                                         region<float>(ws, p.wr32), region<uint16_t>(ws, p.cand),
                                         region<int32_t>(ws, p.ncand), ovf, ovf + 1, idx, gate, s),

@@ -463,17 +463,18 @@ def test_route_near_ties_block_kernels(T, dup):
     assert np.array_equal(host(idx), ref_idx) and np.array_equal(host(gate), ref_gate)
 
 
-@pytest.mark.parametrize("dup", [1, 16, 128])
-def test_route_norms_from_logits_gemm(dup):
-    """256 experts at a token count (51 200 + 77) whose router logits run on
-    256-row tiles of the persistent kernel, which also forms the token norms
-    of the interval test; a partial last tile; token rows of very different
-    norms; exact ties in groups of `dup` router rows (dup = 1: none), with a
-    selection bias. Every token's indices and gates equal the oracle's."""
+@pytest.mark.parametrize("E,dup", [(256, 1), (256, 16), (256, 128), (128, 1), (128, 16), (200, 1)])
+def test_route_norms_from_logits_gemm(E, dup):
+    """E experts at a token count (51 200 + 77) whose router logits run on
+    256-row tiles of the persistent kernel (the logit row rounded up to 256
+    columns), which also forms the token norms of the interval test; a
+    partial last tile; token rows of very different norms; exact ties in
+    groups of `dup` router rows (dup = 1: none), with a selection bias. Every
+    token's indices and gates equal the oracle's."""
     from workloads import bf16_bits_to_f32, f32_to_bf16_bits
 
-    T, d, E, K = 51200 + 77, 128, 256, 8
-    rng = np.random.default_rng(7 + dup)
+    T, d, K = 51200 + 77, 128, 8
+    rng = np.random.default_rng(7 + dup + E)
     scale = np.exp(rng.uniform(-3.0, 1.5, (T, 1))).astype(np.float32)
     x = f32_to_bf16_bits(rng.standard_normal((T, d)).astype(np.float32) * scale)
     base = f32_to_bf16_bits((rng.standard_normal((E // dup, d)) * 0.05).astype(np.float32))
