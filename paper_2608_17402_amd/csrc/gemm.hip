@@ -476,8 +476,11 @@ void k_gemm_bf16(const GemmArgs a) {
     // written to the wave's own LDS area row by row (rows padded by 16 bytes
     // so the 32 rows of one write spread over the banks), then read back as
     // 16-byte row pieces so that consecutive lanes store whole 128-byte lines.
-    constexpr bool OUT_F32 = EPI == EPI_STORE_F32 || EPI == EPI_SCATTER_SLOT_F32 || WGRAD;
-    constexpr int OES = OUT_F32 ? 4 : 2;           // output element size
+    // The fused combine (dense, K <= 8) stages the shared expert's fp32 output.
+    constexpr bool COMB = EPI == EPI_COMBINE;
+    static_assert(!(COMB && GROUPED), "the fused combine is a dense (shared expert) epilogue");
+    constexpr bool OUT_F32 = EPI == EPI_STORE_F32 || EPI == EPI_SCATTER_SLOT_F32 || WGRAD || COMB;
+    constexpr int OES = OUT_F32 ? 4 : 2;           // staged element size
     constexpr int SEG = (SWIGLU ? HW : WTN) * OES * (DSW ? 2 : 1);  // bytes of one wave-tile row
     constexpr int RSTR = SEG + 16;                 // padded LDS row stride
     constexpr int CPRO = SEG / 16;                 // 16-byte pieces per row
@@ -562,6 +565,48 @@ void k_gemm_bf16(const GemmArgs a) {
             const int rr = q / CPRO, pc = q % CPRO;
             const int r = wm * WTM + i * 32 + rr;
             const uint4 v = *reinterpret_cast<const uint4*>(stg + rr * RSTR + pc * 16);
+            if constexpr (COMB) {
+                // y for the piece's four columns, in the separate combine's
+                // order: acc = 0, acc = fma(g_j, O_j, acc) for j = 0..K-1 over
+                // the token's expert-output rows (slot order), then
+                // fma(lambda, S, acc) and one rounding to bf16. Slots past K
+                // re-read slot K - 1 and are not added.
+                if (r < tc.rows) {
+                    const int tok = tc.row0 + r;
+                    const int col = ocol0 + pc * 4;
+                    const int K = a.route_k;
+                    const bf16_t* eo = static_cast<const bf16_t*>(a.eo);
+                    float gj[kMaxCombineK];
+                    uint2 o[kMaxCombineK];
+#pragma unroll
+                    for (int j = 0; j < kMaxCombineK; ++j) {
+                        const int jj = j < K ? j : K - 1;
+                        gj[j] = a.gate[(size_t)tok * K + jj];
+                        o[j] = *reinterpret_cast<const uint2*>(eo + ((size_t)tok * K + jj) * a.N + col);
+                    }
+                    float c4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+                    for (int j = 0; j < kMaxCombineK; ++j)
+                        if (j < K) {
+                            c4[0] = fmaf(gj[j], __uint_as_float(o[j].x << 16), c4[0]);
+                            c4[1] = fmaf(gj[j], __uint_as_float(o[j].x & 0xffff0000u), c4[1]);
+                            c4[2] = fmaf(gj[j], __uint_as_float(o[j].y << 16), c4[2]);
+                            c4[3] = fmaf(gj[j], __uint_as_float(o[j].y & 0xffff0000u), c4[3]);
+                        }
+                    const float sv[4] = {__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z),
+                                         __uint_as_float(v.w)};
+                    uint32_t h[4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        uint32_t u = __float_as_uint(fmaf(a.lambda, sv[q], c4[q]));
+                        u += 0x7fffu + ((u >> 16) & 1u);  // round to nearest even (finite values)
+                        h[q] = u >> 16;
+                    }
+                    *reinterpret_cast<uint2*>(static_cast<bf16_t*>(a.C) + (size_t)tok * a.N + col) =
+                        make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+                }
+                continue;
+            }
             if (r < tc.rows && (!SWIGLU || ocol0 < a.act_ld)) {
                 size_t orow = O_SCATTER ? (size_t)srow[r] : (size_t)(tc.row0 + r);
                 void* obase = a.C;
@@ -2086,7 +2131,11 @@ hipError_t dispatch(const moe_desc_t& d, int epilogue, int bm, const GemmArgs& a
                 break;
             case EPI_COMBINE:
                 if (!GROUPED && gemm_combine_fusable(d, bm, a.N, a.Kdim) && a.route_k == d.K)
-                    return launch_pp_combine(a, s);
+                {
+                    if (bm == 256) return launch_pp_combine(a, s);
+                    if (a.N % 128 == 0) return launch_bf16<64, 128, 1, 4, 64, 3, 2, EPI_COMBINE, false>(a, s);
+                    return launch_bf16<64, 64, 2, 2, 64, 3, 2, EPI_COMBINE, false>(a, s);
+                }
                 break;
         }
     } else {
@@ -2127,8 +2176,10 @@ bool gemm_backward_transposed(const moe_desc_t& d, int bm) {
 }
 
 bool gemm_combine_fusable(const moe_desc_t& d, int bm, int n, int kdim) {
-    // The persistent 256 x 256 kernel with its combine epilogue (K <= 8).
-    return d.dtype == MOE_BF16 && d.K <= 8 && bm == 256 && n % 256 == 0 && kdim >= 128;
+    // The persistent 256 x 256 kernel with its combine epilogue, or the
+    // 64-row tiled kernel with its own (K <= 8 either way).
+    if (d.dtype != MOE_BF16 || d.K > kMaxCombineK) return false;
+    return (bm == 256 && n % 256 == 0 && kdim >= 128) || (bm == 64 && n % 64 == 0);
 }
 
 hipError_t launch_gemm(const moe_desc_t& d, int epilogue, int bm, const GemmArgs& a, hipStream_t s) {

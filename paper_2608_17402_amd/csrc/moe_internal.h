@@ -17,6 +17,7 @@ typedef uint16_t bf16_t;
 constexpr int kWave = 64;          // CDNA wavefront width
 constexpr int kNumXcd = 8;         // MI355X: 8 accelerator complex dies, 32 CUs each
 constexpr int kMaxE = 1024;
+constexpr int kMaxCombineK = 8;  // routed slots per token the fused combine epilogues take
 constexpr int kMaxK = 16;
 
 // One M-tile of a grouped GEMM: `rows` rows (<= BM) of expert `e`, starting

@@ -106,34 +106,73 @@ __global__ __launch_bounds__(1024) void k_scan(int32_t* __restrict__ blockhist, 
                                               int32_t* __restrict__ offsets, int bm, int max_tiles,
                                               TileDesc* __restrict__ tiles, int32_t* __restrict__ n_tiles) {
     __shared__ int buf[kScanMax];
+    __shared__ int segtot[1024];
     __shared__ int tmp[32];
     __shared__ int offl[kMaxE + 1];
     __shared__ int start[kMaxE + 1];
+    const int tid = threadIdx.x;
     const int n = nb * E;
-    for (int i = threadIdx.x; i < n; i += blockDim.x) buf[i] = blockhist[i];
-    __syncthreads();
-    int cnt = 0;
-    if ((int)threadIdx.x < E) {
-        for (int b = 0; b < nb; ++b) {
-            const int v = buf[b * E + threadIdx.x];
-            buf[b * E + threadIdx.x] = cnt;
-            cnt += v;
+    {  // 16-byte loads, four per thread in flight (n <= kScanMax = 16 x 1024)
+        const int n4 = n / 4;
+        const int4* bh4 = reinterpret_cast<const int4*>(blockhist);
+        const int nt = blockDim.x;
+        for (int i = tid; i < n4; i += 4 * nt) {
+            int4 v[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (i + u * nt < n4) v[u] = bh4[i + u * nt];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (i + u * nt < n4) {
+                    const int j = 4 * (i + u * nt);
+                    buf[j] = v[u].x;
+                    buf[j + 1] = v[u].y;
+                    buf[j + 2] = v[u].z;
+                    buf[j + 3] = v[u].w;
+                }
         }
+        for (int i = 4 * n4 + tid; i < n; i += nt) buf[i] = blockhist[i];
+    }
+    // Each expert's column of chunk counts is cut into S segments of
+    // consecutive chunks, thread (segment g, expert e) = tid g E + e.
+    const int S = max(1, min(nb, (int)blockDim.x / E));
+    const int per = (nb + S - 1) / S;
+    const int e = tid % E, g = tid / E;
+    const bool act = g < S;
+    const int b0 = min(nb, g * per), b1 = min(nb, b0 + per);
+    __syncthreads();
+    int seg = 0;
+    if (act)
+        for (int b = b0; b < b1; ++b) seg += buf[b * E + e];
+    if (act) segtot[g * E + e] = seg;
+    __syncthreads();
+    // The segment's start within its expert, then the exclusive prefix of
+    // every chunk of the segment; thread (0, e) also forms the expert's total.
+    int cnt = 0;
+    if (act) {
+        int run = 0;
+        for (int q = 0; q < g; ++q) run += segtot[q * E + e];
+        for (int b = b0; b < b1; ++b) {
+            const int v = buf[b * E + e];
+            buf[b * E + e] = run;
+            run += v;
+        }
+        if (g == 0)
+            for (int q = 0; q < S; ++q) cnt += segtot[q * E + e];
     }
     int total;
-    const int excl = block_exclusive_scan_1024((int)threadIdx.x < E ? cnt : 0, tmp, &total);
-    if ((int)threadIdx.x < E) {
-        counts[threadIdx.x] = cnt;
-        offsets[threadIdx.x] = excl;
-        offl[threadIdx.x] = excl;
-        for (int b = 0; b < nb; ++b) buf[b * E + threadIdx.x] += excl;
+    const int excl = block_exclusive_scan_1024(tid < E ? cnt : 0, tmp, &total);
+    if (tid < E) {
+        counts[tid] = cnt;
+        offsets[tid] = excl;
+        offl[tid] = excl;
     }
-    if (threadIdx.x == 0) {
+    if (tid == 0) {
         offsets[E] = total;
         offl[E] = total;
     }
     __syncthreads();
-    for (int i = threadIdx.x; i < n; i += blockDim.x) blockhist[i] = buf[i];
+    for (int i = tid; i < n; i += blockDim.x) blockhist[i] = buf[i] + offl[i % E];
     if (tiles) build_tiles_block(E, bm, max_tiles, offl, tiles, n_tiles, start, tmp);
 }
 

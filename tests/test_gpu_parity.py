@@ -386,6 +386,28 @@ def test_fused_combine_any_k(K):
     check_close(yh[tail], y_ref[tail], True, f"fused combine K={K} (tail tile)")
 
 
+@pytest.mark.parametrize("d", [192, 256])
+@pytest.mark.parametrize("K", [1, 3, 7, 8])
+def test_fused_combine_tiled_any_k(K, d):
+    """On 64-row tiles (a few hundred tokens) the shared expert's fc2 also
+    performs the combine, for every K <= 8, on both tile widths (128 columns
+    for d = 256, 64 for d = 192) and a ragged last tile: every token matches
+    the oracle, and a repeat is bit-identical."""
+    from workloads.configs import LayerConfig
+
+    cfg = LayerConfig(name=f"fused_tiled_k{K}_d{d}", T=700, d=d, E=16, K=K, h=128, h_shared=320,
+                      dtype="bf16", bias="uniform", seed=60 + K + d)
+    inp = make_inputs(cfg)
+    lay = DeviceLayer(inp)
+    y, idx, gate = lay.forward()
+    y2, _, _ = lay.forward()
+    torch.cuda.synchronize()
+    assert np.array_equal(host(y).view(np.uint32), host(y2).view(np.uint32))
+    o_idx, o_gate, y_ref = _oracle_layer(inp, cfg)
+    assert np.array_equal(host(idx), o_idx) and np.array_equal(host(gate), o_gate)
+    check_close(host(y), y_ref, True, f"tiled fused combine K={K} d={d} (every token)")
+
+
 @pytest.fixture(scope="module")
 def persistent_layer():
     """ViT-G widths (d = 1536, h = 768, h_s = 1536) with 8 experts and K = 2
