@@ -326,6 +326,10 @@ static moe_status_t enqueue_routed_mlp(const moe_desc_t& d, const WorkspacePlan&
     g.a_bytes = (uint32_t)((size_t)d.T * d.d * elem_size(d.dtype));
     g.act_n = d.h;
     g.act_ld = ldh;
+    // Weight-read-bound (one 64-row M-tile per expert on average): each expert's
+    // weights are read once, non-temporally, so that they do not evict the
+    // gathered token rows and the activation rows, which are read again.
+    g.b_nt = p.tile_bm == 64 && (int64_t)d.T * d.K <= (int64_t)64 * d.E;
     HIP_CHECK(launch_gemm(d, swiglu ? EPI_SWIGLU_STORE : EPI_GELU_STORE, p.tile_bm, g, s), "fc1 grouped gemm");
     if (events) HIP_CHECK(hipEventRecord(static_cast<hipEvent_t>(events[1]), s), "event record");
     GemmArgs g2 = g;

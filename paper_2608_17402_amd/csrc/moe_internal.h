@@ -104,6 +104,8 @@ struct GemmArgs {
     float lambda;              // EPI_COMBINE: shared-expert weight
     int32_t k_splits;          // tiled kernel, dense EPI_STORE_F32 only: K split into this many parts (0 or
                                // 1 = none), part p writing its partial sums to C + p * dense_rows * N
+    int32_t b_nt;              // tiled kernel: B is read once by the launch (one M-tile per group on
+                               // average), so its copies carry the non-temporal hint
 };
 
 // Offsets (bytes) of every workspace region for one descriptor.
