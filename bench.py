@@ -207,6 +207,18 @@ def main():
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / reps
 
+    def split_fc1_fc2(L, reps):
+        """Average fc1 and fc2 times (ms) from a pass with all three of
+        moe_layer_forward's events (the middle one's queue gap included)."""
+        ev = binding.HipEvents(3 * reps)
+        for i in range(reps):
+            L.forward(ev.handles[3 * i:3 * i + 3])
+        torch.cuda.synchronize()
+        f1 = sum(ev.elapsed_ms(3 * i, 3 * i + 1) for i in range(reps)) / reps
+        f2 = sum(ev.elapsed_ms(3 * i + 1, 3 * i + 2) for i in range(reps)) / reps
+        ev.close()
+        return f1, f2
+
     if args.mode == "copy":
         n = args.copy_mib << 20
         a = torch.ones(n // 2, dtype=torch.bfloat16, device="cuda")
@@ -270,20 +282,23 @@ def main():
     wall0 = time.perf_counter()
     sev[0].record(stream)
     for i in range(args.steps):
-        lay.forward(hev.handles[3 * i:3 * i + 3])
+        # The events right before fc1 and right after fc2 (no event between
+        # them, whose queue gap would count in the pair's time).
+        h = hev.handles[3 * i:3 * i + 3]
+        lay.forward([h[0], None, h[2]])
         sev[i + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     ms = sev[0].elapsed_time(sev[-1]) / args.steps
     step_ms = np.array([sev[i].elapsed_time(sev[i + 1]) for i in range(args.steps)])
     value = cfg.T / (ms * 1e-3)
-    fc1_ms = sum(hev.elapsed_ms(3 * i, 3 * i + 1) for i in range(args.steps)) / args.steps
-    fc2_ms = sum(hev.elapsed_ms(3 * i + 1, 3 * i + 2) for i in range(args.steps)) / args.steps
+    gemm_ms = sum(hev.elapsed_ms(3 * i, 3 * i + 2) for i in range(args.steps)) / args.steps
     hev.close()
+    # The fc1 / fc2 split, from a pass with the middle event as well.
+    fc1_ms, fc2_ms = split_fc1_fc2(lay, args.steps)
 
     # Per-stage times (the stage entry points run the same kernels).
     stages_ms = {k: time_calls(f, args.stage_reps) for k, f in lay.stages().items()}
-    gemm_ms = fc1_ms + fc2_ms
     routed_flops = 2.0 * cfg.n_mats * cfg.T * cfg.K * cfg.d * cfg.h
     achieved = routed_flops / (gemm_ms * 1e-3) / 1e12
     roofline = {
@@ -292,7 +307,8 @@ def main():
         "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic_bytes(cfg.name),
         "algorithmic_flops_per_launch": routed_flops, "avg_launch_us": round(gemm_ms * 1e3, 2),
         "fc1_us": round(fc1_ms * 1e3, 2), "fc2_us": round(fc2_ms * 1e3, 2),
-        "timing": "HIP events recorded by moe_layer_forward on its stream around fc1 and fc2, every timed step",
+        "timing": "HIP events recorded by moe_layer_forward on its stream right before fc1 and right after fc2, "
+                  "every timed step; fc1_us / fc2_us from a further pass with an event between them as well",
     }
     layer_flops = cfg.gemm_flops()
 
@@ -335,12 +351,13 @@ def main():
         l_ms = e0.elapsed_time(e1) / reps
         ev = binding.HipEvents(3 * reps)
         for i in range(reps):
-            L.forward(ev.handles[3 * i:3 * i + 3])
+            h = ev.handles[3 * i:3 * i + 3]
+            L.forward([h[0], None, h[2]])
         torch.cuda.synchronize()
-        f1 = sum(ev.elapsed_ms(3 * i, 3 * i + 1) for i in range(reps)) / reps
-        f2 = sum(ev.elapsed_ms(3 * i + 1, 3 * i + 2) for i in range(reps)) / reps
+        pair = sum(ev.elapsed_ms(3 * i, 3 * i + 2) for i in range(reps)) / reps
         ev.close()
-        return L, l_ms, f1, f2
+        f1, f2 = split_fc1_fc2(L, reps)
+        return L, l_ms, pair, f1, f2
 
     def dense_reference(c, routed_tflops):
         """Same-box context for the routed grouped GEMM: hipBLASLt (through
@@ -434,7 +451,7 @@ def main():
                          "algorithmic_flops_per_launch": fl, "avg_launch_us": round(b_ms * 1e3, 2)},
         }
 
-    def hbm_line(c, L, l_ms, g_ms):
+    def hbm_line(c, L, l_ms, g_ms, f1, f2):
         w_bytes = c.routed_weight_bytes()
         gbs = w_bytes / (g_ms * 1e-3) / 1e9
         return {
@@ -444,13 +461,14 @@ def main():
                          "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                          "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": traffic_bytes(c.name),
                          "algorithmic_bytes_per_launch": w_bytes,
-                         "avg_launch_us": round(g_ms * 1e3, 2)},
+                         "avg_launch_us": round(g_ms * 1e3, 2),
+                         "fc1_us": round(f1 * 1e3, 2), "fc2_us": round(f2 * 1e3, 2)},
             "layer_weight_gbs": round((w_bytes + c.shared_weight_bytes()) / (l_ms * 1e-3) / 1e9, 1),
         }
 
-    def mfma_line(c, l_ms, f1, f2):
+    def mfma_line(c, l_ms, pair, f1, f2):
         fl = 2.0 * c.n_mats * c.T * c.K * c.d * c.h
-        tf = fl / ((f1 + f2) * 1e-3) / 1e12
+        tf = fl / (pair * 1e-3) / 1e12
         return {
             "workload": c.name, "tokens": c.T, "act": c.act, "us_per_layer": round(l_ms * 1e3, 1),
             "tokens_per_s": round(c.T / (l_ms * 1e-3), 1),
@@ -458,7 +476,7 @@ def main():
             "roofline": {"kernel": "routed grouped GEMM (fc1 with its activation, fc2)", "bound": "mfma",
                          "achieved": round(tf, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                          "frac": round(tf / PEAK_BF16_TFLOPS, 4), "traffic": traffic_bytes(c.name),
-                         "algorithmic_flops_per_launch": fl, "avg_launch_us": round((f1 + f2) * 1e3, 2),
+                         "algorithmic_flops_per_launch": fl, "avg_launch_us": round(pair * 1e3, 2),
                          "fc1_us": round(f1 * 1e3, 2), "fc2_us": round(f2 * 1e3, 2)},
         }
 
@@ -470,8 +488,8 @@ def main():
         out["mfma_layers"] = {}
         for name in mf_names:
             c = get_config(name)
-            L, l_ms, f1, f2 = measure(c, max(args.steps, 20))
-            line = mfma_line(c, l_ms, f1, f2)
+            L, l_ms, pair, f1, f2 = measure(c, max(args.steps, 20))
+            line = mfma_line(c, l_ms, pair, f1, f2)
             st_ms = {k: time_calls(f, args.stage_reps) for k, f in L.stages().items()}
             line["stages_us"] = {k: round(v * 1e3, 1) for k, v in st_ms.items()}
             line["stages_gbs"] = stage_gbs(c, st_ms)
@@ -481,9 +499,9 @@ def main():
     if not args.no_single_image:
         c5 = get_config(args.single_image_config)
         reps = max(args.steps, 20)
-        si, si_ms, f1, f2 = measure(c5, reps)
+        si, si_ms, pair, f1, f2 = measure(c5, reps)
         si_stages = {k: time_calls(f, max(args.stage_reps, 20)) for k, f in si.stages().items()}
-        out["single_image"] = hbm_line(c5, si, si_ms, f1 + f2)
+        out["single_image"] = hbm_line(c5, si, si_ms, pair, f1, f2)
         out["single_image"]["stages_us"] = {k: round(v * 1e3, 1) for k, v in si_stages.items()}
         del si
 
@@ -495,10 +513,11 @@ def main():
         out["swiglu"] = {}
         for name in sw_names:
             c = get_config(name)
-            L, l_ms, f1, f2 = measure(c, max(args.steps, 20))
+            L, l_ms, pair, f1, f2 = measure(c, max(args.steps, 20))
             # ~32 rows per expert is weight-read bound; large batches are MFMA bound.
             weight_bound = c.T * c.K / c.E < 256
-            out["swiglu"][name] = hbm_line(c, L, l_ms, f1 + f2) if weight_bound else mfma_line(c, l_ms, f1, f2)
+            out["swiglu"][name] = (hbm_line(c, L, l_ms, pair, f1, f2) if weight_bound
+                                   else mfma_line(c, l_ms, pair, f1, f2))
             if not weight_bound and not args.no_backward:
                 out["swiglu"][name]["backward"] = backward_line(c, L)
             del L

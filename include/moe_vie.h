@@ -173,9 +173,13 @@ moe_status_t moe_combine(const moe_desc_t *desc, const void *expert_out, const f
  *   y [T, d] layer dtype out
  *   topk_idx_out [T, K] int32 and topk_gate_out [T, K] fp32: optional
  *   copies of the routing (NULL = not returned)
- *   events: NULL, or three hipEvent_t (created by the caller) recorded on
- *   `stream` right before the routed fc1 launch, between fc1 and fc2, and
- *   right after fc2, to time the grouped expert GEMMs inside the layer
+ *   events: NULL, or three hipEvent_t slots (events created by the caller)
+ *   recorded on `stream` right before the routed fc1 launch, between fc1 and
+ *   fc2, and right after fc2: a timing hook for the grouped expert GEMMs
+ *   inside the layer. The middle slot may be NULL (not recorded): each
+ *   recorded event leaves a gap of a few microseconds in the queue, so the
+ *   pair is timed best from the outer two alone. The first and the last must
+ *   be events (MOE_ERR_INVALID_ARG otherwise)
  * The shared expert's output stays fp32 until the combine. */
 moe_status_t moe_layer_forward(const moe_desc_t *desc, const void *x, const void *w_router,
                                const float *bias, const void *w1, const void *w2,

@@ -177,12 +177,13 @@ def moe_combine(desc, expert_out, topk_gate, shared_out, y, stream=None):
 def moe_layer_forward(desc, x, w_router, bias, w1, w2, w1s, w2s, y, topk_idx_out=None, topk_gate_out=None,
                       workspace=None, stream=None, events=None):
     """events: None or three raw hipEvent_t handles (ints) recorded before the
-    routed fc1, between fc1 and fc2, and after fc2."""
+    routed fc1, between fc1 and fc2, and after fc2; the middle one may be
+    None (not recorded)."""
     dt = torch_dtype(desc)
     ev = None
     if events is not None:
         if len(events) != 3:
-            raise ValueError("events must hold three hipEvent_t handles")
+            raise ValueError("events must hold three hipEvent_t handles (the middle one may be None)")
         ev = (ctypes.c_void_p * 3)(*events)
     _check(load().moe_layer_forward(ctypes.byref(desc), _ptr(x, "x", dt), _ptr(w_router, "w_router", dt),
                                     _ptr(bias, "bias", torch.float32), _ptr(w1, "w1", dt), _ptr(w2, "w2", dt),

@@ -919,6 +919,9 @@ void k_gemm_pp(const GemmArgs a) {
     // Workgroups of odd XCDs start about 80k cycles later, so that their
     // epilogues overlap the other XCDs' K loops (whole XCDs, so that each L2
     // still sees its tiles in step). Measured at ViT-G: the layer -1.3 %.
+    // "xcd" is blockIdx mod kNumXcd, which names the XCD only under the
+    // round-robin dispatch of MI355X; under another dispatch a different half
+    // of the workgroups waits, which changes the speed, never the tiles.
     if constexpr (EPI == EPI_COMBINE) {
         if (xcd & 1)
             for (int q = 0; q < 10; ++q) __builtin_amdgcn_s_sleep(127);

@@ -15,7 +15,11 @@ namespace moe {
 typedef uint16_t bf16_t;
 
 constexpr int kWave = 64;          // CDNA wavefront width
-constexpr int kNumXcd = 8;         // MI355X: 8 accelerator complex dies, 32 CUs each
+// MI355X: 8 accelerator complex dies, 32 CUs each, workgroups dispatched
+// round-robin over them. A performance assumption only: the XCD-aware tile
+// orders built on it are bijections over the grid, so which tiles run, and
+// every result, is the same on a part with another XCD count or dispatch.
+constexpr int kNumXcd = 8;
 constexpr int kMaxE = 1024;
 constexpr int kMaxCombineK = 8;  // routed slots per token the fused combine epilogues take
 constexpr int kMaxK = 16;

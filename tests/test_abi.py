@@ -128,6 +128,10 @@ def test_entry_points_reject_bad_pointers_before_any_launch(lib):
     assert lib.moe_layer_forward(ctypes.byref(desc0), fake, fake, None, fake, fake, None, None, fake, None,
                                  None, fake, S(need), half, None) == 1
     assert b"events" in lib.moe_last_error()
+    first_null = (ctypes.c_void_p * 3)(None, 1 << 21, 1 << 22)
+    assert lib.moe_layer_forward(ctypes.byref(desc0), fake, fake, None, fake, fake, None, None, fake, None,
+                                 None, fake, S(need), first_null, None) == 1
+    assert b"events" in lib.moe_last_error()
 
 
 def test_bias_update_rejects_bad_arguments(lib):

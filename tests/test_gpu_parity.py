@@ -170,6 +170,23 @@ def test_layer_forward(small):
     check_close(host(y), y_ref, bf16, "layer y")
 
 
+def test_layer_timing_events_change_nothing(small):
+    """The timing hook: three events, or the outer two with the middle slot
+    NULL, are recorded in order around the routed GEMMs and leave y as it is."""
+    cfg, inp, lay, bf16, _, _ = small
+    y0, _, _ = lay.forward()
+    ev = binding.HipEvents(6)
+    h = ev.handles
+    for events in (h[0:3], [h[3], None, h[5]]):
+        y = lay.empty(lay.desc.T, lay.desc.d)
+        binding.moe_layer_forward(lay.desc, lay.x, lay.w_router, lay.bias, lay.w1, lay.w2, lay.w1s, lay.w2s, y,
+                                  workspace=lay.ws, events=events)
+        torch.cuda.synchronize()
+        assert torch.equal(y.view(torch.int16) if bf16 else y, y0.view(torch.int16) if bf16 else y0)
+    assert ev.elapsed_ms(0, 1) >= 0 and ev.elapsed_ms(1, 2) >= 0 and ev.elapsed_ms(3, 5) > 0
+    ev.close()
+
+
 def test_layer_deterministic(small):
     _, _, lay, _, _, _ = small
     y1, i1, g1 = lay.forward()
