@@ -338,6 +338,16 @@ void k_gemm_bf16(const GemmArgs a) {
         for (int j = 0; j < FN; ++j) tie(wf[j]);
     };
 
+    // Router logits of small batches (dense fp32 output with C2 set): the
+    // workgroups of M-tile 0 also add up the squares of the weight rows of
+    // their K part (the weight fragments pass through registers anyway), for
+    // the norms of the router's interval test; C2 [parts][N] gets them.
+    constexpr bool WSQ = !GROUPED && EPI == EPI_STORE_F32;
+    const bool wsq_on = WSQ && a.C2 && tc.row0 == 0 && wm == 0;
+    float wsq[FN];
+#pragma unroll
+    for (int j = 0; j < FN; ++j) wsq[j] = 0.0f;
+
 #pragma unroll
     for (int sl = 0; sl < STAGES - 1; ++sl)
         if (sl < nk) issue(sl, sl);
@@ -369,10 +379,31 @@ void k_gemm_bf16(const GemmArgs a) {
 #pragma unroll
                 for (int i = 0; i < FM; ++i)
                     acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[c][j], xf[c][i], acc[j][i], 0, 0, 0);
+            if constexpr (WSQ) {
+                if (wsq_on) {
+#pragma unroll
+                    for (int j = 0; j < FN; ++j)
+#pragma unroll
+                        for (int q = 0; q < 8; ++q) {
+                            const float v = (float)wf[c][j][q];
+                            wsq[j] = fmaf(v, v, wsq[j]);
+                        }
+                }
+            }
             __builtin_amdgcn_sched_barrier(0);
             if (ks + 1 < KS) settle(xf[c ^ 1], wf[c ^ 1]);
         }
         if (++cur_stage == STAGES) cur_stage = 0;
+    }
+    if constexpr (WSQ) {
+        if (wsq_on) {  // lanes l and l + 32 hold the two K halves of weight row l % 32
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+                const float v = wsq[j] + __shfl_xor(wsq[j], 32);
+                const int col = tc.n0 + wn * WTN + j * 32 + fr;
+                if (fk == 0 && col < a.N) static_cast<float*>(a.C2)[(size_t)blockIdx.y * a.N + col] = v;
+            }
+        }
     }
 
     // Epilogue, one 32-row block of the wave tile at a time. Block (j, i):

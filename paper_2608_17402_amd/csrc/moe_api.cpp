@@ -200,7 +200,9 @@ WorkspacePlan plan_workspace(const moe_desc_t& d) {
     p.router_splits = router_splits(d);
     p.scores = take((size_t)p.router_splits * d.T * router_ld(d) * 4);
     p.wnorm = take((size_t)d.E * 4);
-    p.wr32 = take(fast_router(d) && router_small_batch(d) ? (size_t)d.E * d.d * 4 : 0);
+    const bool small_fused = fast_router(d) && router_small_fused(d);
+    p.wr32 = take(fast_router(d) && router_small_batch(d) && !small_fused ? (size_t)d.E * d.d * 4 : 0);
+    p.wsq = take(small_fused ? (size_t)p.router_splits * router_ld(d) * 4 : 0);
     p.xnorm2 = take(router_norms_in_gemm(d) ? (size_t)d.T * 4 : 0);
     p.ovf = take((size_t)(d.T + 1) * 4);
     p.cand = take((size_t)d.T * router_cand_slots(d.K) * 2);
@@ -287,11 +289,15 @@ static moe_status_t enqueue_route(const moe_desc_t& d, const WorkspacePlan& p, v
         g.max_tiles = (d.T + 255) / 256;
         g.C2 = xnorm2;
     }
+    // Small batches: the logits GEMM (64-row tiles) also forms the weight
+    // rows' sums of squares per K part, and the repair is one launch.
+    float* wsq = router_small_fused(d) ? region<float>(ws, p.wsq) : nullptr;
+    if (wsq) g.C2 = wsq;
     HIP_CHECK(launch_gemm(d, norms ? EPI_ROUTER_F32 : EPI_STORE_F32, norms ? 256 : bm, g, s), "router logits gemm");
     int32_t* ovf = region<int32_t>(ws, p.ovf);
     HIP_CHECK(launch_router_fast_finish(d, scores, router_ld(d), p.router_splits, x, xnorm2, w_router, bias,
                                         region<float>(ws, p.wnorm),
-                                        region<float>(ws, p.wr32), region<uint16_t>(ws, p.cand),
+                                        region<float>(ws, p.wr32), wsq, region<uint16_t>(ws, p.cand),
                                         region<int32_t>(ws, p.ncand), ovf, ovf + 1, idx, gate, s),
               "router repair");
     return MOE_OK;

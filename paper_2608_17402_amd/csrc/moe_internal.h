@@ -88,7 +88,9 @@ struct GemmArgs {
     int32_t b_rows;            // dense bf16 only: rows of B that exist (0 = N); rows past them read as zeros
     uint32_t a_bytes;          // bytes of the A operand buffer (bounds of its buffer resource)
     void* C2;                  // EPI_GELU_BWD: second output (fp32); EPI_WGRAD_F32: partial blocks;
-                               // EPI_ROUTER_F32: the rows' sums of squares [dense_rows] (fp32)
+                               // EPI_ROUTER_F32: the rows' sums of squares [dense_rows] (fp32);
+                               // tiled dense EPI_STORE_F32: the sums of squares of B's rows over each K
+                               // part, [k_splits][N] (fp32), or null
     // Backward, persistent kernel: the bf16 output (the activation, or dH) also
     // written transposed into the weight-gradient K windows, slab-major
     // [windows / 64][ct_cols][64]: sorted position p of expert e goes to window
@@ -115,7 +117,7 @@ struct GemmArgs {
 // Offsets (bytes) of every workspace region for one descriptor.
 struct WorkspacePlan {
     size_t idx, gate, scores, counts, offsets, slots, blockhist, tiles, ntiles;
-    size_t wnorm, ovf, cand, ncand, wr32, xnorm2;
+    size_t wnorm, ovf, cand, ncand, wr32, xnorm2, wsq;
     int32_t router_splits;   // split-K parts of the fast router's logits GEMM
     size_t act, eout, sact, sout;
     size_t total;
@@ -178,13 +180,20 @@ hipError_t launch_topk(const moe_desc_t& d, const float* scores, const float* bi
 // wr32 [E, d], which the norm kernel writes; larger ones ignore it. xnorm2
 // [T]: the tokens' sums of squares if the logits GEMM formed them
 // (EPI_ROUTER_F32), else nullptr and the candidate kernel reads x for them.
+// wsq [nsplit][ld]: the weight rows' sums of squares over each K part (the
+// logits GEMM's second output), given exactly when router_small_fused holds;
+// the whole repair then runs in one launch and wnorm, wr32, cand, ncand and
+// the overflow queue are not touched.
 hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, int ld, int nsplit, const void* x,
                                      const float* xnorm2, const void* w_router, const float* bias, float* wnorm,
-                                     float* wr32,
+                                     float* wr32, const float* wsq,
                                      uint16_t* cand, int32_t* ncand, int32_t* ovf_count, int32_t* ovf_list,
                                      int32_t* topk_idx, float* topk_gate, hipStream_t s);
 // Whether the fast router takes the small-batch chain kernel (fp32 weight copy).
 bool router_small_batch(const moe_desc_t& d);
+// Whether the small-batch repair runs as one launch (K <= 8, E <= 256,
+// d <= 4096): the logits GEMM then also forms the weight rows' sums of squares.
+bool router_small_fused(const moe_desc_t& d);
 int router_cand_slots(int K);
 // Grouping of slots by expert; with a tile table (tiles != nullptr) the scan
 // kernel also cuts the segments into M-tiles of bm rows (as launch_build_tiles).

@@ -8,6 +8,7 @@
 //             Taylor polynomial, using only correctly rounded operations.
 // This file is compiled with -ffp-contract=off so the compiler cannot fuse or
 // reorder any of these steps.
+#include "gemm_device.h"
 #include "moe_internal.h"
 
 #include <math.h>
@@ -283,27 +284,6 @@ __global__ __launch_bounds__(256) void k_row_norms(const bf16_t* __restrict__ a,
     if (lane == 0) out[row] = sqrtf(acc) * 1.001f + 1e-30f;
 }
 
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-
-// Candidates of each token: LPA lanes per token, lane g holding experts
-// g PER .. g PER + PER - 1 (contiguous, so that its logits are PER / 4
-// 16-byte loads); the MFMA logits have rows of ld >= E (a multiple of 64), in
-// nsplit partial arrays (split K) sstride floats apart. L = the K-th largest
-// lower end of the key intervals; the candidates are the experts whose upper
-// end reaches L, written to cand[t][0 .. NS) (in no particular order) with
-// their count in ncand[t]. A token with more than NS candidates gets
-// ncand = -1 and is appended to the overflow queue.
-// Compile-time loop: f(std::integral_constant<int, i>) for i = 0 .. N-1.
-template <typename F, int... Is>
-__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, Is...>) {
-    (f(std::integral_constant<int, Is>{}), ...);
-}
-template <int N, typename F>
-__device__ __forceinline__ void static_for(F&& f) {
-    static_for_impl(f, std::make_integer_sequence<int, N>{});
-}
-
-
 // Maximum over each aligned group of 16 lanes (a DPP row), in every lane of
 // the group: swaps inside quads (xor 1, xor 2), then the mirror inside each
 // half row and the mirror of the whole row.
@@ -343,6 +323,15 @@ __device__ __forceinline__ void load_row(const float* p, float (&v)[PER]) {
         v[4 * i + 3] = q.w;
     }
 }
+
+// Candidates of each token: LPA lanes per token, lane g holding experts
+// g PER .. g PER + PER - 1 (contiguous, so that its logits are PER / 4
+// 16-byte loads); the MFMA logits have rows of ld >= E (a multiple of 64), in
+// nsplit partial arrays (split K) sstride floats apart. L = the K-th largest
+// lower end of the key intervals; the candidates are the experts whose upper
+// end reaches L, written to cand[t][0 .. NS) (in no particular order) with
+// their count in ncand[t]. A token with more than NS candidates gets
+// ncand = -1 and is appended to the overflow queue.
 template <int LPA, int PER, int NS, bool SPLIT>
 __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s_fast,
                                                     const bf16_t* __restrict__ x,
@@ -515,15 +504,25 @@ __device__ __forceinline__ void chain_select(uint8_t* lds, int tl, int g, int t,
         }
     }
     __syncthreads();
+    // The token's NS keys and experts in 16-byte reads (slots from nc on are
+    // read but not counted).
+    static_assert(NS % 4 == 0, "whole 16-byte reads");
+    float kq[NS];
+    int eq[NS];
+#pragma unroll
+    for (int q = 0; q < NS; q += 4) {
+        const float4 k4 = *reinterpret_cast<const float4*>(skey + tl * NS + q);
+        const int4 e4 = *reinterpret_cast<const int4*>(sexp + tl * NS + q);
+        kq[q] = k4.x, kq[q + 1] = k4.y, kq[q + 2] = k4.z, kq[q + 3] = k4.w;
+        eq[q] = e4.x, eq[q + 1] = e4.y, eq[q + 2] = e4.z, eq[q + 3] = e4.w;
+    }
 #pragma unroll
     for (int c = 0; c < CPL; ++c) {
         if (!on[c]) continue;
         int rank = 0;  // the candidate itself compares neither greater nor lower
-        for (int q = 0; q < nc; ++q) {
-            const float kq = skey[tl * NS + q];
-            const int eq = sexp[tl * NS + q];
-            rank += (kq > kc[c] || (kq == kc[c] && eq < ec[c])) ? 1 : 0;
-        }
+#pragma unroll
+        for (int q = 0; q < NS; ++q)
+            rank += (q < nc && (kq[q] > kc[c] || (kq[q] == kc[c] && eq[q] < ec[c]))) ? 1 : 0;
         if (rank < K) {
             osig[tl * kMaxK + rank] = sc[c];
             oexp[tl * kMaxK + rank] = ec[c];
@@ -531,8 +530,16 @@ __device__ __forceinline__ void chain_select(uint8_t* lds, int tl, int g, int t,
     }
     __syncthreads();
     if (t >= T || nc == 0) return;
-    float den = osig[tl * kMaxK];
-    for (int j = 1; j < K; ++j) den = den + osig[tl * kMaxK + j];
+    // Gate denominator in slot order 0 .. K - 1.
+    float os[kMaxK];
+#pragma unroll
+    for (int j = 0; j < kMaxK; j += 4) {
+        const float4 o4 = *reinterpret_cast<const float4*>(osig + tl * kMaxK + j);
+        os[j] = o4.x, os[j + 1] = o4.y, os[j + 2] = o4.z, os[j + 3] = o4.w;
+    }
+    float den = os[0];
+#pragma unroll
+    for (int j = 1; j < kMaxK; ++j) den = j < K ? den + os[j] : den;
     for (int j = g; j < K; j += LPT) {
         topk_idx[(size_t)t * K + j] = oexp[tl * kMaxK + j];
         topk_gate[(size_t)t * K + j] = osig[tl * kMaxK + j] / den;
@@ -722,6 +729,74 @@ __global__ __launch_bounds__(TPB* LPT) void k_router_chain(const bf16_t* __restr
     chain_select<TPB, LPT, CPL>(lds, tl, g, t, T, nc, K, on, ec, acc, bc, bias != nullptr, topk_idx, topk_gate);
 }
 
+// Exact top-K of token t from its E sigmoids (sig, in LDS) and gates, by one
+// wave: each of the K rounds takes the wave-wide best key (descending, lower
+// expert index first on equal keys) with a butterfly of cross-lane exchanges.
+__device__ __forceinline__ void exact_select_wave(const float* sig, const float* __restrict__ bias, int E, int K,
+                                                  int t, int lane, int32_t* __restrict__ topk_idx,
+                                                  float* __restrict__ topk_gate) {
+    const int per = (E + kWave - 1) / kWave;
+    float sg[kPerLane], key[kPerLane];
+#pragma unroll
+    for (int m = 0; m < kPerLane; ++m) {
+        const int e = lane + kWave * m;
+        const bool ok = m < per && e < E;
+        sg[m] = ok ? sig[e] : 0.0f;
+        key[m] = ok ? (bias ? sg[m] + bias[e] : sg[m]) : -INFINITY;
+    }
+    uint32_t taken = 0;
+    float csig[kMaxK];
+    int cidx[kMaxK];
+#pragma unroll
+    for (int j = 0; j < kMaxK; ++j) {
+        csig[j] = 0.0f;
+        cidx[j] = 0;
+        if (j >= K) continue;
+        float bk = -INFINITY;
+        int be = 0x7fffffff;
+        float bs = 0.0f;
+#pragma unroll
+        for (int m = 0; m < kPerLane; ++m) {
+            const int e = lane + kWave * m;
+            if (m < per && e < E && !((taken >> m) & 1u) && (key[m] > bk || (key[m] == bk && e < be))) {
+                bk = key[m];
+                be = e;
+                bs = sg[m];
+            }
+        }
+#pragma unroll
+        for (int off = kWave / 2; off > 0; off >>= 1) {
+            const float ok = __shfl_xor(bk, off);
+            const int oe = __shfl_xor(be, off);
+            const float os = __shfl_xor(bs, off);
+            if (ok > bk || (ok == bk && oe < be)) {
+                bk = ok;
+                be = oe;
+                bs = os;
+            }
+        }
+        if ((be & (kWave - 1)) == lane) taken |= 1u << (be / kWave);
+        csig[j] = bs;
+        cidx[j] = be;
+    }
+    float den = csig[0];
+#pragma unroll
+    for (int j = 1; j < kMaxK; ++j)
+        if (j < K) den = den + csig[j];
+    int my_e = 0;
+    float my_g = 0.0f;
+#pragma unroll
+    for (int j = 0; j < kMaxK; ++j)
+        if (j == lane && j < K) {
+            my_e = cidx[j];
+            my_g = csig[j] / den;
+        }
+    if (lane < K) {
+        topk_idx[(size_t)t * K + lane] = my_e;
+        topk_gate[(size_t)t * K + lane] = my_g;
+    }
+}
+
 // Exact routing of the queued tokens: all E logits by the FMA chain, then
 // the same top-K. Blocks first, first + stride, ... walk the queue (fixed by
 // the time this runs); every block exits once it is exhausted. Any block
@@ -757,68 +832,7 @@ __device__ __forceinline__ void exact_list_run(const bf16_t* __restrict__ x, con
             sig[e] = sigmoid_fp32(a);
         }
         __syncthreads();
-        if (threadIdx.x < kWave) {
-            const int per = (E + kWave - 1) / kWave;
-            float sg[kPerLane], key[kPerLane];
-#pragma unroll
-            for (int m = 0; m < kPerLane; ++m) {
-                const int e = lane + kWave * m;
-                const bool ok = m < per && e < E;
-                sg[m] = ok ? sig[e] : 0.0f;
-                key[m] = ok ? (bias ? sg[m] + bias[e] : sg[m]) : -INFINITY;
-            }
-            uint32_t taken = 0;
-            float csig[kMaxK];
-            int cidx[kMaxK];
-#pragma unroll
-            for (int j = 0; j < kMaxK; ++j) {
-                csig[j] = 0.0f;
-                cidx[j] = 0;
-                if (j >= K) continue;
-                float bk = -INFINITY;
-                int be = 0x7fffffff;
-                float bs = 0.0f;
-#pragma unroll
-                for (int m = 0; m < kPerLane; ++m) {
-                    const int e = lane + kWave * m;
-                    if (m < per && e < E && !((taken >> m) & 1u) && (key[m] > bk || (key[m] == bk && e < be))) {
-                        bk = key[m];
-                        be = e;
-                        bs = sg[m];
-                    }
-                }
-#pragma unroll
-                for (int off = kWave / 2; off > 0; off >>= 1) {
-                    const float ok = __shfl_xor(bk, off);
-                    const int oe = __shfl_xor(be, off);
-                    const float os = __shfl_xor(bs, off);
-                    if (ok > bk || (ok == bk && oe < be)) {
-                        bk = ok;
-                        be = oe;
-                        bs = os;
-                    }
-                }
-                if ((be & (kWave - 1)) == lane) taken |= 1u << (be / kWave);
-                csig[j] = bs;
-                cidx[j] = be;
-            }
-            float den = csig[0];
-#pragma unroll
-            for (int j = 1; j < kMaxK; ++j)
-                if (j < K) den = den + csig[j];
-            int my_e = 0;
-            float my_g = 0.0f;
-#pragma unroll
-            for (int j = 0; j < kMaxK; ++j)
-                if (j == lane && j < K) {
-                    my_e = cidx[j];
-                    my_g = csig[j] / den;
-                }
-            if (lane < K) {
-                topk_idx[(size_t)t * K + lane] = my_e;
-                topk_gate[(size_t)t * K + lane] = my_g;
-            }
-        }
+        if (threadIdx.x < kWave) exact_select_wave(sig, bias, E, K, t, lane, topk_idx, topk_gate);
         __syncthreads();
     }
 }
@@ -950,6 +964,371 @@ __global__ __launch_bounds__(kWave) void k_router_chain_direct(const bf16_t* __r
     chain_select<TPB, LPT, 1>(lds_dyn, tl, g, t, T, nc, K, on, ec, acc, bc, bias != nullptr, topk_idx, topk_gate);
 }
 
+// Small batches with K <= 8, at most 256 experts and d <= 4096: the whole
+// repair in one launch. A one-wave block takes 4 tokens, 16 lanes each (lane
+// g holding experts g PER .. g PER + PER - 1, as in the candidate kernel):
+//  - the weight-row norms come from the logits GEMM's per-part sums of
+//    squares (wsq [nsplit][ld]), the token norms from the token's x row,
+//    which the block stages in LDS widened to fp32 for the chains anyway;
+//  - the interval test of the candidate kernel, the candidate list in LDS;
+//  - lane g runs the exact chain of the token's candidate g (slot 16 tl + g).
+//    The weight rows of the block's 64 slots stream through LDS in chunks of
+//    128 columns, three buffers deep, by direct-to-LDS copies of 1 KB that
+//    each carry 256 contiguous bytes of four slots' rows (8 cache lines per
+//    copy, where a row per lane would touch 64). The chain is a run of
+//    dependent multiply-adds; the bf16 weights of the next 16 columns are
+//    widened between them, so that the adds never wait on the widening;
+//  - then the chain kernels' selection;
+//  - a token with more candidates than its 16 slots is routed by the block
+//    itself: every E logit by the same chain, recipe S and the exact top-K,
+//    so no queue crosses blocks.
+// Every multiply-add chain and selection is the same as on the other paths,
+// so indices and gates are identical bit for bit.
+constexpr int kSmallTpb = 4;      // tokens per one-wave block
+constexpr int kSmallChunk = 128;  // weight columns per LDS chunk
+constexpr int kSmallBufs = 3;     // chunk buffers (two chunks in flight)
+// One copy: 16-byte piece j (columns 8j .. 8j + 7 of the chunk) of slot
+// 4i + q at byte 16 (4 j + q); 64 bytes of padding after each copy put the 16
+// slots that a quarter wave reads at once on distinct LDS banks.
+constexpr int kSmallCopyBytes = kWave * 16 + 64;
+constexpr int kSmallBufBytes = (kWave / 4) * kSmallCopyBytes;
+constexpr int kSmallSelBytes = kSmallTpb * (16 * 12 + kMaxK * 8);
+static_assert(kSmallSelBytes + 256 * 4 <= kSmallBufs * kSmallBufBytes, "selection arrays fit the buffers");
+
+// 16 bytes from LDS at addr + OFF (inline assembly: the compiler neither sees
+// the read nor waits for it; the caller waits with lgkmcnt and pins the
+// result with tie()).
+template <int OFF>
+__device__ __forceinline__ u32x4_t lds_read16u_off(uint32_t addr) {
+    u32x4_t r;
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+    return r;
+}
+
+// Element j (0..15) of 16 bf16 held in two 16-byte registers, widened.
+__device__ __forceinline__ float bf16_elem(const u32x4_t (&w)[2], int j) {
+    const uint32_t bits = w[j / 8][(j / 2) % 4];
+    return __uint_as_float((j & 1) ? (bits & 0xffff0000u) : (bits << 16));
+}
+
+// Dynamic LDS of k_router_small: the 4 x rows (d + 4 floats each: the pad
+// spreads the 4 tokens' reads over the banks) and the chunk buffers, which
+// the selection's arrays and the overflow path's sigmoids reuse afterwards.
+// At d = 1536 this and the static arrays stay under half the LDS, so two
+// blocks share a CU (one image's 257 blocks all run at once).
+size_t router_small_lds_bytes(int d) {
+    return (size_t)kSmallTpb * (d + 4) * 4 + (size_t)kSmallBufs * kSmallBufBytes;
+}
+
+template <int PER>
+__global__ __launch_bounds__(kWave) void k_router_small(const float* __restrict__ s_fast, int nsplit,
+                                                      size_t sstride, int ld, const float* __restrict__ wsq,
+                                                      const bf16_t* __restrict__ x, const bf16_t* __restrict__ wr,
+                                                      const float* __restrict__ bias, int T, int d, int E, int K,
+                                                      float cst, int32_t* __restrict__ topk_idx,
+                                                      float* __restrict__ topk_gate) {
+    constexpr int LPA = 16, NS = 16, TPB = kSmallTpb, EM = LPA * PER;
+    static_assert(TPB * LPA == kWave, "one wave of 4 tokens");
+    static_assert(PER % 4 == 0 && 64 % PER == 0, "whole 16-byte loads inside a row of a multiple of 64");
+    extern __shared__ __attribute__((aligned(16))) uint8_t lds_dyn[];
+    __shared__ __attribute__((aligned(16))) float sb[EM];
+    __shared__ __attribute__((aligned(16))) float swn[EM];
+    __shared__ uint16_t scand[TPB][NS];
+    __shared__ int snc[TPB];  // candidates per token (more than NS: the block routes it in full)
+    const int lane = threadIdx.x;
+    const int g = lane % LPA, tl = lane / LPA;
+    const int t = blockIdx.x * TPB + tl;
+    const bool live = t < T;  // uniform within the token's lanes
+    const uint64_t grp = ((1ull << LPA) - 1ull) << (lane - g);
+    const int XS = d + 4;  // x row stride in LDS (floats)
+    float* xs = reinterpret_cast<float*>(lds_dyn);
+    uint8_t* wbuf = lds_dyn + (size_t)TPB * XS * 4;
+    uint8_t* sel = wbuf;                                        // after the chains
+    float* ssig = reinterpret_cast<float*>(wbuf + kSmallSelBytes);  // overflow path
+
+    // Every global load of the token phase is issued before the first use:
+    // the partial logits of the lane's experts, the parts' sums of squares of
+    // the weight rows and the x pieces (tokens past T read row T - 1, lanes
+    // past the logit row read column 0; neither is used).
+    const int e0 = g * PER;
+    float pv[8][PER];
+    {
+        const float* row = s_fast + (size_t)(live ? t : T - 1) * ld + (e0 < ld ? e0 : 0);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) load_row<PER>(row + (q < nsplit ? q * sstride : 0), pv[q]);
+    }
+    constexpr int EPL = EM / kWave > 0 ? EM / kWave : 1;
+    float part[EPL][8];
+#pragma unroll
+    for (int m = 0; m < EPL; ++m) {
+        const int e = lane + kWave * m;
+        const int ec = e < E ? e : 0;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) part[m][q] = wsq[(size_t)(q < nsplit ? q : 0) * ld + ec];
+    }
+    // x: sixteen 16-byte pieces per lane and round (2048 columns), the last
+    // round's pieces past d re-reading the row's last piece.
+    const bf16_t* xt = x + (size_t)(live ? t : T - 1) * d;
+    constexpr int XU = 16;
+    u32x4_t xr16[XU];
+#pragma unroll
+    for (int u = 0; u < XU; ++u) {
+        const int i = g * 8 + u * LPA * 8;
+        xr16[u] = *reinterpret_cast<const u32x4_t*>(xt + (i < d ? i : d - 8));
+    }
+
+    // Selection biases and weight-row norms: the parts' sums of squares added
+    // in part order and raised by 0.1 % as the norm kernel does (an upper
+    // bound is all the interval needs).
+#pragma unroll
+    for (int m = 0; m < EPL; ++m) {
+        const int e = lane + kWave * m;
+        float ss = part[m][0];
+#pragma unroll
+        for (int q = 1; q < 8; ++q) ss = q < nsplit ? ss + part[m][q] : ss;
+        if (e < E) {
+            swn[e] = sqrtf(ss) * 1.001f + 1e-30f;
+            sb[e] = bias ? bias[e] : 0.0f;
+        }
+    }
+
+    // x rows widened to fp32 in LDS, and the token's sum of squares from the
+    // same values.
+    float ssq[4] = {0.0f, 0.0f, 0.0f, 0.0f};  // four partial sums: no long dependent run
+    for (int i0 = g * 8; i0 < d; i0 += XU * LPA * 8) {
+        if (i0 != g * 8) {  // rounds past the first (d > 2048)
+#pragma unroll
+            for (int u = 0; u < XU; ++u) {
+                const int i = i0 + u * LPA * 8;
+                xr16[u] = *reinterpret_cast<const u32x4_t*>(xt + (i < d ? i : d - 8));
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < XU; ++u) {
+            const int i = i0 + u * LPA * 8;
+            if (i < d) {
+                const u32x4_t v = xr16[u];
+                const float f[8] = {__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u),
+                                    __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xffff0000u),
+                                    __uint_as_float(v.z << 16), __uint_as_float(v.z & 0xffff0000u),
+                                    __uint_as_float(v.w << 16), __uint_as_float(v.w & 0xffff0000u)};
+                *reinterpret_cast<float4*>(xs + tl * XS + i) = make_float4(f[0], f[1], f[2], f[3]);
+                *reinterpret_cast<float4*>(xs + tl * XS + i + 4) = make_float4(f[4], f[5], f[6], f[7]);
+#pragma unroll
+                for (int q = 0; q < 8; ++q) ssq[q % 4] = fmaf(f[q], f[q], ssq[q % 4]);
+            }
+        }
+    }
+    float ssx = (ssq[0] + ssq[1]) + (ssq[2] + ssq[3]);
+#pragma unroll
+    for (int off = LPA / 2; off > 0; off >>= 1) ssx += __shfl_xor(ssx, off);
+    const float xn = live ? sqrtf(ssx) * 1.001f + 1e-30f : 0.0f;
+
+    // Fast logits of the lane's experts: the K parts added in part order.
+    float sf[PER];
+#pragma unroll
+    for (int m = 0; m < PER; ++m) sf[m] = pv[0][m];
+#pragma unroll
+    for (int q = 1; q < 8; ++q)
+#pragma unroll
+        for (int m = 0; m < PER; ++m) sf[m] = q < nsplit ? sf[m] + pv[q][m] : sf[m];
+    __syncthreads();
+    // The interval test, as in the candidate kernel.
+    // The lane's biases and norms in 16-byte LDS reads (entries past E are
+    // read but not used), then every interval without a branch.
+    float bv[PER], wn[PER];
+#pragma unroll
+    for (int q = 0; q < PER / 4; ++q) {
+        const float4 b4 = *reinterpret_cast<const float4*>(sb + e0 + 4 * q);
+        const float4 n4 = *reinterpret_cast<const float4*>(swn + e0 + 4 * q);
+        bv[4 * q] = b4.x, bv[4 * q + 1] = b4.y, bv[4 * q + 2] = b4.z, bv[4 * q + 3] = b4.w;
+        wn[4 * q] = n4.x, wn[4 * q + 1] = n4.y, wn[4 * q + 2] = n4.z, wn[4 * q + 3] = n4.w;
+    }
+    float lo[PER], hi[PER];
+#pragma unroll
+    for (int m = 0; m < PER; ++m) {
+        const bool ok = live && e0 + m < E;
+        const float key = sigmoid_fast(sf[m]) + bv[m];
+        const float delta = 0.25f * (cst * xn * wn[m]) + 4e-6f + 1e-6f * fabsf(bv[m]);
+        lo[m] = ok ? key - delta : -INFINITY;
+        hi[m] = ok ? key + delta : -INFINITY;
+    }
+    float t1 = -INFINITY, t2 = -INFINITY, t3 = -INFINITY;
+#pragma unroll
+    for (int m = 0; m < PER; ++m) {
+        const float v = lo[m];
+        t3 = fmaxf(t3, fminf(t2, v));
+        t2 = fmaxf(t2, fminf(t1, v));
+        t1 = fmaxf(t1, v);
+    }
+    float L = -INFINITY;
+    int used = 0;
+    for (int j = 0; j < K; ++j) {
+        const float mine = used == 0 ? t1 : (used == 1 ? t2 : (used == 2 ? t3 : -INFINITY));
+        const float gmax = group_max<LPA>(mine);
+        const uint64_t holders = __ballot(used < 3 && mine == gmax) & grp;
+        if (holders && lane == __ffsll((unsigned long long)holders) - 1) ++used;
+        L = gmax;
+    }
+    // Candidates: lane g's in expert order after those of lanes 0 .. g - 1
+    // (an inclusive scan of the lanes' counts along the 16-lane DPP row).
+    uint32_t cbits = 0;
+#pragma unroll
+    for (int m = 0; m < PER; ++m) cbits |= (live && hi[m] >= L) ? (1u << m) : 0u;
+    const int cnt = __popc(cbits);
+    int incl = cnt;
+    incl += __builtin_amdgcn_update_dpp(0, incl, 0x111, 0xF, 0xF, false);  // row_shr:1
+    incl += __builtin_amdgcn_update_dpp(0, incl, 0x112, 0xF, 0xF, false);  // row_shr:2
+    incl += __builtin_amdgcn_update_dpp(0, incl, 0x114, 0xF, 0xF, false);  // row_shr:4
+    incl += __builtin_amdgcn_update_dpp(0, incl, 0x118, 0xF, 0xF, false);  // row_shr:8
+    const int nc = __builtin_amdgcn_update_dpp(0, incl, 0x15F, 0xF, 0xF, false);  // row_newbcast:15
+#pragma unroll
+    for (int m = 0; m < PER; ++m) {
+        const int pos = incl - cnt + __popc(cbits & ((1u << m) - 1u));
+        if (((cbits >> m) & 1u) && pos < NS) scand[tl][pos] = (uint16_t)(e0 + m);
+    }
+    if (g == 0) snc[tl] = nc;
+    __syncthreads();
+
+    // Exact chain of candidate g (slot 16 tl + g).
+    const int ncx = nc > NS ? 0 : nc;  // an overflowing token is routed below
+    const bool on[1] = {g < ncx};
+    const int ec[1] = {on[0] ? (int)scand[tl][g] : 0};
+    const float bc[1] = {(bias && on[0]) ? sb[ec[0]] : 0.0f};
+    float acc[1] = {0.0f};
+    if (__ballot(on[0]) != 0) {
+        // Copy sources: in copy i this lane carries 16 bytes of slot
+        // 4i + lane % 4, piece lane / 4 of the chunk's 256 bytes of that
+        // slot's row. Free slots copy row 0 (in bounds, never read); the rest
+        // of a ragged last chunk is never read either.
+        int ncs[TPB];
+#pragma unroll
+        for (int u = 0; u < TPB; ++u) ncs[u] = snc[u] > NS ? 0 : snc[u];
+        uint32_t roff[kWave / 4];
+#pragma unroll
+        for (int i = 0; i < kWave / 4; ++i) {
+            const int slot = 4 * i + (lane & 3);
+            const int su = slot / NS, sg = slot % NS;
+            const int e = sg < ncs[su] ? (int)scand[su][sg] : 0;
+            roff[i] = (uint32_t)e * (uint32_t)d * 2u + (uint32_t)(lane >> 2) * 16u;
+        }
+        const __amdgpu_buffer_rsrc_t rw = make_rsrc(wr, (uint32_t)((size_t)E * d * 2));
+        auto copy_chunk = [&](int c) {
+            uint8_t* dst = wbuf + (size_t)(c % kSmallBufs) * kSmallBufBytes;
+#pragma unroll
+            for (int i = 0; i < kWave / 4; ++i)
+                copy16_to_lds(rw, roff[i], (uint32_t)c * (kSmallChunk * 2), dst + i * kSmallCopyBytes);
+        };
+        // This lane's slot in buffer 0 (piece j at + 64 j) and its token's x row.
+        const uint32_t wa0 = lds_address(wbuf) + (uint32_t)(lane >> 2) * kSmallCopyBytes + (uint32_t)(lane & 3) * 16u;
+        const uint32_t xa0 = lds_address(reinterpret_cast<uint8_t*>(xs + tl * XS));
+        const int nch = (d + kSmallChunk - 1) / kSmallChunk;
+        float a = 0.0f;
+        // Register sets of three units in rotation (raw 16-byte reads) and the
+        // widened weights of two units.
+        u32x4_t wv[3][2] = {}, xv[3][4] = {};
+        float wf[2][16];
+        copy_chunk(0);
+        if (nch > 1) copy_chunk(1);
+        for (int c = 0; c < nch; ++c) {
+            // Chunk c is in LDS once at most one chunk's copies are in flight
+            // (a single wave: its own copies).
+            if (c + 1 < nch) wait_vmcnt<kWave / 4>(); else wait_vmcnt<0>();
+            // Chunk c - 1's buffer is free: every LDS read of it was awaited.
+            if (c + 2 < nch) copy_chunk(c + 2);
+            const uint32_t wa = wa0 + (uint32_t)(c % kSmallBufs) * kSmallBufBytes;
+            const uint32_t xa = xa0 + (uint32_t)c * (kSmallChunk * 4);
+            const int left = (d - c * kSmallChunk) / 16;
+            const int nu = left < kSmallChunk / 16 ? left : kSmallChunk / 16;  // units of 16 columns
+            auto issue = [&](auto KC) {
+                constexpr int k = decltype(KC)::value;
+                constexpr int r = k % 3;
+                wv[r][0] = lds_read16u_off<k * 128>(wa);
+                wv[r][1] = lds_read16u_off<k * 128 + 64>(wa);
+                xv[r][0] = lds_read16u_off<k * 64>(xa);
+                xv[r][1] = lds_read16u_off<k * 64 + 16>(xa);
+                xv[r][2] = lds_read16u_off<k * 64 + 32>(xa);
+                xv[r][3] = lds_read16u_off<k * 64 + 48>(xa);
+            };
+            auto settle = [&](int r) {
+                tie(wv[r][0]);
+                tie(wv[r][1]);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) tie(xv[r][q]);
+            };
+            issue(std::integral_constant<int, 0>{});
+            if (nu > 1) issue(std::integral_constant<int, 1>{});
+            if (nu > 1) wait_lgkmcnt<6>(); else wait_lgkmcnt<0>();
+            settle(0);
+#pragma unroll
+            for (int j = 0; j < 16; ++j) wf[0][j] = bf16_elem(wv[0], j);
+            static_for<kSmallChunk / 16>([&](auto KC) {
+                constexpr int k = decltype(KC)::value;
+                constexpr int r = k % 3, r1 = (k + 1) % 3;
+                if (k < nu) {
+                    wait_lgkmcnt<0>();  // unit k + 1's reads (the last ones issued)
+                    settle(r1);
+                    if constexpr (k + 2 < kSmallChunk / 16)
+                        if (k + 2 < nu) issue(std::integral_constant<int, k + 2>{});
+                    // Unit k's 16 multiply-adds in column order, unit k + 1's
+                    // weights widened in between.
+#pragma unroll
+                    for (int j = 0; j < 16; ++j) {
+                        a = fmaf(__uint_as_float(xv[r][j / 4][j % 4]), wf[k % 2][j], a);
+                        wf[(k + 1) % 2][j] = bf16_elem(wv[r1], j);
+                    }
+                }
+            });
+        }
+        acc[0] = a;
+    }
+    // The selection's arrays reuse the chunk buffers (no copy is in flight).
+    chain_select<TPB, LPA, 1>(sel, tl, g, t, T, ncx, K, on, ec, acc, bc, bias != nullptr, topk_idx, topk_gate);
+
+    // Overflowing tokens, one at a time: lane l runs the chains of experts
+    // l, l + 64, ... side by side (at most 4 for E <= 256), each the same fma
+    // sequence over i = 0..d-1 from +0, then recipe S and the exact top-K.
+    for (int u = 0; u < TPB; ++u) {
+        if (snc[u] <= NS) continue;  // uniform: one LDS value for the whole wave
+        const int tu = blockIdx.x * TPB + u;
+        const float* xr = xs + u * XS;
+        constexpr int EPL = EM / kWave > 0 ? EM / kWave : 1;
+        float av[EPL];
+        const bf16_t* we[EPL];
+#pragma unroll
+        for (int m = 0; m < EPL; ++m) {
+            av[m] = 0.0f;
+            const int e = lane + kWave * m;
+            we[m] = wr + (size_t)(e < E ? e : 0) * d;
+        }
+        for (int i = 0; i < d; i += 8) {
+            const float4 x0 = *reinterpret_cast<const float4*>(xr + i);
+            const float4 x1 = *reinterpret_cast<const float4*>(xr + i + 4);
+            const float xv8[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+            u32x4_t wq4[EPL];
+#pragma unroll
+            for (int m = 0; m < EPL; ++m) wq4[m] = *reinterpret_cast<const u32x4_t*>(we[m] + i);
+#pragma unroll
+            for (int m = 0; m < EPL; ++m) {
+                const uint32_t wq[4] = {wq4[m].x, wq4[m].y, wq4[m].z, wq4[m].w};
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    av[m] = fmaf(xv8[2 * q], __uint_as_float(wq[q] << 16), av[m]);
+                    av[m] = fmaf(xv8[2 * q + 1], __uint_as_float(wq[q] & 0xffff0000u), av[m]);
+                }
+            }
+        }
+#pragma unroll
+        for (int m = 0; m < EPL; ++m) {
+            const int e = lane + kWave * m;
+            if (e < E) ssig[e] = sigmoid_fp32(av[m]);
+        }
+        __syncthreads();
+        exact_select_wave(ssig, bias, E, K, tu, lane, topk_idx, topk_gate);
+        __syncthreads();
+    }
+}
+
 }  // namespace
 
 hipError_t launch_router_scores(const moe_desc_t& d, const void* x, const void* w_router,
@@ -987,19 +1366,41 @@ float router_fast_bound_constant(int d) {
 
 bool router_small_batch(const moe_desc_t& d) { return d.T < 256 * 64; }
 
+bool router_small_fused(const moe_desc_t& d) {
+    return router_small_batch(d) && d.K <= 8 && d.E <= 256 && d.d <= 4096;
+}
+
 hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, int ld, int nsplit, const void* x,
                                      const float* xnorm2, const void* w_router, const float* bias, float* wnorm,
-                                     float* wr32,
+                                     float* wr32, const float* wsq,
                                      uint16_t* cand, int32_t* ncand, int32_t* ovf_count, int32_t* ovf_list,
                                      int32_t* topk_idx, float* topk_gate, hipStream_t s) {
     const bf16_t* xb = static_cast<const bf16_t*>(x);
     const bf16_t* wb = static_cast<const bf16_t*>(w_router);
+    if (nsplit < 1 || nsplit > 8) return hipErrorInvalidValue;  // the candidate kernels add at most 8 parts
+    if (wsq) {  // one launch: norms, candidates, chains, selection and overflow
+        if (!router_small_fused(d)) return hipErrorInvalidValue;
+        const size_t shm = router_small_lds_bytes(d.d);
+        auto launch = [&](auto kern) -> hipError_t {
+            if (shm > 65536) {
+                const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
+                if (e != hipSuccess) return e;
+            }
+            hipLaunchKernelGGL(kern, dim3((d.T + 3) / 4), dim3(kWave), shm, s, s_fast, nsplit, (size_t)d.T * ld, ld,
+                               wsq, xb, wb, bias, d.T, d.d, d.E, d.K, router_fast_bound_constant(d.d), topk_idx,
+                               topk_gate);
+            return hipGetLastError();
+        };
+        if (d.E <= 64) return launch(k_router_small<4>);
+        if (d.E <= 128) return launch(k_router_small<8>);
+        return launch(k_router_small<16>);
+    }
     const bool small = router_small_batch(d);
     // Weight-row norms (the token norms are formed in the candidate kernel);
     // for small batches also the fp32 copy of the weights the chains read.
     hipLaunchKernelGGL(k_row_norms, dim3((d.E + 3) / 4), dim3(256), 0, s, wb, d.E, wnorm, nullptr, 0, nullptr, d.d,
                        ovf_count, small ? wr32 : nullptr);
-    if (nsplit < 1 || nsplit > 8) return hipErrorInvalidValue;  // the candidate kernel adds at most 8 parts
     const size_t sstride = (size_t)d.T * ld;
     const float cst = router_fast_bound_constant(d.d);
     const int ns = router_cand_slots(d.K);

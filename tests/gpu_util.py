@@ -65,6 +65,10 @@ class DeviceLayer:
     """Device copies of one layer's inputs plus a workspace."""
 
     def __init__(self, inp, T=None):
+        # The kernels read T rows of x through a raw pointer: T past the rows
+        # that exist would read outside the allocation.
+        if T is not None and not 0 <= T <= inp.x.shape[0]:
+            raise ValueError(f"T = {T} but the inputs hold {inp.x.shape[0]} token rows")
         self.inp = inp
         self.cfg = inp.cfg
         self.desc = desc_for(self.cfg, T)
