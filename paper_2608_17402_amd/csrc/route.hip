@@ -348,10 +348,11 @@ __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s
     const int t = blockIdx.x * (blockDim.x / LPA) + threadIdx.x / LPA;
     const bool live = t < T;  // uniform within the group: dead groups compute on -inf
     const uint64_t grp = (LPA == kWave ? ~0ull : ((1ull << LPA) - 1ull)) << (lane - g);
-    const uint64_t below = grp & ((1ull << lane) - 1ull);
 
     // Selection biases and weight-row norms of all experts, in LDS.
-    __shared__ float sb[kMaxE], swn[kMaxE];
+    static_assert(LPA * PER <= kMaxE, "the lanes' experts inside the arrays");
+    __shared__ __attribute__((aligned(16))) float sb[kMaxE];
+    __shared__ __attribute__((aligned(16))) float swn[kMaxE];
     for (int e = threadIdx.x; e < E; e += blockDim.x) {
         sb[e] = bias ? bias[e] : 0.0f;
         swn[e] = wnorm[e];
@@ -391,12 +392,12 @@ __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s
     // parts): the partial sums in part order (any order of the d products is
     // covered by the bound), with every part's loads issued before the first
     // add (parts past nsplit re-read part 0 and are not added).
+    // Dead tokens read row 0 and lanes past the logit row column 0 (neither
+    // is used), so the loads need no branch.
     const int e0 = g * PER;
     float sf[PER];
-#pragma unroll
-    for (int m = 0; m < PER; ++m) sf[m] = 0.0f;
-    if (live && e0 < ld) {
-        const float* row = s_fast + (size_t)t * ld + e0;
+    {
+        const float* row = s_fast + (size_t)(live ? t : 0) * ld + (e0 < ld ? e0 : 0);
         if constexpr (SPLIT) {
             float pv[8][PER];
 #pragma unroll
@@ -412,19 +413,24 @@ __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s
         }
     }
     __syncthreads();
+    // The lane's biases and norms in 16-byte LDS reads (entries past E are
+    // read but not used), then every interval without a branch.
+    float bv[PER], wn[PER];
+#pragma unroll
+    for (int q = 0; q < PER / 4; ++q) {
+        const float4 b4 = *reinterpret_cast<const float4*>(sb + e0 + 4 * q);
+        const float4 n4 = *reinterpret_cast<const float4*>(swn + e0 + 4 * q);
+        bv[4 * q] = b4.x, bv[4 * q + 1] = b4.y, bv[4 * q + 2] = b4.z, bv[4 * q + 3] = b4.w;
+        wn[4 * q] = n4.x, wn[4 * q + 1] = n4.y, wn[4 * q + 2] = n4.z, wn[4 * q + 3] = n4.w;
+    }
     float lo[PER], hi[PER];
 #pragma unroll
     for (int m = 0; m < PER; ++m) {
-        const int e = e0 + m;
-        lo[m] = -INFINITY;
-        hi[m] = -INFINITY;
-        if (live && e < E) {
-            const float b = sb[e];
-            const float key = sigmoid_fast(sf[m]) + b;
-            const float delta = 0.25f * (cst * xn * swn[e]) + 4e-6f + 1e-6f * fabsf(b);
-            lo[m] = key - delta;
-            hi[m] = key + delta;
-        }
+        const bool ok = live && e0 + m < E;
+        const float key = sigmoid_fast(sf[m]) + bv[m];
+        const float delta = 0.25f * (cst * xn * wn[m]) + 4e-6f + 1e-6f * fabsf(bv[m]);
+        lo[m] = ok ? key - delta : -INFINITY;
+        hi[m] = ok ? key + delta : -INFINITY;
     }
     // L: the K-th largest of the lanes' three largest lower ends. These are a
     // subset of all lower ends, so L is at most the K-th largest lower end and
@@ -448,15 +454,36 @@ __global__ __launch_bounds__(256) void k_router_cand(const float* __restrict__ s
         L = gmax;
     }
     int nc = 0;
+    if constexpr (LPA == 16) {
+        // Lane g's candidates in expert order after those of lanes 0 .. g - 1
+        // (an inclusive scan of the lanes' counts along the 16-lane DPP row).
+        uint32_t cbits = 0;
 #pragma unroll
-    for (int m = 0; m < PER; ++m) {
-        const bool c = live && hi[m] >= L;
-        const uint64_t bal = __ballot(c) & grp;
-        if (c) {
-            const int pos = nc + __popcll(bal & below);
-            if (pos < NS) cand[(size_t)t * NS + pos] = (uint16_t)(e0 + m);
+        for (int m = 0; m < PER; ++m) cbits |= (live && hi[m] >= L) ? (1u << m) : 0u;
+        const int cnt = __popc(cbits);
+        int incl = cnt;
+        incl += __builtin_amdgcn_update_dpp(0, incl, 0x111, 0xF, 0xF, false);  // row_shr:1
+        incl += __builtin_amdgcn_update_dpp(0, incl, 0x112, 0xF, 0xF, false);  // row_shr:2
+        incl += __builtin_amdgcn_update_dpp(0, incl, 0x114, 0xF, 0xF, false);  // row_shr:4
+        incl += __builtin_amdgcn_update_dpp(0, incl, 0x118, 0xF, 0xF, false);  // row_shr:8
+        nc = __builtin_amdgcn_update_dpp(0, incl, 0x15F, 0xF, 0xF, false);     // row_newbcast:15
+#pragma unroll
+        for (int m = 0; m < PER; ++m) {
+            const int pos = incl - cnt + __popc(cbits & ((1u << m) - 1u));
+            if (((cbits >> m) & 1u) && pos < NS) cand[(size_t)t * NS + pos] = (uint16_t)(e0 + m);
         }
-        nc += __popcll(bal);
+    } else {
+        const uint64_t below = grp & ((1ull << lane) - 1ull);
+#pragma unroll
+        for (int m = 0; m < PER; ++m) {
+            const bool c = live && hi[m] >= L;
+            const uint64_t bal = __ballot(c) & grp;
+            if (c) {
+                const int pos = nc + __popcll(bal & below);
+                if (pos < NS) cand[(size_t)t * NS + pos] = (uint16_t)(e0 + m);
+            }
+            nc += __popcll(bal);
+        }
     }
     if (live && g == 0) {
         if (nc > NS) {
@@ -546,6 +573,114 @@ __device__ __forceinline__ void chain_select(uint8_t* lds, int tl, int g, int t,
     }
 }
 
+// Exact top-K of token t from its E sigmoids (sig, in LDS) and gates, by one
+// wave: each of the K rounds takes the wave-wide best key (descending, lower
+// expert index first on equal keys) with a butterfly of cross-lane exchanges.
+__device__ __forceinline__ void exact_select_wave(const float* sig, const float* __restrict__ bias, int E, int K,
+                                                  int t, int lane, int32_t* __restrict__ topk_idx,
+                                                  float* __restrict__ topk_gate) {
+    const int per = (E + kWave - 1) / kWave;
+    float sg[kPerLane], key[kPerLane];
+#pragma unroll
+    for (int m = 0; m < kPerLane; ++m) {
+        const int e = lane + kWave * m;
+        const bool ok = m < per && e < E;
+        sg[m] = ok ? sig[e] : 0.0f;
+        key[m] = ok ? (bias ? sg[m] + bias[e] : sg[m]) : -INFINITY;
+    }
+    uint32_t taken = 0;
+    float csig[kMaxK];
+    int cidx[kMaxK];
+#pragma unroll
+    for (int j = 0; j < kMaxK; ++j) {
+        csig[j] = 0.0f;
+        cidx[j] = 0;
+        if (j >= K) continue;
+        float bk = -INFINITY;
+        int be = 0x7fffffff;
+        float bs = 0.0f;
+#pragma unroll
+        for (int m = 0; m < kPerLane; ++m) {
+            const int e = lane + kWave * m;
+            if (m < per && e < E && !((taken >> m) & 1u) && (key[m] > bk || (key[m] == bk && e < be))) {
+                bk = key[m];
+                be = e;
+                bs = sg[m];
+            }
+        }
+#pragma unroll
+        for (int off = kWave / 2; off > 0; off >>= 1) {
+            const float ok = __shfl_xor(bk, off);
+            const int oe = __shfl_xor(be, off);
+            const float os = __shfl_xor(bs, off);
+            if (ok > bk || (ok == bk && oe < be)) {
+                bk = ok;
+                be = oe;
+                bs = os;
+            }
+        }
+        if ((be & (kWave - 1)) == lane) taken |= 1u << (be / kWave);
+        csig[j] = bs;
+        cidx[j] = be;
+    }
+    float den = csig[0];
+#pragma unroll
+    for (int j = 1; j < kMaxK; ++j)
+        if (j < K) den = den + csig[j];
+    int my_e = 0;
+    float my_g = 0.0f;
+#pragma unroll
+    for (int j = 0; j < kMaxK; ++j)
+        if (j == lane && j < K) {
+            my_e = cidx[j];
+            my_g = csig[j] / den;
+        }
+    if (lane < K) {
+        topk_idx[(size_t)t * K + lane] = my_e;
+        topk_gate[(size_t)t * K + lane] = my_g;
+    }
+}
+
+// Exact routing of the queued tokens: all E logits by the FMA chain, then
+// the same top-K. Blocks first, first + stride, ... walk the queue (fixed by
+// the time this runs); every block exits once it is exhausted. Any block
+// size that is a multiple of the wave works (the selection uses wave 0).
+__device__ __forceinline__ void exact_list_run(const bf16_t* __restrict__ x, const bf16_t* __restrict__ wr,
+                               const float* __restrict__ bias, int d, int E, int K,
+                               const int32_t* __restrict__ ovf_count, const int32_t* __restrict__ ovf_list,
+                               int32_t* __restrict__ topk_idx, float* __restrict__ topk_gate, int first,
+                               int stride) {
+    __shared__ float sig[kMaxE];
+    const int n = *ovf_count;
+    const int lane = threadIdx.x & (kWave - 1);
+    for (int it = first; it < n; it += stride) {
+        const int t = ovf_list[it];
+        const bf16_t* xt = x + (size_t)t * d;
+        for (int e = threadIdx.x; e < E; e += blockDim.x) {
+            const bf16_t* we = wr + (size_t)e * d;
+            // The same fma sequence over i = 0..d-1; the loads of 32 columns
+            // are issued before their multiply-adds (d is a multiple of 64).
+            float a = 0.0f;
+            for (int i = 0; i < d; i += 32) {
+                float xv[4][8], wv[4][8];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    load8(xt + i + 8 * q, xv[q]);
+                    load8(we + i + 8 * q, wv[q]);
+                }
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) a = fmaf(xv[q][u], wv[q][u], a);
+            }
+            sig[e] = sigmoid_fp32(a);
+        }
+        __syncthreads();
+        if (threadIdx.x < kWave) exact_select_wave(sig, bias, E, K, t, lane, topk_idx, topk_gate);
+        __syncthreads();
+    }
+}
+
 // Exact logits of the candidates, recipe S, exact top-K and gates. LPT lanes
 // per token, each running CPL candidate chains (slots g, g + LPT, ...) side by
 // side: one fused multiply-add chain per candidate over the model width, in
@@ -561,7 +696,17 @@ __global__ __launch_bounds__(TPB* LPT) void k_router_chain(const bf16_t* __restr
                                                          const uint16_t* __restrict__ cand,
                                                          const int32_t* __restrict__ ncand, int T, int d, int E,
                                                          int K, int32_t* __restrict__ topk_idx,
-                                                         float* __restrict__ topk_gate) {
+                                                         float* __restrict__ topk_gate, int chain_blocks,
+                                                         const int32_t* __restrict__ ovf_count,
+                                                         const int32_t* __restrict__ ovf_list) {
+    // Blocks from chain_blocks on route the tokens of the overflow queue (all
+    // of it is written: the candidate kernel has finished); with an empty
+    // queue they exit at once.
+    if ((int)blockIdx.x >= chain_blocks) {
+        exact_list_run(x, wr, bias, d, E, K, ovf_count, ovf_list, topk_idx, topk_gate,
+                       (int)blockIdx.x - chain_blocks, (int)gridDim.x - chain_blocks);
+        return;
+    }
     constexpr int NT = TPB * LPT;
     constexpr int NS = LPT * CPL;
     constexpr int ROW = DC + 8;             // bf16 per LDS row (16 bytes of padding)
@@ -727,125 +872,6 @@ __global__ __launch_bounds__(TPB* LPT) void k_router_chain(const bf16_t* __restr
 
     // Selection (the ring is free after the last barrier).
     chain_select<TPB, LPT, CPL>(lds, tl, g, t, T, nc, K, on, ec, acc, bc, bias != nullptr, topk_idx, topk_gate);
-}
-
-// Exact top-K of token t from its E sigmoids (sig, in LDS) and gates, by one
-// wave: each of the K rounds takes the wave-wide best key (descending, lower
-// expert index first on equal keys) with a butterfly of cross-lane exchanges.
-__device__ __forceinline__ void exact_select_wave(const float* sig, const float* __restrict__ bias, int E, int K,
-                                                  int t, int lane, int32_t* __restrict__ topk_idx,
-                                                  float* __restrict__ topk_gate) {
-    const int per = (E + kWave - 1) / kWave;
-    float sg[kPerLane], key[kPerLane];
-#pragma unroll
-    for (int m = 0; m < kPerLane; ++m) {
-        const int e = lane + kWave * m;
-        const bool ok = m < per && e < E;
-        sg[m] = ok ? sig[e] : 0.0f;
-        key[m] = ok ? (bias ? sg[m] + bias[e] : sg[m]) : -INFINITY;
-    }
-    uint32_t taken = 0;
-    float csig[kMaxK];
-    int cidx[kMaxK];
-#pragma unroll
-    for (int j = 0; j < kMaxK; ++j) {
-        csig[j] = 0.0f;
-        cidx[j] = 0;
-        if (j >= K) continue;
-        float bk = -INFINITY;
-        int be = 0x7fffffff;
-        float bs = 0.0f;
-#pragma unroll
-        for (int m = 0; m < kPerLane; ++m) {
-            const int e = lane + kWave * m;
-            if (m < per && e < E && !((taken >> m) & 1u) && (key[m] > bk || (key[m] == bk && e < be))) {
-                bk = key[m];
-                be = e;
-                bs = sg[m];
-            }
-        }
-#pragma unroll
-        for (int off = kWave / 2; off > 0; off >>= 1) {
-            const float ok = __shfl_xor(bk, off);
-            const int oe = __shfl_xor(be, off);
-            const float os = __shfl_xor(bs, off);
-            if (ok > bk || (ok == bk && oe < be)) {
-                bk = ok;
-                be = oe;
-                bs = os;
-            }
-        }
-        if ((be & (kWave - 1)) == lane) taken |= 1u << (be / kWave);
-        csig[j] = bs;
-        cidx[j] = be;
-    }
-    float den = csig[0];
-#pragma unroll
-    for (int j = 1; j < kMaxK; ++j)
-        if (j < K) den = den + csig[j];
-    int my_e = 0;
-    float my_g = 0.0f;
-#pragma unroll
-    for (int j = 0; j < kMaxK; ++j)
-        if (j == lane && j < K) {
-            my_e = cidx[j];
-            my_g = csig[j] / den;
-        }
-    if (lane < K) {
-        topk_idx[(size_t)t * K + lane] = my_e;
-        topk_gate[(size_t)t * K + lane] = my_g;
-    }
-}
-
-// Exact routing of the queued tokens: all E logits by the FMA chain, then
-// the same top-K. Blocks first, first + stride, ... walk the queue (fixed by
-// the time this runs); every block exits once it is exhausted. Any block
-// size that is a multiple of the wave works (the selection uses wave 0).
-__device__ __forceinline__ void exact_list_run(const bf16_t* __restrict__ x, const bf16_t* __restrict__ wr,
-                               const float* __restrict__ bias, int d, int E, int K,
-                               const int32_t* __restrict__ ovf_count, const int32_t* __restrict__ ovf_list,
-                               int32_t* __restrict__ topk_idx, float* __restrict__ topk_gate, int first,
-                               int stride) {
-    __shared__ float sig[kMaxE];
-    const int n = *ovf_count;
-    const int lane = threadIdx.x & (kWave - 1);
-    for (int it = first; it < n; it += stride) {
-        const int t = ovf_list[it];
-        const bf16_t* xt = x + (size_t)t * d;
-        for (int e = threadIdx.x; e < E; e += blockDim.x) {
-            const bf16_t* we = wr + (size_t)e * d;
-            // The same fma sequence over i = 0..d-1; the loads of 32 columns
-            // are issued before their multiply-adds (d is a multiple of 64).
-            float a = 0.0f;
-            for (int i = 0; i < d; i += 32) {
-                float xv[4][8], wv[4][8];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    load8(xt + i + 8 * q, xv[q]);
-                    load8(we + i + 8 * q, wv[q]);
-                }
-#pragma unroll
-                for (int q = 0; q < 4; ++q)
-#pragma unroll
-                    for (int u = 0; u < 8; ++u) a = fmaf(xv[q][u], wv[q][u], a);
-            }
-            sig[e] = sigmoid_fp32(a);
-        }
-        __syncthreads();
-        if (threadIdx.x < kWave) exact_select_wave(sig, bias, E, K, t, lane, topk_idx, topk_gate);
-        __syncthreads();
-    }
-}
-
-
-__global__ __launch_bounds__(256) void k_router_exact_list(const bf16_t* __restrict__ x,
-                                                          const bf16_t* __restrict__ wr,
-                                                          const float* __restrict__ bias, int d, int E, int K,
-                                                          const int32_t* __restrict__ ovf_count,
-                                                          const int32_t* __restrict__ ovf_list,
-                                                          int32_t* __restrict__ topk_idx,
-                                                          float* __restrict__ topk_gate) {
-    exact_list_run(x, wr, bias, d, E, K, ovf_count, ovf_list, topk_idx, topk_gate, blockIdx.x, gridDim.x);
 }
 
 // Exact logits for small batches, where streaming every expert's weights
@@ -1424,8 +1450,9 @@ hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, i
     // still gives a block per CU, then 64 tokens per block, then (small
     // batches) one wave per 4 (or 2) tokens reading weights directly.
 #define MOE_CHAIN(TPBv, LPTv, CPLv, EMv, DCv)                                                               \
-    hipLaunchKernelGGL((k_router_chain<TPBv, LPTv, CPLv, EMv, DCv>), dim3((d.T + TPBv - 1) / TPBv),          \
-                       dim3(TPBv * LPTv), 0, s, xb, wb, bias, cand, ncand, d.T, d.d, d.E, d.K, topk_idx, topk_gate)
+    hipLaunchKernelGGL((k_router_chain<TPBv, LPTv, CPLv, EMv, DCv>), dim3((d.T + TPBv - 1) / TPBv + 64),     \
+                       dim3(TPBv * LPTv), 0, s, xb, wb, bias, cand, ncand, d.T, d.d, d.E, d.K, topk_idx, topk_gate, \
+                       (d.T + TPBv - 1) / TPBv, ovf_count, ovf_list)
 #define MOE_CHAIN_E(TPBv, LPTv, CPLv, DCv)                                                                     \
     do {                                                                                                    \
         if (d.E <= 64) MOE_CHAIN(TPBv, LPTv, CPLv, 64, DCv);                                                \
@@ -1460,8 +1487,6 @@ hipError_t launch_router_fast_finish(const moe_desc_t& d, const float* s_fast, i
     }
 #undef MOE_CHAIN_E
 #undef MOE_CHAIN
-    hipLaunchKernelGGL(k_router_exact_list, dim3(64), dim3(256), 0, s, xb, wb, bias, d.d, d.E, d.K, ovf_count,
-                       ovf_list, topk_idx, topk_gate);
     return hipGetLastError();
 }
 
