@@ -853,14 +853,11 @@ __global__ __launch_bounds__(TPB* LPT) void k_router_chain(const bf16_t* __restr
                 if (tid + NT * i < WP && e < E) wrg[i] = *reinterpret_cast<const u32x4_t*>(wr + (size_t)e * d + k1 + c);
             }
         }
-        static_assert(CPL == 4, "chain counts handled below");
-        switch (nmax) {
-            case 4: chunk(std::integral_constant<int, 4>{}, buf); break;
-            case 3: chunk(std::integral_constant<int, 3>{}, buf); break;
-            case 2: chunk(std::integral_constant<int, 2>{}, buf); break;
-            case 1: chunk(std::integral_constant<int, 1>{}, buf); break;
-            default: break;
-        }
+        // The wave's chain count (uniform) picks an unrolled chunk.
+        static_for<CPL>([&](auto IC) {
+            constexpr int n = decltype(IC)::value + 1;
+            if (nmax == n) chunk(std::integral_constant<int, n>{}, buf);
+        });
         if (ch + 1 < nch) {
             stash(buf ^ 1);
 #pragma unroll

@@ -65,6 +65,31 @@ def test_route_exact_flag_agrees(small):
     assert np.array_equal(host(idx), ref_idx) and np.array_equal(host(gate), ref_gate)
 
 
+@pytest.mark.parametrize("T,d,E,K", [(1, 64, 8, 2), (130, 2048, 256, 8), (77, 4096, 200, 6), (300, 4096, 64, 8),
+                                     (513, 1344, 128, 1)])
+def test_route_small_batch_widths(T, d, E, K):
+    # Small batches route in one launch after the logits GEMM, the weight
+    # rows streaming through LDS in 128-column chunks (d = 1344 ends on a
+    # 64-column chunk); up to d = 4096 the x rows and three chunk buffers
+    # share the LDS. Bit-exact against the oracle and the all-exact path.
+    from workloads import bf16_bits_to_f32, f32_to_bf16_bits
+
+    rng = np.random.default_rng(T * 7 + d + E + K)
+    x = f32_to_bf16_bits(rng.standard_normal((T, d)).astype(np.float32))
+    wr = f32_to_bf16_bits((rng.standard_normal((E, d)) * 0.02).astype(np.float32))
+    bias = rng.uniform(-0.02, 0.02, E).astype(np.float32)
+    ref_idx, ref_gate = oracle.route(bf16_bits_to_f32(x), bf16_bits_to_f32(wr), bias, K)
+    for flags in (0, binding.MOE_FLAG_EXACT_ROUTER):
+        desc = binding.make_desc(T, d, E, K, 64, flags=flags)
+        ws = binding.alloc_workspace(desc)
+        idx = torch.empty(T, K, dtype=torch.int32, device="cuda")
+        gate = torch.empty(T, K, dtype=torch.float32, device="cuda")
+        binding.moe_route(desc, dev(x), dev(wr), dev(bias), idx, gate, ws)
+        torch.cuda.synchronize()
+        assert np.array_equal(host(idx), ref_idx), flags
+        assert np.array_equal(host(gate), ref_gate), flags
+
+
 @pytest.mark.parametrize("dup", [1, 16, 128])
 def test_route_near_ties_take_exact_fallback(dup):
     # Groups of `dup` identical router rows tie exactly for every token; with
