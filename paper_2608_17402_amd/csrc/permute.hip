@@ -8,7 +8,8 @@
 //                 slot order and ranks equal experts inside a round with
 //                 ballots, so slots of one expert keep ascending slot order.
 // Plus k_build_tiles, which cuts every expert's segment into M-tiles for the
-// grouped GEMMs (the device-side tile list that replaces a host round trip).
+// grouped GEMMs (the device-side tile list that replaces a host round trip),
+// and k_permute_small, all of it in one block for small batches.
 #include "moe_internal.h"
 
 namespace moe {
@@ -234,6 +235,78 @@ __global__ __launch_bounds__(1024) void k_scatter(const int32_t* __restrict__ id
     }
 }
 
+// Small batches (up to kPermuteOneBlock slots): the three passes in one
+// 1024-thread block, so the permute is one launch. Each of the 16 waves takes
+// a sixteenth of the slots in slot order: its expert histogram (LDS atomics),
+// then per expert the waves' bases in wave order, the counts, the exclusive
+// scan over experts (offsets), the stable scatter as in k_scatter, and the
+// tile table as in k_scan.
+constexpr int64_t kPermuteOneBlock = 65536;
+
+__global__ __launch_bounds__(1024) void k_permute_small(const int32_t* __restrict__ idx, int64_t n_slots, int E,
+                                                        int nbits, int32_t* __restrict__ counts,
+                                                        int32_t* __restrict__ offsets,
+                                                        int32_t* __restrict__ sorted_slots, int bm, int max_tiles,
+                                                        TileDesc* __restrict__ tiles, int32_t* __restrict__ n_tiles) {
+    constexpr int kWaves = 16;
+    __shared__ int base[kWaves][kMaxE];
+    __shared__ int tmp[32];
+    __shared__ int offl[kMaxE + 1];
+    __shared__ int start[kMaxE + 1];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int64_t sub = (n_slots + kWaves - 1) / kWaves;
+    const int64_t ws = min(n_slots, (int64_t)wave * sub);
+    const int64_t we = min(n_slots, ws + sub);
+
+    for (int i = threadIdx.x; i < kWaves * kMaxE; i += blockDim.x) (&base[0][0])[i] = 0;
+    __syncthreads();
+    for (int64_t n = ws + lane; n < we; n += kWave) {
+        const int e = idx[n];
+        if ((unsigned)e < (unsigned)E) atomicAdd(&base[wave][e], 1);  // ids outside [0, E) are dropped
+    }
+    __syncthreads();
+    // Per expert: each wave's start within the expert, and the expert's count.
+    int cnt = 0;
+    if ((int)threadIdx.x < E) {
+        const int e = threadIdx.x;
+        for (int w = 0; w < kWaves; ++w) {
+            const int c = base[w][e];
+            base[w][e] = cnt;
+            cnt += c;
+        }
+    }
+    int total;
+    const int excl = block_exclusive_scan_1024((int)threadIdx.x < E ? cnt : 0, tmp, &total);
+    if ((int)threadIdx.x < E) {
+        counts[threadIdx.x] = cnt;
+        offsets[threadIdx.x] = excl;
+        offl[threadIdx.x] = excl;
+    }
+    if (threadIdx.x == 0) {
+        offsets[E] = total;
+        offl[E] = total;
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < kWaves * E; i += blockDim.x) base[i / E][i % E] += offl[i % E];
+    __syncthreads();
+    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
+    for (int64_t r0 = ws; r0 < we; r0 += kWave) {
+        const int64_t n = r0 + lane;
+        const int e_raw = n < we ? idx[n] : -1;
+        const bool valid = (unsigned)e_raw < (unsigned)E;
+        const int e = valid ? e_raw : 0;
+        const uint64_t peers = match_peers(e, valid, nbits);
+        if (valid) {
+            const int rank = __popcll(peers & lt);
+            const int pos = base[wave][e] + rank;
+            sorted_slots[pos] = (int32_t)n;
+            if (rank == 0) base[wave][e] = pos + __popcll(peers);
+        }
+    }
+    if (tiles) build_tiles_block(E, bm, max_tiles, offl, tiles, n_tiles, start, tmp);
+}
+
 // M-tiles of height bm over every expert's segment, in expert order.
 __global__ __launch_bounds__(1024) void k_build_tiles(int E, int bm, int max_tiles,
                                                      const int32_t* __restrict__ offsets,
@@ -254,6 +327,11 @@ hipError_t launch_permute(const moe_desc_t& d, const int32_t* topk_idx, int32_t*
     const int64_t chunk = (n_slots + n_blocks - 1) / n_blocks;
     int nbits = 0;
     while ((1 << nbits) < d.E) ++nbits;
+    if (n_slots <= kPermuteOneBlock) {
+        hipLaunchKernelGGL(k_permute_small, dim3(1), dim3(1024), 0, s, topk_idx, n_slots, d.E, nbits, counts, offsets,
+                           sorted_slots, bm, max_tiles, tiles, n_tiles);
+        return hipGetLastError();
+    }
     hipLaunchKernelGGL(k_hist, dim3(n_blocks), dim3(1024), 0, s, topk_idx, n_slots, d.E, chunk, blockhist);
     hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, s, blockhist, n_blocks, d.E, counts, offsets, bm, max_tiles,
                        tiles, n_tiles);
