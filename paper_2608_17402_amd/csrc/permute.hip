@@ -9,7 +9,8 @@
 //                 ballots, so slots of one expert keep ascending slot order.
 // Plus k_build_tiles, which cuts every expert's segment into M-tiles for the
 // grouped GEMMs (the device-side tile list that replaces a host round trip),
-// and k_permute_small, all of it in one block for small batches.
+// and k_permute_small, all of it in one block for small batches (up to 16384
+// slots).
 #include "moe_internal.h"
 
 namespace moe {
@@ -237,11 +238,13 @@ __global__ __launch_bounds__(1024) void k_scatter(const int32_t* __restrict__ id
 
 // Small batches (up to kPermuteOneBlock slots): the three passes in one
 // 1024-thread block, so the permute is one launch. Each of the 16 waves takes
-// a sixteenth of the slots in slot order: its expert histogram (LDS atomics),
+// a sixteenth of the slots in slot order, all of its indices loaded at once
+// (up to 16 per lane, kept in registers): its expert histogram (LDS atomics),
 // then per expert the waves' bases in wave order, the counts, the exclusive
 // scan over experts (offsets), the stable scatter as in k_scatter, and the
 // tile table as in k_scan.
-constexpr int64_t kPermuteOneBlock = 65536;
+constexpr int kPermuteRounds = 16;  // 64-slot rounds per wave
+constexpr int64_t kPermuteOneBlock = 16 * kWave * kPermuteRounds;
 
 __global__ __launch_bounds__(1024) void k_permute_small(const int32_t* __restrict__ idx, int64_t n_slots, int E,
                                                         int nbits, int32_t* __restrict__ counts,
@@ -255,16 +258,21 @@ __global__ __launch_bounds__(1024) void k_permute_small(const int32_t* __restric
     __shared__ int start[kMaxE + 1];
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
-    const int64_t sub = (n_slots + kWaves - 1) / kWaves;
-    const int64_t ws = min(n_slots, (int64_t)wave * sub);
-    const int64_t we = min(n_slots, ws + sub);
+    const int sub = (int)((n_slots + kWaves - 1) / kWaves);  // <= kWave * kPermuteRounds
+    const int ws = (int)min(n_slots, (int64_t)wave * sub);
+    const int we = (int)min(n_slots, (int64_t)ws + sub);
 
+    int ev[kPermuteRounds];  // expert of slot ws + 64 r + lane, or -1
+#pragma unroll
+    for (int r = 0; r < kPermuteRounds; ++r) {
+        const int n = ws + kWave * r + lane;
+        ev[r] = n < we ? idx[n] : -1;
+    }
     for (int i = threadIdx.x; i < kWaves * kMaxE; i += blockDim.x) (&base[0][0])[i] = 0;
     __syncthreads();
-    for (int64_t n = ws + lane; n < we; n += kWave) {
-        const int e = idx[n];
-        if ((unsigned)e < (unsigned)E) atomicAdd(&base[wave][e], 1);  // ids outside [0, E) are dropped
-    }
+#pragma unroll
+    for (int r = 0; r < kPermuteRounds; ++r)
+        if ((unsigned)ev[r] < (unsigned)E) atomicAdd(&base[wave][ev[r]], 1);  // ids outside [0, E) are dropped
     __syncthreads();
     // Per expert: each wave's start within the expert, and the expert's count.
     int cnt = 0;
@@ -291,11 +299,12 @@ __global__ __launch_bounds__(1024) void k_permute_small(const int32_t* __restric
     for (int i = threadIdx.x; i < kWaves * E; i += blockDim.x) base[i / E][i % E] += offl[i % E];
     __syncthreads();
     const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
-    for (int64_t r0 = ws; r0 < we; r0 += kWave) {
-        const int64_t n = r0 + lane;
-        const int e_raw = n < we ? idx[n] : -1;
-        const bool valid = (unsigned)e_raw < (unsigned)E;
-        const int e = valid ? e_raw : 0;
+#pragma unroll
+    for (int r = 0; r < kPermuteRounds; ++r) {
+        if (ws + kWave * r >= we) break;  // uniform: the wave's rounds are done
+        const int n = ws + kWave * r + lane;
+        const bool valid = (unsigned)ev[r] < (unsigned)E;
+        const int e = valid ? ev[r] : 0;
         const uint64_t peers = match_peers(e, valid, nbits);
         if (valid) {
             const int rank = __popcll(peers & lt);
