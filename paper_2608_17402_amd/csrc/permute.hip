@@ -262,12 +262,18 @@ __global__ __launch_bounds__(1024) void k_permute_small(const int32_t* __restric
     const int ws = (int)min(n_slots, (int64_t)wave * sub);
     const int we = (int)min(n_slots, (int64_t)ws + sub);
 
-    int ev[kPermuteRounds];  // expert of slot ws + 64 r + lane, or -1
+    // Expert of slot ws + 64 r + lane, or -1 past the wave's range. The loads
+    // are unconditional (past the range they re-read the last slot), so all
+    // sixteen are in flight together.
+    int ev[kPermuteRounds];
 #pragma unroll
     for (int r = 0; r < kPermuteRounds; ++r) {
         const int n = ws + kWave * r + lane;
-        ev[r] = n < we ? idx[n] : -1;
+        ev[r] = idx[n < n_slots ? n : n_slots - 1];
     }
+#pragma unroll
+    for (int r = 0; r < kPermuteRounds; ++r)
+        if (ws + kWave * r + lane >= we) ev[r] = -1;
     for (int i = threadIdx.x; i < kWaves * kMaxE; i += blockDim.x) (&base[0][0])[i] = 0;
     __syncthreads();
 #pragma unroll
@@ -302,14 +308,13 @@ __global__ __launch_bounds__(1024) void k_permute_small(const int32_t* __restric
 #pragma unroll
     for (int r = 0; r < kPermuteRounds; ++r) {
         if (ws + kWave * r >= we) break;  // uniform: the wave's rounds are done
-        const int n = ws + kWave * r + lane;
         const bool valid = (unsigned)ev[r] < (unsigned)E;
         const int e = valid ? ev[r] : 0;
         const uint64_t peers = match_peers(e, valid, nbits);
         if (valid) {
             const int rank = __popcll(peers & lt);
             const int pos = base[wave][e] + rank;
-            sorted_slots[pos] = (int32_t)n;
+            sorted_slots[pos] = (int32_t)(ws + kWave * r + lane);
             if (rank == 0) base[wave][e] = pos + __popcll(peers);
         }
     }
