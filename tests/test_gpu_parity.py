@@ -66,12 +66,14 @@ def test_route_exact_flag_agrees(small):
 
 
 @pytest.mark.parametrize("T,d,E,K", [(1, 64, 8, 2), (130, 2048, 256, 8), (77, 4096, 200, 6), (300, 4096, 64, 8),
-                                     (513, 1344, 128, 1)])
+                                     (513, 1344, 128, 1), (9001, 256, 128, 8), (16383, 192, 256, 4)])
 def test_route_small_batch_widths(T, d, E, K):
     # Small batches route in one launch after the logits GEMM, the weight
     # rows streaming through LDS in 128-column chunks (d = 1344 ends on a
     # 64-column chunk); up to d = 4096 the x rows and three chunk buffers
-    # share the LDS. Bit-exact against the oracle and the all-exact path.
+    # share the LDS. From 8192 tokens the logits GEMM runs unsplit, and 16383
+    # is the largest batch on this path. Bit-exact against the oracle and the
+    # all-exact path.
     from workloads import bf16_bits_to_f32, f32_to_bf16_bits
 
     rng = np.random.default_rng(T * 7 + d + E + K)
