@@ -153,13 +153,15 @@ static bool fast_router(const moe_desc_t& d) { return d.dtype == MOE_BF16 && !(d
 static int router_bm(const moe_desc_t& d) { return (int64_t)d.T * router_ld(d) >= (int64_t)200 * 65536 ? 256 : 64; }
 
 // K split of the fast router's logits GEMM. Small batches have too few
-// 64-row tiles to occupy the chip (17 x 4 for one image against 256 CUs), so
-// the d / 64 K slabs are split over up to 8 parts of at least two slabs, each
+// 64-row tiles to occupy the chip (17 x 2 for one image against 256 CUs), so
+// the d / 64 K slabs are split over up to 4 parts of at least two slabs, each
 // writing its own partial logits; the candidate kernel adds them in order.
+// (8 parts: one image's route 29 -> 31 us, the repair reading twice the
+// partial logits.)
 static int32_t router_splits(const moe_desc_t& d) {
     if (!fast_router(d) || router_bm(d) != 64 || d.T >= 8192) return 1;
     const int nk = d.d / 64;
-    for (int p = 8; p >= 2; p /= 2)
+    for (int p = 4; p >= 2; p /= 2)
         if (nk % p == 0 && nk / p >= 2) return p;
     return 1;
 }
