@@ -92,6 +92,43 @@ def test_route_small_batch_widths(T, d, E, K):
         assert np.array_equal(host(gate), ref_gate), flags
 
 
+def _route_case(rng):
+    T = int(rng.choice([1, 2, 3, 5, 17, 64, 100, 257, 513, 1025, 2047, 3000, 8200, 12000]))
+    d = int(rng.choice([64, 128, 192, 320, 512, 768, 1024, 1344, 1536, 2048]))
+    E = int(rng.integers(1, 257))
+    K = int(rng.integers(1, min(E, 8) + 1))
+    T = max(1, min(T, int(1.5e8 / (d * E))))  # the oracle's work per case
+    dup = int(rng.choice([1, 1, 1, 2, 4, 16])) if E >= 16 else 1  # groups of identical rows tie exactly
+    return T, d, E, K, dup
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_route_random_small_batches(seed):
+    # Seeded random shapes of the small-batch router (one launch after the
+    # logits GEMM; overflowing tokens routed in full by their block): widths
+    # 64 to 2048, E 1 to 256, K up to 8, some experts in groups of identical
+    # rows, with and without a bias. Bit-exact against the oracle.
+    from workloads import bf16_bits_to_f32, f32_to_bf16_bits
+
+    rng = np.random.default_rng(5000 + seed)
+    T, d, E, K, dup = _route_case(rng)
+    x = f32_to_bf16_bits(rng.standard_normal((T, d)).astype(np.float32))
+    scale = float(rng.choice([0.01, 0.05]))
+    base = f32_to_bf16_bits((rng.standard_normal(((E + dup - 1) // dup, d)) * scale).astype(np.float32))
+    wr = np.repeat(base, dup, axis=0)[:E].copy()
+    bias = rng.uniform(-0.03, 0.03, E).astype(np.float32) if rng.random() < 0.7 else None
+    ref_idx, ref_gate = oracle.route(bf16_bits_to_f32(x), bf16_bits_to_f32(wr),
+                                     bias if bias is not None else np.zeros(E, np.float32), K)
+    desc = binding.make_desc(T, d, E, K, 64)
+    ws = binding.alloc_workspace(desc)
+    idx = torch.empty(T, K, dtype=torch.int32, device="cuda")
+    gate = torch.empty(T, K, dtype=torch.float32, device="cuda")
+    binding.moe_route(desc, dev(x), dev(wr), dev(bias) if bias is not None else None, idx, gate, ws)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(idx), ref_idx), (T, d, E, K, dup)
+    assert np.array_equal(host(gate), ref_gate), (T, d, E, K, dup)
+
+
 @pytest.mark.parametrize("dup", [1, 16, 128])
 def test_route_near_ties_take_exact_fallback(dup):
     # Groups of `dup` identical router rows tie exactly for every token; with
