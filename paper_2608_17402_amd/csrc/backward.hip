@@ -176,56 +176,74 @@ __global__ __launch_bounds__(256) void k_wgrad_reduce(const float* __restrict__ 
 // in: [rows, C] bf16; out: [C, ld] bf16 stored slab-major, [ld / 64][C][64]
 // (element (c, q) at ((q / 64) C + c) 64 + q % 64), so that one 64-column K
 // slab of a product's operand tile is contiguous. C a multiple of 64.
-// Positions past koff[E] are left alone. A workgroup moves 64 positions x CW
-// columns: gathered rows are read in CW * 2-byte runs.
-template <int CW>
+// Positions past koff[E] are left alone.
+//
+// A workgroup moves one 64-position block across all C columns. Windows are
+// multiples of 64, so the block lies in one expert's window: one search per
+// workgroup. Lane (rg, cg) of a wave holds an 8 x 8 block, positions 8 rg ..
+// 8 rg + 7 and 8 columns: it loads 8 16-byte row pieces, transposes them in
+// registers and stores 8 16-byte column pieces. The 8 lanes of one cg cover a
+// whole 128-byte line both ways: 8 rows' 8 columns in, one column's 64
+// positions out. The 4 waves take 64-column quarters of each 256-column step.
+__device__ __forceinline__ uint32_t pair16(uint32_t a, uint32_t b, bool high) {
+    return high ? (a >> 16) | (b & 0xFFFF0000u) : (a & 0xFFFFu) | (b << 16);
+}
+__device__ __forceinline__ uint32_t word_of(const uint4& v, int w) {
+    return w == 0 ? v.x : (w == 1 ? v.y : (w == 2 ? v.z : v.w));
+}
+
 __global__ __launch_bounds__(256) void k_transpose_window(const bf16_t* __restrict__ in, int C, int mode,
                                                          const int32_t* __restrict__ row_map, int K,
                                                          const int32_t* __restrict__ offsets,
                                                          const int32_t* __restrict__ koff, int E,
                                                          bf16_t* __restrict__ out) {
-    __shared__ bf16_t tile[TT][CW + 2];
-    __shared__ int32_t srow[TT];
-    const int q0 = blockIdx.x * TT, c0 = blockIdx.y * CW;
+    const int q0 = blockIdx.x * TT;
     const int total = koff[E];
     if (q0 >= total) return;  // uniform per workgroup
-    const int tid = threadIdx.x;
-    if (tid < TT) {
-        const int q = q0 + tid;
+    int lo = 0, hi = E - 1;   // last expert with koff[e] <= q0
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) / 2;
+        if (koff[mid] <= q0) lo = mid;
+        else hi = mid - 1;
+    }
+    const int base = offsets[lo], count = offsets[lo + 1] - base;
+    const int i0 = q0 - koff[lo];
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    const int rg = lane & 7, cg = lane >> 3;
+    // Source rows of the lane's 8 positions (-1: padding, zeros).
+    int srow[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const int i = i0 + rg * 8 + j;
         int v = -1;
-        if (q < total) {
-            int lo = 0, hi = E - 1;  // last expert with koff[e] <= q
-            while (lo < hi) {
-                const int mid = (lo + hi + 1) / 2;
-                if (koff[mid] <= q) lo = mid;
-                else hi = mid - 1;
-            }
-            const int i = q - koff[lo];
-            if (i < offsets[lo + 1] - offsets[lo]) {
-                const int p = offsets[lo] + i;
-                v = mode == SRC_SORTED ? p : (mode == SRC_SLOT ? row_map[p] : row_map[p] / K);
-            }
+        if (i < count) {
+            const int p = base + i;
+            v = mode == SRC_SORTED ? p : (mode == SRC_SLOT ? row_map[p] : row_map[p] / K);
         }
-        srow[tid] = v;
+        srow[j] = v;
     }
-    __syncthreads();
-    for (int t = tid; t < TT * CW / 8; t += 256) {
-        const int r = t / (CW / 8), c = (t % (CW / 8)) * 8;
-        uint4 v = make_uint4(0u, 0u, 0u, 0u);
-        if (srow[r] >= 0) v = *reinterpret_cast<const uint4*>(in + (size_t)srow[r] * C + c0 + c);
-        const bf16_t* e = reinterpret_cast<const bf16_t*>(&v);
+    bf16_t* const ob = out + (size_t)(q0 / TT) * C * TT + rg * 8;
+    for (int c = wave * 64 + cg * 8; c < C; c += 256) {
+        // Padding positions load row 0 (T >= 1, so it exists) and keep zeros:
+        // no branch, so all 8 loads are in flight together.
+        uint4 v[8];
 #pragma unroll
-        for (int k = 0; k < 8; ++k) tile[r][c + k] = e[k];
-    }
-    __syncthreads();
-    // total is a multiple of 64 and q0 < total: the whole tile is inside.
-    for (int t = tid; t < TT * CW / 8; t += 256) {
-        const int c = t / (TT / 8), r = (t % (TT / 8)) * 8;
-        uint4 v;
-        bf16_t* e = reinterpret_cast<bf16_t*>(&v);
+        for (int j = 0; j < 8; ++j) {
+            const uint4 t = *reinterpret_cast<const uint4*>(in + (size_t)(srow[j] < 0 ? 0 : srow[j]) * C + c);
+            v[j] = srow[j] >= 0 ? t : make_uint4(0u, 0u, 0u, 0u);
+        }
+        // Column k of the block: element k of each row, rows in pairs per word.
 #pragma unroll
-        for (int k = 0; k < 8; ++k) e[k] = tile[r + k][c];
-        store16_nt(out + ((size_t)(q0 / TT) * C + c0 + c) * TT + r, v);
+        for (int k = 0; k < 8; ++k) {
+            const int w = k >> 1;
+            const bool high = k & 1;
+            uint4 o;
+            o.x = pair16(word_of(v[0], w), word_of(v[1], w), high);
+            o.y = pair16(word_of(v[2], w), word_of(v[3], w), high);
+            o.z = pair16(word_of(v[4], w), word_of(v[5], w), high);
+            o.w = pair16(word_of(v[6], w), word_of(v[7], w), high);
+            store16_nt(ob + (size_t)(c + k) * TT, o);
+        }
     }
 }
 
@@ -323,14 +341,8 @@ hipError_t launch_wgrad_reduce(const float* partials, const TileDesc* rlist, con
 hipError_t launch_transpose_window(const void* in, int C, int mode, const int32_t* row_map, int K,
                                    const int32_t* offsets, const int32_t* koff, int E, void* out, int ld,
                                    hipStream_t s) {
-    if (C % 256 == 0)
-        hipLaunchKernelGGL(k_transpose_window<256>, dim3(ld / TT, C / 256), dim3(256), 0, s,
-                           static_cast<const bf16_t*>(in), C, mode, row_map, K, offsets, koff, E,
-                           static_cast<bf16_t*>(out));
-    else
-        hipLaunchKernelGGL(k_transpose_window<TT>, dim3(ld / TT, C / TT), dim3(256), 0, s,
-                           static_cast<const bf16_t*>(in), C, mode, row_map, K, offsets, koff, E,
-                           static_cast<bf16_t*>(out));
+    hipLaunchKernelGGL(k_transpose_window, dim3(ld / TT), dim3(256), 0, s, static_cast<const bf16_t*>(in), C, mode,
+                       row_map, K, offsets, koff, E, static_cast<bf16_t*>(out));
     return hipGetLastError();
 }
 
