@@ -149,24 +149,28 @@ __global__ __launch_bounds__(1024) void k_wgrad_plan(const int32_t* __restrict__
 }
 
 // Gradients of the split experts: out[e] = sum of its partial blocks in
-// order (fp32), four elements per thread. blockIdx.y = split expert.
+// order (fp32), four elements per thread. The split experts (their number is
+// known on the device only) are dealt to the gridDim.y rows of workgroups in
+// turn, so that the grid does not hold a row per expert that mostly exits.
 __global__ __launch_bounds__(256) void k_wgrad_reduce(const float* __restrict__ partials,
                                                      const TileDesc* __restrict__ rlist,
                                                      const int32_t* __restrict__ wcount, size_t mn,
                                                      float* __restrict__ out) {
-    if ((int)blockIdx.y >= wcount[1]) return;
-    const TileDesc r = rlist[blockIdx.y];
     const size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
     if (i >= mn) return;
-    float4 acc = *reinterpret_cast<const float4*>(partials + (size_t)r.row0 * mn + i);
-    for (int c = 1; c < r.rows; ++c) {
-        const float4 v = *reinterpret_cast<const float4*>(partials + ((size_t)r.row0 + c) * mn + i);
-        acc.x += v.x;
-        acc.y += v.y;
-        acc.z += v.z;
-        acc.w += v.w;
+    const int nsplit = wcount[1];
+    for (int y = blockIdx.y; y < nsplit; y += gridDim.y) {
+        const TileDesc r = rlist[y];
+        float4 acc = *reinterpret_cast<const float4*>(partials + (size_t)r.row0 * mn + i);
+        for (int c = 1; c < r.rows; ++c) {
+            const float4 v = *reinterpret_cast<const float4*>(partials + ((size_t)r.row0 + c) * mn + i);
+            acc.x += v.x;
+            acc.y += v.y;
+            acc.z += v.z;
+            acc.w += v.w;
+        }
+        *reinterpret_cast<float4*>(out + (size_t)r.e * mn + i) = acc;
     }
-    *reinterpret_cast<float4*>(out + (size_t)r.e * mn + i) = acc;
 }
 
 // Transposing gather into the K windows: out[c][q] for window position q of
@@ -333,8 +337,8 @@ hipError_t launch_wgrad_plan(const int32_t* offsets, int E, int32_t* koff, TileD
 hipError_t launch_wgrad_reduce(const float* partials, const TileDesc* rlist, const int32_t* wcount, int E,
                                size_t mn, float* out, hipStream_t s) {
     const size_t blocks = (mn / 4 + 255) / 256;
-    hipLaunchKernelGGL(k_wgrad_reduce, dim3((unsigned)blocks, (unsigned)E), dim3(256), 0, s, partials, rlist, wcount,
-                       mn, out);
+    hipLaunchKernelGGL(k_wgrad_reduce, dim3((unsigned)blocks, (unsigned)(E < 8 ? E : 8)), dim3(256), 0, s, partials,
+                       rlist, wcount, mn, out);
     return hipGetLastError();
 }
 
