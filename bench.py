@@ -54,18 +54,33 @@ TRAFFIC_SOURCES = ("paper_2608_17402_amd/csrc/gemm.hip", "paper_2608_17402_amd/c
                    "workloads/configs.py", "workloads/generate.py", "tests/golden/vitg_skew_bias_seed0.txt")
 
 
-def gemm_source_hash():
+# HBM bytes of one expert-MLP backward call (all its kernels), from the same
+# two counters and scale factors, taken with `bench.py --mode backward`; they
+# hold for the sources whose hash is BACKWARD_TRAFFIC_SOURCE_HASH (those of
+# the forward pair and backward.hip).
+BACKWARD_TRAFFIC_SOURCE_HASH = "865c96a4296c9d79"
+BACKWARD_TRAFFIC_BYTES = {"vitg_skew_bf16": 41302785542, "vith_swiglu_bf16": 47960849723}
+BACKWARD_TRAFFIC_SOURCES = TRAFFIC_SOURCES + ("paper_2608_17402_amd/csrc/backward.hip",)
+
+
+def source_hash(files):
     import hashlib
 
     m = hashlib.sha256()
-    for f in TRAFFIC_SOURCES:
+    for f in files:
         with open(os.path.join(ROOT, f), "rb") as fh:
             m.update(fh.read())
     return m.hexdigest()[:16]
 
 
+def backward_traffic_bytes(workload):
+    if source_hash(BACKWARD_TRAFFIC_SOURCES) != BACKWARD_TRAFFIC_SOURCE_HASH:
+        return None
+    return BACKWARD_TRAFFIC_BYTES.get(workload)
+
+
 def traffic_bytes(workload):
-    if gemm_source_hash() != TRAFFIC_SOURCE_HASH:
+    if source_hash(TRAFFIC_SOURCES) != TRAFFIC_SOURCE_HASH:
         return None
     return TRAFFIC_BYTES.get(workload)
 
@@ -110,14 +125,40 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=15.0,
                    help="target CPU time of the oracle sample")
     p.add_argument("--stage-reps", type=int, default=10)
-    p.add_argument("--mode", choices=("layer", "gemm", "stages", "dense", "copy"), default="layer",
+    p.add_argument("--mode", choices=("layer", "gemm", "stages", "backward", "dense", "copy"), default="layer",
                    help="layer: the benchmark; gemm: only the routed grouped GEMMs of --config, repeated "
                         "(hardware-counter runs); stages: route, permute and combine of --config, repeated "
+                        "(hardware-counter runs); backward: the expert-MLP backward of --config, repeated "
                         "(hardware-counter runs); dense: hipBLASLt (torch) dense bf16 GEMMs of the routed "
                         "GEMMs' total shapes, repeated (hardware-counter runs); copy: a plain device copy of "
                         "--copy-mib MiB (calibration of the byte counters)")
     p.add_argument("--copy-mib", type=int, default=1024)
     return p.parse_args()
+
+
+def backward_call(c, L):
+    """The expert-MLP backward call on layer L's own routing, with a seeded
+    output gradient, and its flop count: fc1 again (SwiGLU: two products), dA,
+    dx (SwiGLU: K = 2h), dW2 and dW1 (SwiGLU: two), 2 T K d h each."""
+    import torch
+
+    from paper_2608_17402_amd import binding
+
+    T, K, E, d, h = c.T, c.K, c.E, c.d, c.h
+    L.forward()
+    binding.moe_permute(L.desc, L.idx, L.counts, L.offsets, L.slots, L.ws)
+    bws = binding.alloc_backward_workspace(L.desc)
+    gen = torch.Generator(device="cuda").manual_seed(5)
+    gout = (torch.randn(T * K, d, device="cuda", generator=gen) * 0.5).to(torch.bfloat16)
+    dx = torch.empty(T, d, dtype=torch.bfloat16, device="cuda")
+    dw1 = torch.empty(E, L.w1.shape[1], d, dtype=torch.float32, device="cuda")
+    dw2 = torch.empty(E, d, L.w2.shape[2], dtype=torch.float32, device="cuda")
+
+    def bwd():
+        binding.moe_grouped_mlp_backward(L.desc, L.x, L.slots, L.offsets, L.w1, L.w2, gout, dx, dw1, dw2, bws)
+
+    fl = (8.0 if c.act == "swiglu" else 5.0) * 2.0 * T * K * d * h
+    return bwd, fl
 
 
 def main():
@@ -258,6 +299,16 @@ def main():
                 st[name]()
         torch.cuda.synchronize()
         print(json.dumps({"mode": "stages", "workload": cfg.name, "launches_per_stage": args.steps}), flush=True)
+        return
+
+    if args.mode == "backward":
+        # The expert-MLP backward alone, repeated, for the counter passes.
+        bwd, _ = backward_call(cfg, lay)
+        for _ in range(args.warmup + args.steps):
+            bwd()
+        torch.cuda.synchronize()
+        print(json.dumps({"mode": "backward", "workload": cfg.name, "calls": args.warmup + args.steps}),
+              flush=True)
         return
 
     if args.mode == "gemm":
@@ -422,32 +473,17 @@ def main():
     def backward_line(c, L):
         """Expert-MLP backward on layer L's own routing: five products of
         2 T K d h (SwiGLU: the gate/up products count twice) flop."""
-        T, K, E, d, h = c.T, c.K, c.E, c.d, c.h
-        sw = c.act == "swiglu"
-        L.forward()
-        binding.moe_permute(L.desc, L.idx, L.counts, L.offsets, L.slots, L.ws)
-        bws = binding.alloc_backward_workspace(L.desc)
-        gen = torch.Generator(device="cuda").manual_seed(5)
-        gout = (torch.randn(T * K, d, device="cuda", generator=gen) * 0.5).to(torch.bfloat16)
-        dx = torch.empty(T, d, dtype=torch.bfloat16, device="cuda")
-        dw1 = torch.empty(E, L.w1.shape[1], d, dtype=torch.float32, device="cuda")
-        dw2 = torch.empty(E, d, L.w2.shape[2], dtype=torch.float32, device="cuda")
-
-        def bwd():
-            binding.moe_grouped_mlp_backward(L.desc, L.x, L.slots, L.offsets, L.w1, L.w2, gout, dx, dw1, dw2, bws)
-
+        bwd, fl = backward_call(c, L)
         for _ in range(2):
             bwd()
         b_ms = time_calls(bwd, max(3, args.steps // 2))
-        # fc1 again (SwiGLU: two), dA, dx (SwiGLU: K = 2h), dW2, dW1 (SwiGLU: two)
-        fl = (8.0 if sw else 5.0) * 2.0 * T * K * d * h
         tf = fl / (b_ms * 1e-3) / 1e12
         return {
             "workload": c.name, "act": c.act, "entry": "moe_grouped_mlp_backward", "us": round(b_ms * 1e3, 1),
-            "tokens_per_s": round(T / (b_ms * 1e-3), 1),
+            "tokens_per_s": round(c.T / (b_ms * 1e-3), 1),
             "roofline": {"kernel": "expert-MLP backward: fc1 again, dA, dx, dW2, dW1 products plus transposes",
                          "bound": "mfma", "achieved": round(tf, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                         "frac": round(tf / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                         "frac": round(tf / PEAK_BF16_TFLOPS, 4), "traffic": backward_traffic_bytes(c.name),
                          "algorithmic_flops_per_launch": fl, "avg_launch_us": round(b_ms * 1e3, 2)},
         }
 
