@@ -108,8 +108,8 @@ def stage_gbs(c, stages_ms):
 def parse():
     p = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=20)
-    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--steps", type=int, default=1000)
+    p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--config", default="vitg_skew_bf16")
     p.add_argument("--single-image-config", default="single_image_bf16")
     p.add_argument("--no-single-image", action="store_true")
@@ -346,7 +346,7 @@ def main():
     gemm_ms = sum(hev.elapsed_ms(3 * i, 3 * i + 2) for i in range(args.steps)) / args.steps
     hev.close()
     # The fc1 / fc2 split, from a pass with the middle event as well.
-    fc1_ms, fc2_ms = split_fc1_fc2(lay, args.steps)
+    fc1_ms, fc2_ms = split_fc1_fc2(lay, min(args.steps, 100))
 
     # Per-stage times (the stage entry points run the same kernels).
     stages_ms = {k: time_calls(f, args.stage_reps) for k, f in lay.stages().items()}
@@ -476,7 +476,7 @@ def main():
         bwd, fl = backward_call(c, L)
         for _ in range(2):
             bwd()
-        b_ms = time_calls(bwd, max(3, args.steps // 2))
+        b_ms = time_calls(bwd, max(3, min(args.steps // 2, 10)))
         tf = fl / (b_ms * 1e-3) / 1e12
         return {
             "workload": c.name, "act": c.act, "entry": "moe_grouped_mlp_backward", "us": round(b_ms * 1e3, 1),
@@ -519,12 +519,14 @@ def main():
     if not args.no_dense_reference and cfg.dtype == "bf16":
         out["dense_reference"] = dense_reference(cfg, achieved)
 
+    # The lines beside the main workload: 20 to 50 timed layers each.
+    sec_reps = min(max(args.steps, 20), 50)
     mf_names = [n for n in args.mfma_configs.split(",") if n]
     if mf_names:
         out["mfma_layers"] = {}
         for name in mf_names:
             c = get_config(name)
-            L, l_ms, pair, f1, f2 = measure(c, max(args.steps, 20))
+            L, l_ms, pair, f1, f2 = measure(c, sec_reps)
             line = mfma_line(c, l_ms, pair, f1, f2)
             st_ms = {k: time_calls(f, args.stage_reps) for k, f in L.stages().items()}
             line["stages_us"] = {k: round(v * 1e3, 1) for k, v in st_ms.items()}
@@ -534,7 +536,7 @@ def main():
 
     if not args.no_single_image:
         c5 = get_config(args.single_image_config)
-        reps = max(args.steps, 20)
+        reps = sec_reps
         si, si_ms, pair, f1, f2 = measure(c5, reps)
         si_stages = {k: time_calls(f, max(args.stage_reps, 20)) for k, f in si.stages().items()}
         out["single_image"] = hbm_line(c5, si, si_ms, pair, f1, f2)
@@ -549,7 +551,7 @@ def main():
         out["swiglu"] = {}
         for name in sw_names:
             c = get_config(name)
-            L, l_ms, pair, f1, f2 = measure(c, max(args.steps, 20))
+            L, l_ms, pair, f1, f2 = measure(c, sec_reps)
             # ~32 rows per expert is weight-read bound; large batches are MFMA bound.
             weight_bound = c.T * c.K / c.E < 256
             out["swiglu"][name] = (hbm_line(c, L, l_ms, pair, f1, f2) if weight_bound
