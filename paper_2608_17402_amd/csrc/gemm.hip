@@ -1297,26 +1297,30 @@ void k_gemm_pp(const GemmArgs a) {
         const int wlen = a.koff[e + 1] - a.koff[e];
         const int vrows = t.rows - (wm * WT + i * 32);  // rows of the block that exist
         uint8_t* const ct = static_cast<uint8_t*>(a.CT);
-        // Piece k of a lane: staged column cc = (lane + 64 k) / 4, rows
-        // 8 rg .. 8 rg + 7 with rg = lane % 4, one zero-extended 16-bit read
-        // per row (a read into half of a register would merge with that
-        // register as it was when issued, not with a read still in flight).
-        // Two pieces in flight: the reads of piece k + 1 are issued before
-        // piece k is stored.
-        const int nit = ncc * 4 / kWave;
+        // Piece k of a lane: staged column cc = 16 k + lane % 16, rows 8 g ..
+        // 8 g + 7 with g = lane / 16, as two transposing 8-byte reads, the even
+        // rows 8 g, 8 g + 2, .. and the odd rows 8 g + 1, 8 g + 3, ..: in each
+        // read the 16 lanes of a quarter-wave name 4 rows x 16 columns (lane r:
+        // row r / 4 of the four, columns 4 (r % 4) ..) and each receives its
+        // column's 4 rows, which are then interleaved into the row order the
+        // window stores. Rows two apart keep the 16-byte pieces a quarter-wave
+        // reads in distinct banks under the staging swizzle. Two pieces in
+        // flight: the reads of piece k + 1 are issued before piece k is stored.
+        const int nit = ncc / 16;
         // The lane index through an opaque copy: the per-piece addresses are
-        // then computed here instead of being hoisted out of the tile loop
-        // (64 live registers).
+        // then computed here instead of being hoisted out of the tile loop.
         int ln = lane;
         asm volatile("" : "+v"(ln));
-        const int rg = ln & 3;
-        uint32_t w[2][8];
-        auto issue = [&](int k, uint32_t(&dst)[8]) {
-            const int cc = (ln + kWave * k) >> 2;
-            const uint32_t b = stg + (uint32_t)(rg * 8) * 256u + (uint32_t)(cc & 7) * 2u;
+        const int g = ln >> 4, c16 = ln & 15;
+        u32x2_t w[2][2];
+        auto issue = [&](int k, u32x2_t(&dst)[2]) {
+            const int col = 16 * k + 4 * (c16 & 3);
 #pragma unroll
-            for (int u = 0; u < 8; ++u)
-                lds_read_u16_asm(dst[u], b + (uint32_t)u * 256u + ((uint32_t)((cc >> 3) ^ ((rg * 8 + u) & 15)) << 4));
+            for (int hh = 0; hh < 2; ++hh) {
+                const int row = 8 * g + hh + 2 * (c16 >> 2);
+                lds_read_tr8_asm(dst[hh], stg + (uint32_t)row * 256u +
+                                              ((uint32_t)((col >> 3) ^ (row & 15)) << 4) + (uint32_t)(col & 7) * 2u);
+            }
         };
         issue(0, w[0]);
 #pragma unroll
@@ -1324,25 +1328,25 @@ void k_gemm_pp(const GemmArgs a) {
             __builtin_amdgcn_sched_barrier(0);
             if (k + 1 < nit) {
                 issue(k + 1, w[(k + 1) & 1]);
-                wait_lgkmcnt<8>();
+                wait_lgkmcnt<2>();
             } else {
                 wait_lgkmcnt0();
             }
-#pragma unroll
-            for (int u = 0; u < 8; ++u) tie(w[k & 1][u]);
-            const int cc = (ln + kWave * k) >> 2;
-            const int orow = colmap(cc);
-            if (orow < 0 || gpos + rg * 8 >= wlen) continue;
-            uint32_t* const r16 = w[k & 1];
+            tie(w[k & 1][0]);
+            tie(w[k & 1][1]);
+            const int orow = colmap(16 * k + c16);
+            if (orow < 0 || gpos + g * 8 >= wlen) continue;
+            const u32x2_t ev = w[k & 1][0], od = w[k & 1][1];  // rows 0, 2, 4, 6 and 1, 3, 5, 7 of the piece
+            u32x4_t v = {(ev.x & 0xffffu) | (od.x << 16), (ev.x >> 16) | (od.x & 0xffff0000u),
+                         (ev.y & 0xffffu) | (od.y << 16), (ev.y >> 16) | (od.y & 0xffff0000u)};
             if (vrows < 32) {  // the expert's last rows: zeros past them
 #pragma unroll
-                for (int u = 0; u < 8; ++u)
-                    if (rg * 8 + u >= vrows) r16[u] = 0u;
+                for (int u = 0; u < 4; ++u) {
+                    if (g * 8 + 2 * u >= vrows) v[u] &= 0xffff0000u;
+                    if (g * 8 + 2 * u + 1 >= vrows) v[u] &= 0x0000ffffu;
+                }
             }
-            u32x4_t v;
-#pragma unroll
-            for (int u = 0; u < 4; ++u) v[u] = r16[2 * u] | (r16[2 * u + 1] << 16);
-            const int q = wq + rg * 8;
+            const int q = wq + g * 8;
             store16_asm(ct + (((size_t)(q / 64) * a.ct_cols + orow) * 64 + q % 64) * 2, v);
         }
     };

@@ -158,6 +158,15 @@ __device__ __forceinline__ void lds_read_u16_asm(uint32_t& r, uint32_t addr) {
     asm volatile("ds_read_u16 %0, %1" : "=v"(r) : "v"(addr));
 }
 __device__ __forceinline__ void tie(uint32_t& v) { asm volatile("" : "+v"(v)); }
+// Transposing 8-byte LDS read (ds_read_b64_tr_b16, CDNA4). Within each group
+// of 16 lanes, lane r names 4 consecutive 16-bit values M[r][0..3]; lane i
+// receives M[i / 4 + 4 j][i % 4] as its 16-bit element j (j = 0..3). With
+// lane r pointing at row r / 4 and columns 4 (r % 4) .. of a 4 x 16 block,
+// lane i gets column i of the 4 rows, row j in element j.
+__device__ __forceinline__ void lds_read_tr8_asm(u32x2_t& r, uint32_t addr) {
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(r) : "v"(addr));
+}
+__device__ __forceinline__ void tie(u32x2_t& v) { asm volatile("" : "+v"(v)); }
 // One accumulator moved to a vector register at this point of the program
 // (volatile: not hoisted, so only one staged block's values are live at once).
 __device__ __forceinline__ float acc_read(float x) {
