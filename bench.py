@@ -40,10 +40,10 @@ PEAK_HBM_GBS = 8000.0
 # commands and raw figures. The figures hold for the GEMM sources whose hash is
 # TRAFFIC_SOURCE_HASH: once those change, traffic is reported as null until
 # the counters are taken again.
-TRAFFIC_SOURCE_HASH = "5da4740e29ab04de"
-TRAFFIC_BYTES = {"vitg_skew_bf16": 6943254514, "vitl_bf16": 3646827163, "vitb_bf16": 779556421,
-                 "single_image_bf16": 1275359248, "vith_swiglu_bf16": 6566746701,
-                 "single_image_swiglu_bf16": 1879507779}
+TRAFFIC_SOURCE_HASH = "35d87b3f8476f9ac"
+TRAFFIC_BYTES = {"vitg_skew_bf16": 6924223038, "vitl_bf16": 3643498711, "vitb_bf16": 779626301,
+                 "single_image_bf16": 1275359648, "vith_swiglu_bf16": 6605361156,
+                 "single_image_swiglu_bf16": 1879607968}
 
 
 # Every source that changes the GEMM pair's HBM bytes: the kernels, the tile
@@ -58,8 +58,8 @@ TRAFFIC_SOURCES = ("paper_2608_17402_amd/csrc/gemm.hip", "paper_2608_17402_amd/c
 # two counters and scale factors, taken with `bench.py --mode backward`; they
 # hold for the sources whose hash is BACKWARD_TRAFFIC_SOURCE_HASH (those of
 # the forward pair and backward.hip).
-BACKWARD_TRAFFIC_SOURCE_HASH = "865c96a4296c9d79"
-BACKWARD_TRAFFIC_BYTES = {"vitg_skew_bf16": 41302785542, "vith_swiglu_bf16": 47960849723}
+BACKWARD_TRAFFIC_SOURCE_HASH = "10192b99fe832cc7"
+BACKWARD_TRAFFIC_BYTES = {"vitg_skew_bf16": 41177098056, "vith_swiglu_bf16": 47912615423}
 BACKWARD_TRAFFIC_SOURCES = TRAFFIC_SOURCES + ("paper_2608_17402_amd/csrc/backward.hip",)
 
 
